@@ -1,0 +1,243 @@
+"""Pins that tie the CPU oracle to facts fixed outside it.
+
+Each check takes an oracle library handle (the built oracle, or a mutated
+build in the mutation test) and raises AssertionError on a mismatch. None of
+them re-calls the oracle's own formula: they use exact integer arithmetic,
+scipy's cdist, the expanded form of Eq. (1) through a matrix product, a
+pure-Python node-major loop, and closed forms for planted and constant
+codebooks.
+"""
+from __future__ import annotations
+
+import numpy as np
+from scipy.spatial.distance import cdist
+
+import oracle
+import synth
+
+
+def dense_x(row_ptr, col_idx, V):
+    N = row_ptr.shape[0] - 1
+    X = np.zeros((N, V), dtype=np.int64)
+    for s in range(N):
+        X[s, col_idx[row_ptr[s]:row_ptr[s + 1]]] = 1
+    return X
+
+
+def small_case(seed=5, N=48, V=300, M=40, kind=synth.QUANTISED):
+    rp, ci = synth.make_csr(seed, N, V)
+    W = synth.codebook(seed, kind, V, M)
+    return rp, ci, W
+
+
+def first_min_and_second(D):
+    """Lowest-index argmin per row and the smallest value over the other columns."""
+    b = np.argmin(D, axis=1)  # numpy returns the first occurrence
+    masked = D.astype(np.float64).copy()
+    masked[np.arange(D.shape[0]), b] = np.inf
+    return b, masked.min(axis=1)
+
+
+# ---------------------------------------------------------------- the checks
+
+def check_exact_integer_direct(lib):
+    """Quantised k/256 codebook: 65536*D_i = sum_v (256 x_v - k_{v,i})^2 exactly, in int64."""
+    rp, ci, W = small_case()
+    K = np.rint(W * 256).astype(np.int64)
+    X = dense_x(rp, ci, W.shape[0])
+    Dint = ((256 * X[:, :, None] - K[None, :, :]) ** 2).sum(axis=1)  # N x M, exact
+    b_ref, d2_ref = first_min_and_second(Dint)
+    b, d, d2 = oracle.bmu(W, rp, ci, lib=lib)
+    assert np.array_equal(b, b_ref), "argmin differs from the exact integer argmin"
+    assert np.array_equal(d * 65536.0, Dint[np.arange(len(b)), b_ref].astype(np.float64)), "distance not exact"
+    assert np.array_equal(d2 * 65536.0, d2_ref), "second-best distance not exact"
+
+
+def check_exact_integer_tiny(lib, n_samples=None):
+    """The full tiny workload (16x16 map, V=2000, k/256): indices and distances exact.
+
+    The integer reference uses the expanded identity in int64, which is exact
+    (no rounding), so it is an independent evaluation of the same integers.
+    """
+    cfg = synth.CONFIGS["tiny"]
+    rp, ci = synth.make_csr(cfg.seed, cfg.N, cfg.V)
+    if n_samples is not None:
+        rp = rp[: n_samples + 1]
+    W = synth.codebook(cfg.seed, cfg.kind, cfg.V, cfg.M)
+    K = np.rint(W * 256).astype(np.int64)
+    N = rp.shape[0] - 1
+    nnz = np.diff(rp).astype(np.int64)
+    XK = np.zeros((N, cfg.M), dtype=np.int64)
+    for s in range(N):
+        XK[s] = K[ci[rp[s]:rp[s + 1]]].sum(axis=0)
+    Dint = 65536 * nnz[:, None] - 512 * XK + (K * K).sum(axis=0)[None, :]
+    b_ref, d2_ref = first_min_and_second(Dint)
+    b, d, d2 = oracle.bmu(W, rp, ci, lib=lib)
+    assert np.array_equal(b, b_ref)
+    assert np.array_equal(d * 65536.0, Dint[np.arange(N), b_ref].astype(np.float64))
+    assert np.array_equal(d2 * 65536.0, d2_ref)
+
+
+def check_cdist_node_major(lib):
+    """scipy's sqeuclidean distance on the node-major transpose agrees (continuous codebook)."""
+    rp, ci, W = small_case(seed=11, kind=synth.UNIFORM, M=57)
+    X = dense_x(rp, ci, W.shape[0]).astype(np.float64)
+    Wnm = np.ascontiguousarray(W.T).astype(np.float64)  # node-major: row i = prototype w_i
+    D = cdist(X, Wnm, "sqeuclidean")
+    b, d, d2 = oracle.bmu(W, rp, ci, lib=lib)
+    assert np.allclose(d, D[np.arange(len(b)), b], rtol=1e-12, atol=0)
+    srt = np.sort(D, axis=1)
+    assert np.allclose(d, srt[:, 0], rtol=1e-12, atol=0), "not the minimum distance"
+    assert np.allclose(d2, srt[:, 1], rtol=1e-12, atol=0), "not the second-smallest distance"
+
+
+def check_expanded_form(lib):
+    """Eq. (1): ||x - w||^2 = ||w||^2 - 2<x,w> + ||x||^2, evaluated by a matrix product."""
+    rp, ci, W = small_case(seed=12, kind=synth.UNIFORM, N=40, V=500, M=33)
+    X = dense_x(rp, ci, W.shape[0]).astype(np.float64)
+    W64 = W.astype(np.float64)
+    D = (W64 * W64).sum(axis=0)[None, :] - 2.0 * (X @ W64) + X.sum(axis=1)[:, None]
+    b, d, _ = oracle.bmu(W, rp, ci, lib=lib)
+    assert np.allclose(d, D.min(axis=1), rtol=1e-11, atol=1e-9)
+    assert np.allclose(d, D[np.arange(len(b)), b], rtol=1e-11, atol=1e-9)
+
+
+def check_node_major_python_loop(lib):
+    """A pure-Python node-major loop in ascending v gives bit-identical fp64 distances."""
+    rp, ci, W = small_case(seed=13, kind=synth.UNIFORM, N=6, V=37, M=9)
+    V, M = W.shape
+    Wnm = [[float(W[v, i]) for v in range(V)] for i in range(M)]
+    for s in range(rp.shape[0] - 1):
+        active = set(int(v) for v in ci[rp[s]:rp[s + 1]])
+        Ds = []
+        for i in range(M):
+            acc = 0.0
+            for v in range(V):
+                diff = (1.0 if v in active else 0.0) - Wnm[i][v]
+                acc += diff * diff
+            Ds.append(acc)
+        best = min(range(M), key=lambda i: (Ds[i], i))
+        b, d, _ = oracle.bmu(W, rp[s:s + 2], ci, lib=lib)
+        assert int(b[0]) == best and float(d[0]) == Ds[best]
+
+
+def check_planted_neuron(lib):
+    """A prototype equal to the input has distance 0 and wins."""
+    rp, ci, W = small_case(seed=14, kind=synth.UNIFORM, N=20, V=200, M=31)
+    W = W.copy()
+    for s, j in [(3, 17), (7, 0), (19, 30)]:
+        Wp = W.copy()
+        Wp[:, j] = 0.0
+        Wp[ci[rp[s]:rp[s + 1]], j] = 1.0
+        b, d, d2 = oracle.bmu(Wp, rp[s:s + 2], ci, lib=lib)
+        assert int(b[0]) == j and float(d[0]) == 0.0 and d2[0] > 0
+
+
+def check_constant_codebook(lib):
+    """All prototypes equal: every distance ties, the lowest index (0) wins, closed-form distance."""
+    rp, ci, W = small_case(seed=15, N=30, V=120, M=13)
+    c = 0.25
+    Wc = np.full_like(W, c)
+    b, d, d2 = oracle.bmu(Wc, rp, ci, lib=lib)
+    nnz = np.diff(rp).astype(np.float64)
+    closed = nnz * (1 - c) ** 2 + (W.shape[0] - nnz) * c ** 2
+    assert (b == 0).all()
+    assert np.array_equal(d, closed) and np.array_equal(d2, closed)
+
+
+def check_tie_lowest_index(lib):
+    """Two identical best prototypes far apart: the lower index wins."""
+    rp, ci, W = small_case(seed=16, kind=synth.UNIFORM, N=10, V=150, M=64)
+    s = 4
+    Wp = W.copy()
+    for j in (5, 61):
+        Wp[:, j] = 0.0
+        Wp[ci[rp[s]:rp[s + 1]], j] = 0.9
+    b, d, d2 = oracle.bmu(Wp, rp[s:s + 2], ci, lib=lib)
+    assert int(b[0]) == 5 and d2[0] == d[0]
+    # the same pair seen from a block that starts past the first copy
+    b2, _, _ = oracle.bmu(np.ascontiguousarray(Wp[:, 6:]), rp[s:s + 2], ci, i0=6, lib=lib)
+    assert int(b2[0]) == 61
+
+
+def check_single_neuron_and_empty_row(lib):
+    """M = 1 gives index 0 and an infinite second best; an empty row ranks by ||w||^2."""
+    rp, ci, W = small_case(seed=17, kind=synth.UNIFORM, N=8, V=90, M=21)
+    b, d, d2 = oracle.bmu(np.ascontiguousarray(W[:, 4:5]), rp, ci, i0=4, lib=lib)
+    assert (b == 4).all() and np.isinf(d2).all()
+    X = dense_x(rp, ci, W.shape[0]).astype(np.float64)
+    assert np.allclose(d, ((X - W[:, 4].astype(np.float64)[None, :]) ** 2).sum(axis=1), rtol=1e-13)
+    empty_rp = np.array([0, 0], dtype=np.int32)
+    b, d, _ = oracle.bmu(W, empty_rp, ci, lib=lib)
+    n = (W.astype(np.float64) ** 2).sum(axis=0)
+    assert int(b[0]) == int(np.argmin(n)) and np.isclose(d[0], n.min(), rtol=1e-13)
+
+
+def check_quantisation_error(lib):
+    """QE, the mean input-to-BMU distance (Background, quality measures), recomputed at the returned units."""
+    rp, ci, W = small_case(seed=18, kind=synth.UNIFORM, N=50, V=250, M=36)
+    X = dense_x(rp, ci, W.shape[0]).astype(np.float64)
+    b, d, _ = oracle.bmu(W, rp, ci, lib=lib)
+    D = cdist(X, W.T.astype(np.float64), "sqeuclidean")
+    qe_ref = D.min(axis=1).mean()
+    assert np.isclose(d.mean(), qe_ref, rtol=1e-12)
+    assert np.isclose(np.mean(D[np.arange(len(b)), b]), qe_ref, rtol=1e-12)
+
+
+def check_offset_rows_and_blocks(lib):
+    """A batch slice (row_ptr not starting at 0) and a streamed, merged run equal one whole call."""
+    rp, ci, W = small_case(seed=19, kind=synth.UNIFORM, N=30, V=160, M=50)
+    whole = oracle.bmu(W, rp, ci, lib=lib)
+    sl = oracle.bmu(W, rp[10:21], ci, lib=lib)
+    for a, bb in zip(sl, whole):
+        assert np.array_equal(a, bb[10:20])
+    streamed = oracle.bmu_streamed(lambda i0, i1: np.ascontiguousarray(W[:, i0:i1]), W.shape[1], rp, ci,
+                                   block=7, nthreads=3, lib=lib)
+    for a, bb in zip(streamed, whole):
+        assert np.array_equal(a, bb)
+
+
+def check_norms(lib):
+    """Per-neuron squared norms: exact for k/256 weights, fp64-close otherwise."""
+    _, _, Wq = small_case(seed=20, V=700, M=29)
+    n = oracle.norms(Wq, lib=lib)
+    K = np.rint(Wq * 256).astype(np.int64)
+    assert np.array_equal(n * 65536.0, (K * K).sum(axis=0).astype(np.float64))
+    _, _, Wu = small_case(seed=21, kind=synth.UNIFORM, V=700, M=29)
+    assert np.allclose(oracle.norms(Wu, lib=lib), (Wu.astype(np.float64) ** 2).sum(axis=0), rtol=1e-14)
+
+
+def check_error_codes(lib):
+    """Invalid CSR and bad shapes are rejected with the documented codes."""
+    W = np.zeros((5, 3), dtype=np.float32)
+    out = np.zeros(4, dtype=np.float64)
+    ob = np.zeros(4, dtype=np.int32)
+    f = lib.som_bmu_oracle_host
+    rp = np.array([0, 2], dtype=np.int32)
+    bad_id = np.array([1, 5], dtype=np.int32)
+    assert f(W.ctypes.data, 3, 5, 0, 3, rp.ctypes.data, bad_id.ctypes.data, 1, ob.ctypes.data, out.ctypes.data,
+             None) == oracle.BAD_CSR
+    dec = np.array([2, 0], dtype=np.int32)
+    ok_ids = np.array([1, 2], dtype=np.int32)
+    assert f(W.ctypes.data, 3, 5, 0, 3, dec.ctypes.data, ok_ids.ctypes.data, 1, ob.ctypes.data, out.ctypes.data,
+             None) == oracle.BAD_CSR
+    assert f(W.ctypes.data, 2, 5, 0, 3, rp.ctypes.data, ok_ids.ctypes.data, 1, ob.ctypes.data, out.ctypes.data,
+             None) == oracle.BAD_ARG
+    assert f(None, 3, 5, 0, 3, rp.ctypes.data, ok_ids.ctypes.data, 1, ob.ctypes.data, out.ctypes.data,
+             None) == oracle.BAD_ARG
+
+
+ALL_CHECKS = [
+    check_exact_integer_direct,
+    check_cdist_node_major,
+    check_expanded_form,
+    check_node_major_python_loop,
+    check_planted_neuron,
+    check_constant_codebook,
+    check_tie_lowest_index,
+    check_single_neuron_and_empty_row,
+    check_quantisation_error,
+    check_offset_rows_and_blocks,
+    check_norms,
+    check_error_codes,
+]

@@ -1,0 +1,62 @@
+"""CPU tests: the oracle against what the paper and the mathematics fix.
+
+Parity of the HIP path is judged against the oracle, so the oracle is pinned
+first, by checks that do not re-use its own formula (tests/oracle_pins.py),
+and by a mutation check: each plausible slip planted in a copy of oracle.c
+(wrong sign, dropped square, dropped term, transposed stride, wrong
+tie-break, lost block offset, wrong second best, dropped feature) must make
+at least one pin fail.
+"""
+import os
+import subprocess
+
+import pytest
+
+import oracle
+import oracle_pins as P
+
+
+@pytest.mark.parametrize("check", P.ALL_CHECKS, ids=lambda f: f.__name__)
+def test_oracle_pin(check):
+    check(oracle.load())
+
+
+def test_exact_integer_full_tiny_workload():
+    # all 10,000 rows of the tiny 16x16 workload: exact indices and distances
+    P.check_exact_integer_tiny(oracle.load())
+
+
+MUTANTS = [
+    ("sign", "const double diff = xv - (double)wrow[k];", "const double diff = xv + (double)wrow[k];"),
+    ("dropped_square", "D[k] += diff * diff;", "D[k] += diff;"),
+    ("input_ignored", "            x[v] = 1;\n", "            (void)v;\n"),
+    ("transposed_stride", "const float *wrow = W + v * ldw;\n            for (int64_t k = 0; k < B; ++k) {\n                const double diff",
+     "const float *wrow = W + v;\n            for (int64_t k = 0; k < B; ++k) {\n                const double diff"),
+    ("tie_highest_index", "if (D[k] < D[best]) best = k;", "if (D[k] <= D[best]) best = k;"),
+    ("block_offset_lost", "bmu[s] = (int32_t)(i0 + best);", "bmu[s] = (int32_t)best;"),
+    ("second_best_includes_best", "if (k != best && D[k] < second)", "if (D[k] < second)"),
+    ("last_feature_dropped", "for (int64_t v = 0; v < V; ++v) {\n            const double xv",
+     "for (int64_t v = 0; v < V - 1; ++v) {\n            const double xv"),
+    ("norm_not_squared", "norms[k] += w * w;", "norms[k] += w;"),
+    ("x_off_by_one", "x[v] = 1;", "x[v < V - 1 ? v + 1 : v] = 1;"),
+]
+
+
+@pytest.mark.parametrize("name,old,new", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_mutant_is_caught(tmp_path, name, old, new):
+    src = open(os.path.join(os.path.dirname(oracle.__file__), "oracle.c")).read()
+    assert src.count(old) == 1, f"mutation site for {name} not found exactly once"
+    mutated = tmp_path / "oracle_mut.c"
+    mutated.write_text(src.replace(old, new))
+    # the header sits next to the original source
+    inc = os.path.dirname(oracle.__file__)
+    so = tmp_path / "liboracle_mut.so"
+    subprocess.run(["gcc", *oracle.CFLAGS, f"-I{inc}", str(mutated), "-o", str(so), "-lm"], check=True)
+    lib = oracle.load(str(so))
+    failures = []
+    for check in P.ALL_CHECKS:
+        try:
+            check(lib)
+        except (AssertionError, ValueError):
+            failures.append(check.__name__)
+    assert failures, f"mutant {name} passed every pin"
