@@ -1,0 +1,186 @@
+/*
+ * som.h -- C ABI of libsom.so, the MI355X (gfx950) best-matching-unit search
+ * for sparse-binary self-organising maps.
+ *
+ * What it computes (Method, problem statement, Eq. (1)): for every
+ * sparse-binary input x -- the sorted set of its active feature ids -- and a
+ * codebook of M prototypes w_i over V features stored feature-major
+ * (W[v*M + i], Method, feature-major codebook),
+ *
+ *     BMU(x) = argmin_i ||x - w_i||^2 = argmin_i ( ||w_i||^2 - 2 <x, w_i> ),
+ *     <x, w_i> = sum over the active features v of W[v*M + i]   (a gather-sum),
+ *
+ * ties going to the lowest neuron index (problem statement). The search is
+ * the tiled sweep of the SpMM-tile kernel section (Algorithm 2, steps 4-7):
+ * samples are grouped into tiles, each codebook row a tile touches is read
+ * once and added into every sample of the tile that holds that feature, and
+ * the argmin is taken inside the sweep, so no N x M score block is ever
+ * written.
+ *
+ * Numerics. Norms ||w_i||^2 are fp64 sums in ascending feature order. Each
+ * sample's dot product is an fp32 sum of its weights in ascending feature
+ * order, whatever the tile size. The ranked value is the fp64
+ * d_i = ||w_i||^2 - 2*dot_i (one rounding). The argmin compares 64-bit keys:
+ * the top 44 bits of an order-preserving image of d_i's fp64 pattern, then
+ * the 20-bit neuron index (so M <= 2^20); two values within about 2^-32 of
+ * each other (relative) compare by index. The returned distance is the full
+ * squared Euclidean distance ||x - w_bmu||^2 = d_bmu + nnz(x), in fp64.
+ *
+ * Conventions for every entry point:
+ *   - Pointers documented "device" are HIP device memory of the current
+ *     device (torch tensors' data_ptr() on ROCm); "host" pointers are
+ *     ordinary host memory.
+ *   - `stream` is a hipStream_t (NULL = the default stream). Device work is
+ *     enqueued on it and the call returns without waiting; inputs must stay
+ *     alive and outputs must not be read until the stream has synchronised.
+ *   - The caller owns every buffer. No entry point allocates device memory:
+ *     scratch space comes from the caller's workspace.
+ *   - Calls on different workspaces and streams may run concurrently.
+ *   - Cheap argument checks run on the host before anything is enqueued; on
+ *     failure nothing is enqueued and a status other than SOM_OK is returned,
+ *     with a description available from som_last_error() on the same thread.
+ *   - No C++ exception crosses the ABI. N == 0 is a valid no-op.
+ *
+ * CSR input. row_ptr has N+1 int32 entries; row s holds the feature ids
+ * col_idx[row_ptr[s] .. row_ptr[s+1]). row_ptr[0] need not be 0 (a slice of
+ * a larger batch): col_idx is always the base pointer the offsets index, and
+ * nnz = row_ptr[N] - row_ptr[0]. Each row's ids must be strictly ascending
+ * and in [0, V) (sorted, distinct: the paper's sparse-binary CSR, corpus
+ * section). That is a precondition of the device path, checked on the host
+ * by som_validate_csr_host. The device kernels never access memory outside
+ * the buffers they are given, whatever the CSR holds; a violation they see
+ * is recorded in the workspace and reported by som_bmu_input_flags, and the
+ * results of the affected samples are then unspecified.
+ */
+#ifndef SOM_H
+#define SOM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    SOM_OK = 0,
+    SOM_ERR_INVALID_ARG = 1, /* null pointer, negative or oversized dimension, bad config */
+    SOM_ERR_BAD_CSR = 2,     /* (som_validate_csr_host) the CSR breaks the input rules above */
+    SOM_ERR_WORKSPACE = 3,   /* workspace too small or misaligned */
+    SOM_ERR_HIP = 4          /* a HIP runtime call or launch failed */
+} som_status;
+
+/* Largest map the 20-bit index field of the argmin key can address. */
+#define SOM_MAX_NEURONS (1 << 20)
+
+/* Bits reported by som_bmu_input_flags. */
+#define SOM_FLAG_ID_RANGE 0x1u   /* a feature id outside [0, V) was skipped      */
+#define SOM_FLAG_UNSORTED 0x2u   /* a row's ids were not strictly ascending       */
+#define SOM_FLAG_ROW_PTR 0x4u    /* row_ptr decreased or left [row_ptr[0], +nnz]  */
+
+/*
+ * Optional tuning of the search. Pass NULL for the defaults.
+ *   tile_samples  samples per tile, TA (SpMM-tile kernel section): 8, 16 or
+ *                 32; 0 selects 16. Results do not depend on it: each
+ *                 sample's sum order is fixed by its own feature order.
+ * The same config must be given to every phase of one search.
+ */
+typedef struct {
+    int32_t tile_samples;
+    int32_t reserved[7]; /* must be zero */
+} som_bmu_config;
+
+/*
+ * Workspace bytes a search over N samples with nnz ids in total, on a map of
+ * M neurons and V features, needs (for any tile_samples). Pure host
+ * function; returns 0 if an argument is negative or M exceeds
+ * SOM_MAX_NEURONS. The workspace must be 256-byte aligned device memory.
+ */
+size_t som_bmu_workspace_bytes(int64_t N, int64_t M, int64_t V, int64_t nnz);
+
+/*
+ * Per-neuron squared norms (Algorithm 2, step 6; the separate norm pass of
+ * the profiling section): norms[i] = sum_{v=0}^{V-1} W[v*M+i]^2, each square
+ * formed exactly in fp64 and added in ascending v.
+ *   W      device fp32, V*M elements, feature-major, 4-byte aligned.
+ *   norms  device fp64 [M], written.
+ * Run once per codebook; the result serves every later search on it.
+ */
+som_status som_codebook_norms(const float *W, int64_t V, int64_t M, double *norms, void *stream);
+
+/*
+ * BMU search over a CSR batch (Eq. (1); Algorithm 2, steps 4-7).
+ *   W          device fp32 [V*M] feature-major codebook.
+ *   norms      device fp64 [M] from som_codebook_norms on the same W.
+ *   row_ptr    device int32 [N+1]; col_idx device int32 (see CSR input).
+ *   nnz        row_ptr[N] - row_ptr[0], as the caller knows it (sizes the
+ *              plan inside the workspace; the kernels never read past it).
+ *   bmu        device int32 [N], written: index of the best unit.
+ *   dist       device fp64 [N], written: ||x_s - w_bmu||^2.
+ *   workspace  device, >= som_bmu_workspace_bytes(N, M, V, nnz) bytes,
+ *              256-byte aligned; its contents are scratch.
+ *   config     NULL or a som_bmu_config (host memory, read during the call).
+ * Equivalent to som_bmu_plan, som_bmu_sweep, som_bmu_finalize in order.
+ */
+som_status som_bmu_search(const float *W, const double *norms, int64_t V, int64_t M, const int32_t *row_ptr,
+                          const int32_t *col_idx, int64_t N, int64_t nnz, int32_t *bmu, double *dist,
+                          void *workspace, size_t workspace_bytes, const som_bmu_config *config, void *stream);
+
+/*
+ * The three phases of som_bmu_search, for callers that time or overlap them.
+ * Arguments mean the same as above; each phase reads what the previous one
+ * left in the same workspace, so they must run in this order on one stream.
+ *
+ * som_bmu_plan -- tile plan (Algorithm 2, step 5; SpMM-tile kernel section):
+ *   for each tile of tile_samples consecutive rows, the ascending list of the
+ *   distinct feature ids its rows touch, each with a bit mask of the rows
+ *   that hold it. Also clears and sets the input flags.
+ */
+som_status som_bmu_plan(const int32_t *row_ptr, const int32_t *col_idx, int64_t N, int64_t nnz, int64_t V,
+                        int64_t M, void *workspace, size_t workspace_bytes, const som_bmu_config *config,
+                        void *stream);
+
+/*
+ * som_bmu_sweep -- the fused sweep (Algorithm 2, steps 4, 6, 7): streams each
+ *   planned codebook row once per tile and neuron strip, accumulates every
+ *   sample's dot product in registers, ranks d_i = ||w_i||^2 - 2*dot_i and
+ *   keeps, per sample and group of neurons, the smallest 64-bit key.
+ */
+som_status som_bmu_sweep(const float *W, const double *norms, int64_t V, int64_t M, int64_t N, int64_t nnz,
+                         void *workspace, size_t workspace_bytes, const som_bmu_config *config, void *stream);
+
+/*
+ * som_bmu_finalize -- reduces the per-group keys of each sample to its BMU
+ *   and recomputes the winner's distance from the sample's own ids:
+ *   dist = (||w_bmu||^2 - 2*dot) + nnz(x), the dot summed exactly as in the
+ *   sweep. Writes bmu and dist.
+ */
+som_status som_bmu_finalize(const float *W, const double *norms, int64_t V, int64_t M, const int32_t *row_ptr,
+                            const int32_t *col_idx, int64_t N, int64_t nnz, int32_t *bmu, double *dist,
+                            void *workspace, size_t workspace_bytes, const som_bmu_config *config,
+                            void *stream);
+
+/*
+ * Input flags (SOM_FLAG_*) the last plan on this workspace recorded. Waits
+ * for `stream`, then copies one word to *flags (host). 0 means the device
+ * saw a valid CSR.
+ */
+som_status som_bmu_input_flags(const void *workspace, size_t workspace_bytes, int64_t N, int64_t M, int64_t V,
+                               int64_t nnz, uint32_t *flags, void *stream);
+
+/*
+ * Host check of the CSR input rules (corpus section: sorted descriptor ids
+ * per row; binary values implicit): row_ptr non-decreasing, every id in
+ * [0, V), ids strictly ascending within each row. Host pointers; col_idx
+ * may be NULL when row_ptr[N] == row_ptr[0]. Returns SOM_OK, SOM_ERR_BAD_CSR
+ * (with the first offending row in som_last_error) or SOM_ERR_INVALID_ARG.
+ */
+som_status som_validate_csr_host(const int32_t *row_ptr, const int32_t *col_idx, int64_t N, int64_t V);
+
+/* Text describing the last failure on the calling thread ("" if none). */
+const char *som_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

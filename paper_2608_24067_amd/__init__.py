@@ -1,0 +1,21 @@
+"""MI355X (gfx950) best-matching-unit search for sparse-binary self-organising maps.
+
+The compute path is libsom.so (hand-written HIP kernels behind the C ABI of
+include/som.h); ``paper_2608_24067_amd.som`` is a thin ctypes binding with the
+same names. PyTorch supplies device memory and streams only.
+"""
+from .som import (  # noqa: F401
+    SomError,
+    alloc_workspace,
+    bmu_finalize,
+    bmu_plan,
+    bmu_search,
+    bmu_sweep,
+    codebook_norms,
+    input_flags,
+    last_error,
+    library_path,
+    load,
+    validate_csr_host,
+    workspace_bytes,
+)

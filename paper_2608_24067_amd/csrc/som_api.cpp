@@ -1,0 +1,228 @@
+// som_api.cpp -- host side of the C ABI declared in include/som.h: argument checks,
+// workspace carving, launches on the caller's stream, error text.
+
+#include <hip/hip_runtime.h>
+
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+
+#include "../../include/som.h"
+#include "som_internal.h"
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+som_status fail(som_status st, const char *fmt, ...)
+{
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof g_err, fmt, ap);
+    va_end(ap);
+    return st;
+}
+
+som_status hip_fail(hipError_t e, const char *what)
+{
+    return fail(SOM_ERR_HIP, "%s: %s (%d)", what, hipGetErrorString(e), (int)e);
+}
+
+som_status ok()
+{
+    g_err[0] = '\0';
+    return SOM_OK;
+}
+
+// Tile size from the optional config.
+som_status tile_samples(const som_bmu_config *cfg, int *ta)
+{
+    *ta = som::kDefaultTileSamples;
+    if (!cfg) return SOM_OK;
+    for (int r : cfg->reserved)
+        if (r != 0) return fail(SOM_ERR_INVALID_ARG, "som_bmu_config.reserved must be zero");
+    if (cfg->tile_samples == 0) return SOM_OK;
+    if (cfg->tile_samples != 8 && cfg->tile_samples != 16 && cfg->tile_samples != 32)
+        return fail(SOM_ERR_INVALID_ARG, "tile_samples must be 0, 8, 16 or 32 (got %d)", (int)cfg->tile_samples);
+    *ta = cfg->tile_samples;
+    return SOM_OK;
+}
+
+som_status check_dims(int64_t N, int64_t M, int64_t V, int64_t nnz)
+{
+    if (N < 0 || N >= INT32_MAX) return fail(SOM_ERR_INVALID_ARG, "N must be in [0, 2^31-1) (got %lld)", (long long)N);
+    if (M < 1 || M > SOM_MAX_NEURONS)
+        return fail(SOM_ERR_INVALID_ARG, "M must be in [1, %d] (got %lld)", SOM_MAX_NEURONS, (long long)M);
+    if (V < 1 || V > INT32_MAX) return fail(SOM_ERR_INVALID_ARG, "V must be in [1, 2^31-1] (got %lld)", (long long)V);
+    if (nnz < 0 || nnz > INT32_MAX)
+        return fail(SOM_ERR_INVALID_ARG, "nnz must be in [0, 2^31-1] (got %lld)", (long long)nnz);
+    return SOM_OK;
+}
+
+struct Carved {
+    uint2 *plan;
+    int2 *tiles;
+    unsigned long long *keys;
+    uint32_t *flags;
+    int64_t n_groups;
+};
+
+som_status carve(void *ws, size_t bytes, int64_t N, int64_t M, int64_t nnz, Carved *c)
+{
+    if (!ws) return fail(SOM_ERR_WORKSPACE, "workspace is NULL");
+    if (reinterpret_cast<uintptr_t>(ws) & 255) return fail(SOM_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+    const som::Layout L = som::layout_for(N, M, nnz);
+    if (bytes < L.total)
+        return fail(SOM_ERR_WORKSPACE, "workspace holds %zu bytes, the search needs %zu", bytes, L.total);
+    char *b = static_cast<char *>(ws);
+    c->plan = reinterpret_cast<uint2 *>(b + L.plan);
+    c->tiles = reinterpret_cast<int2 *>(b + L.tiles);
+    c->keys = reinterpret_cast<unsigned long long *>(b + L.keys);
+    c->flags = reinterpret_cast<uint32_t *>(b + L.flags);
+    c->n_groups = L.n_groups;
+    return SOM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t som_bmu_workspace_bytes(int64_t N, int64_t M, int64_t V, int64_t nnz)
+{
+    if (N < 0 || M < 1 || M > SOM_MAX_NEURONS || V < 1 || nnz < 0) return 0;
+    return som::layout_for(N, M, nnz).total;
+}
+
+som_status som_codebook_norms(const float *W, int64_t V, int64_t M, double *norms, void *stream)
+{
+    if (!W || !norms) return fail(SOM_ERR_INVALID_ARG, "som_codebook_norms: null pointer");
+    if (M < 1 || M > SOM_MAX_NEURONS || V < 1 || V > INT32_MAX)
+        return fail(SOM_ERR_INVALID_ARG, "som_codebook_norms: need 1 <= M <= %d and 1 <= V < 2^31", SOM_MAX_NEURONS);
+    if (reinterpret_cast<uintptr_t>(W) & 3) return fail(SOM_ERR_INVALID_ARG, "W must be 4-byte aligned");
+    hipError_t e = som::launch_norms(W, V, M, norms, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "som_codebook_norms launch");
+    return ok();
+}
+
+som_status som_bmu_plan(const int32_t *row_ptr, const int32_t *col_idx, int64_t N, int64_t nnz, int64_t V, int64_t M,
+                        void *workspace, size_t workspace_bytes, const som_bmu_config *config, void *stream)
+{
+    som_status st = check_dims(N, M, V, nnz);
+    if (st != SOM_OK) return st;
+    int ta;
+    if ((st = tile_samples(config, &ta)) != SOM_OK) return st;
+    if (N == 0) return ok();
+    if (!row_ptr || (nnz > 0 && !col_idx)) return fail(SOM_ERR_INVALID_ARG, "som_bmu_plan: null CSR pointer");
+    Carved c;
+    if ((st = carve(workspace, workspace_bytes, N, M, nnz, &c)) != SOM_OK) return st;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipError_t e = som::launch_clear_flags(c.flags, s);
+    if (e != hipSuccess) return hip_fail(e, "som_bmu_plan: flag clear launch");
+    e = som::launch_plan(ta, row_ptr, col_idx, N, nnz, V, c.plan, c.tiles, c.flags, s);
+    if (e != hipSuccess) return hip_fail(e, "som_bmu_plan launch");
+    return ok();
+}
+
+som_status som_bmu_sweep(const float *W, const double *norms, int64_t V, int64_t M, int64_t N, int64_t nnz,
+                         void *workspace, size_t workspace_bytes, const som_bmu_config *config, void *stream)
+{
+    som_status st = check_dims(N, M, V, nnz);
+    if (st != SOM_OK) return st;
+    int ta;
+    if ((st = tile_samples(config, &ta)) != SOM_OK) return st;
+    if (N == 0) return ok();
+    if (!W || !norms) return fail(SOM_ERR_INVALID_ARG, "som_bmu_sweep: null pointer");
+    if (reinterpret_cast<uintptr_t>(W) & 3) return fail(SOM_ERR_INVALID_ARG, "W must be 4-byte aligned");
+    Carved c;
+    if ((st = carve(workspace, workspace_bytes, N, M, nnz, &c)) != SOM_OK) return st;
+    hipError_t e = som::launch_sweep(ta, W, norms, M, N, V, nnz, c.plan, c.tiles, c.keys, c.n_groups,
+                                     static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "som_bmu_sweep launch");
+    return ok();
+}
+
+som_status som_bmu_finalize(const float *W, const double *norms, int64_t V, int64_t M, const int32_t *row_ptr,
+                            const int32_t *col_idx, int64_t N, int64_t nnz, int32_t *bmu, double *dist,
+                            void *workspace, size_t workspace_bytes, const som_bmu_config *config, void *stream)
+{
+    som_status st = check_dims(N, M, V, nnz);
+    if (st != SOM_OK) return st;
+    int ta;
+    if ((st = tile_samples(config, &ta)) != SOM_OK) return st;
+    if (N == 0) return ok();
+    if (!W || !norms || !row_ptr || (nnz > 0 && !col_idx) || !bmu || !dist)
+        return fail(SOM_ERR_INVALID_ARG, "som_bmu_finalize: null pointer");
+    Carved c;
+    if ((st = carve(workspace, workspace_bytes, N, M, nnz, &c)) != SOM_OK) return st;
+    hipError_t e = som::launch_finalize(W, norms, V, M, row_ptr, col_idx, N, nnz, c.keys, c.n_groups, bmu, dist,
+                                        static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "som_bmu_finalize launch");
+    return ok();
+}
+
+som_status som_bmu_search(const float *W, const double *norms, int64_t V, int64_t M, const int32_t *row_ptr,
+                          const int32_t *col_idx, int64_t N, int64_t nnz, int32_t *bmu, double *dist,
+                          void *workspace, size_t workspace_bytes, const som_bmu_config *config, void *stream)
+{
+    som_status st = check_dims(N, M, V, nnz);
+    if (st != SOM_OK) return st;
+    int ta;
+    if ((st = tile_samples(config, &ta)) != SOM_OK) return st;
+    if (N == 0) return ok();
+    if (!W || !norms || !row_ptr || (nnz > 0 && !col_idx) || !bmu || !dist)
+        return fail(SOM_ERR_INVALID_ARG, "som_bmu_search: null pointer");
+    if (reinterpret_cast<uintptr_t>(W) & 3) return fail(SOM_ERR_INVALID_ARG, "W must be 4-byte aligned");
+    Carved c;
+    if ((st = carve(workspace, workspace_bytes, N, M, nnz, &c)) != SOM_OK) return st;
+    if ((st = som_bmu_plan(row_ptr, col_idx, N, nnz, V, M, workspace, workspace_bytes, config, stream)) != SOM_OK)
+        return st;
+    if ((st = som_bmu_sweep(W, norms, V, M, N, nnz, workspace, workspace_bytes, config, stream)) != SOM_OK)
+        return st;
+    return som_bmu_finalize(W, norms, V, M, row_ptr, col_idx, N, nnz, bmu, dist, workspace, workspace_bytes, config,
+                            stream);
+}
+
+som_status som_bmu_input_flags(const void *workspace, size_t workspace_bytes, int64_t N, int64_t M, int64_t V,
+                               int64_t nnz, uint32_t *flags, void *stream)
+{
+    som_status st = check_dims(N, M, V, nnz);
+    if (st != SOM_OK) return st;
+    if (!flags) return fail(SOM_ERR_INVALID_ARG, "som_bmu_input_flags: flags is NULL");
+    *flags = 0;
+    if (N == 0) return ok();
+    Carved c;
+    if ((st = carve(const_cast<void *>(workspace), workspace_bytes, N, M, nnz, &c)) != SOM_OK) return st;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipError_t e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return hip_fail(e, "som_bmu_input_flags: stream synchronize");
+    e = hipMemcpy(flags, c.flags, sizeof(uint32_t), hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return hip_fail(e, "som_bmu_input_flags: copy");
+    return ok();
+}
+
+som_status som_validate_csr_host(const int32_t *row_ptr, const int32_t *col_idx, int64_t N, int64_t V)
+{
+    if (N < 0 || V < 1 || V > INT32_MAX) return fail(SOM_ERR_INVALID_ARG, "need N >= 0 and 1 <= V < 2^31");
+    if (!row_ptr) return fail(SOM_ERR_INVALID_ARG, "row_ptr is NULL");
+    for (int64_t s = 0; s < N; ++s)
+        if (row_ptr[s + 1] < row_ptr[s])
+            return fail(SOM_ERR_BAD_CSR, "row %lld: row_ptr decreases (%d -> %d)", (long long)s, row_ptr[s],
+                        row_ptr[s + 1]);
+    if (row_ptr[N] > row_ptr[0] && !col_idx) return fail(SOM_ERR_INVALID_ARG, "col_idx is NULL");
+    for (int64_t s = 0; s < N; ++s) {
+        for (int64_t p = row_ptr[s]; p < row_ptr[s + 1]; ++p) {
+            const int32_t id = col_idx[p];
+            if (id < 0 || id >= V)
+                return fail(SOM_ERR_BAD_CSR, "row %lld: feature id %d outside [0, %lld)", (long long)s, id,
+                            (long long)V);
+            if (p > row_ptr[s] && id <= col_idx[p - 1])
+                return fail(SOM_ERR_BAD_CSR, "row %lld: ids not strictly ascending (%d after %d)", (long long)s, id,
+                            col_idx[p - 1]);
+        }
+    }
+    return ok();
+}
+
+const char *som_last_error(void) { return g_err; }
+
+}  // extern "C"

@@ -1,0 +1,212 @@
+"""ctypes binding of libsom.so (include/som.h). Argument marshalling only.
+
+Every function takes torch tensors, checks dtype, device, size and
+contiguity, and passes raw pointers plus the current torch stream's handle
+to the C entry point of the same name; all work runs in the library's HIP
+kernels on that stream. If libsom.so is missing, loading fails loudly: there
+is no fallback of any kind.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_HERE, "libsom.so")
+
+SOM_OK, SOM_ERR_INVALID_ARG, SOM_ERR_BAD_CSR, SOM_ERR_WORKSPACE, SOM_ERR_HIP = range(5)
+MAX_NEURONS = 1 << 20
+FLAG_ID_RANGE, FLAG_UNSORTED, FLAG_ROW_PTR = 0x1, 0x2, 0x4
+
+EXPORTS = (
+    "som_bmu_workspace_bytes", "som_codebook_norms", "som_bmu_search", "som_bmu_plan", "som_bmu_sweep",
+    "som_bmu_finalize", "som_bmu_input_flags", "som_validate_csr_host", "som_last_error",
+)
+
+
+class SomError(RuntimeError):
+    def __init__(self, status: int, where: str, text: str):
+        super().__init__(f"{where}: status {status}: {text}")
+        self.status = status
+
+
+class _Config(ctypes.Structure):
+    _fields_ = [("tile_samples", ctypes.c_int32), ("reserved", ctypes.c_int32 * 7)]
+
+
+_lib = None
+
+
+def library_path() -> str:
+    return _LIB_PATH
+
+
+def load():
+    """Load libsom.so (built by __graft_entry__.build()); raises if it is absent."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        raise RuntimeError(f"libsom.so not found at {_LIB_PATH}: build it with __graft_entry__.build()")
+    lib = ctypes.CDLL(_LIB_PATH)
+    i64, vp, sz = ctypes.c_int64, ctypes.c_void_p, ctypes.c_size_t
+    cfgp = ctypes.POINTER(_Config)
+    lib.som_bmu_workspace_bytes.argtypes = [i64, i64, i64, i64]
+    lib.som_bmu_workspace_bytes.restype = sz
+    lib.som_codebook_norms.argtypes = [vp, i64, i64, vp, vp]
+    lib.som_bmu_search.argtypes = [vp, vp, i64, i64, vp, vp, i64, i64, vp, vp, vp, sz, cfgp, vp]
+    lib.som_bmu_plan.argtypes = [vp, vp, i64, i64, i64, i64, vp, sz, cfgp, vp]
+    lib.som_bmu_sweep.argtypes = [vp, vp, i64, i64, i64, i64, vp, sz, cfgp, vp]
+    lib.som_bmu_finalize.argtypes = [vp, vp, i64, i64, vp, vp, i64, i64, vp, vp, vp, sz, cfgp, vp]
+    lib.som_bmu_input_flags.argtypes = [vp, sz, i64, i64, i64, i64, ctypes.POINTER(ctypes.c_uint32), vp]
+    lib.som_validate_csr_host.argtypes = [vp, vp, i64, i64]
+    for name in ("som_codebook_norms", "som_bmu_search", "som_bmu_plan", "som_bmu_sweep", "som_bmu_finalize",
+                 "som_bmu_input_flags", "som_validate_csr_host"):
+        getattr(lib, name).restype = ctypes.c_int
+    lib.som_last_error.argtypes = []
+    lib.som_last_error.restype = ctypes.c_char_p
+    _lib = lib
+    return lib
+
+
+def last_error() -> str:
+    return load().som_last_error().decode()
+
+
+def _check(status: int, where: str):
+    if status != SOM_OK:
+        raise SomError(status, where, last_error())
+
+
+def _stream(t: torch.Tensor) -> int:
+    return torch.cuda.current_stream(t.device).cuda_stream
+
+
+def _dev(t: torch.Tensor, name: str, dtype: torch.dtype, min_numel: int = 0) -> int:
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be on the GPU")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype} (got {t.dtype})")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if t.numel() < min_numel:
+        raise ValueError(f"{name} holds {t.numel()} elements, needs {min_numel}")
+    return t.data_ptr()
+
+
+def _cfg(tile_samples: int):
+    c = _Config()
+    c.tile_samples = int(tile_samples)
+    return ctypes.byref(c)
+
+
+def workspace_bytes(N: int, M: int, V: int, nnz: int) -> int:
+    n = load().som_bmu_workspace_bytes(N, M, V, nnz)
+    if n == 0:
+        raise ValueError("som_bmu_workspace_bytes: invalid sizes")
+    return n
+
+
+def alloc_workspace(N: int, M: int, V: int, nnz: int, device) -> torch.Tensor:
+    return torch.empty(workspace_bytes(N, M, V, nnz), dtype=torch.uint8, device=device)
+
+
+def codebook_norms(W: torch.Tensor, V: int, M: int, out: torch.Tensor | None = None) -> torch.Tensor:
+    """fp64 per-neuron squared norms of the feature-major V x M codebook W."""
+    if W.numel() != V * M:
+        raise ValueError("W must hold V*M elements")
+    wp = _dev(W, "W", torch.float32)
+    if out is None:
+        out = torch.empty(M, dtype=torch.float64, device=W.device)
+    op = _dev(out, "norms", torch.float64, M)
+    _check(load().som_codebook_norms(wp, V, M, op, _stream(W)), "som_codebook_norms")
+    return out
+
+
+def _csr(row_ptr, col_idx, N, nnz=None):
+    rp = _dev(row_ptr, "row_ptr", torch.int32, N + 1)
+    ci = _dev(col_idx, "col_idx", torch.int32) if col_idx.numel() else None
+    if nnz is not None and col_idx.numel() < nnz:
+        raise ValueError(f"col_idx holds {col_idx.numel()} ids, nnz is {nnz}")
+    return rp, ci
+
+
+def _nnz(row_ptr: torch.Tensor, N: int, nnz: int | None) -> int:
+    if nnz is None:  # one device read; pass nnz to avoid it
+        nnz = int(row_ptr[N].item()) - int(row_ptr[0].item())
+    return int(nnz)
+
+
+def bmu_search(W, norms, row_ptr, col_idx, V: int, M: int, nnz: int | None = None, bmu=None, dist=None,
+               workspace=None, tile_samples: int = 0):
+    """BMU index (int32) and squared distance (fp64) of every CSR row. Returns (bmu, dist)."""
+    N = row_ptr.numel() - 1
+    nnz = _nnz(row_ptr, N, nnz)
+    dev = W.device
+    if bmu is None:
+        bmu = torch.empty(N, dtype=torch.int32, device=dev)
+    if dist is None:
+        dist = torch.empty(N, dtype=torch.float64, device=dev)
+    if workspace is None:
+        workspace = alloc_workspace(N, M, V, nnz, dev)
+    if W.numel() != V * M:
+        raise ValueError("W must hold V*M elements")
+    rp, ci = _csr(row_ptr, col_idx, N, nnz)
+    st = load().som_bmu_search(
+        _dev(W, "W", torch.float32), _dev(norms, "norms", torch.float64, M), V, M, rp, ci, N, nnz,
+        _dev(bmu, "bmu", torch.int32, N), _dev(dist, "dist", torch.float64, N),
+        _dev(workspace, "workspace", torch.uint8), workspace.numel(), _cfg(tile_samples), _stream(W))
+    _check(st, "som_bmu_search")
+    return bmu, dist
+
+
+def bmu_plan(row_ptr, col_idx, V: int, M: int, nnz: int, workspace, tile_samples: int = 0):
+    N = row_ptr.numel() - 1
+    rp, ci = _csr(row_ptr, col_idx, N, nnz)
+    st = load().som_bmu_plan(rp, ci, N, nnz, V, M, _dev(workspace, "workspace", torch.uint8), workspace.numel(),
+                             _cfg(tile_samples), _stream(row_ptr))
+    _check(st, "som_bmu_plan")
+
+
+def bmu_sweep(W, norms, V: int, M: int, N: int, nnz: int, workspace, tile_samples: int = 0):
+    if W.numel() != V * M:
+        raise ValueError("W must hold V*M elements")
+    st = load().som_bmu_sweep(_dev(W, "W", torch.float32), _dev(norms, "norms", torch.float64, M), V, M, N, nnz,
+                              _dev(workspace, "workspace", torch.uint8), workspace.numel(), _cfg(tile_samples),
+                              _stream(W))
+    _check(st, "som_bmu_sweep")
+
+
+def bmu_finalize(W, norms, row_ptr, col_idx, V: int, M: int, nnz: int, bmu, dist, workspace, tile_samples: int = 0):
+    N = row_ptr.numel() - 1
+    if W.numel() != V * M:
+        raise ValueError("W must hold V*M elements")
+    rp, ci = _csr(row_ptr, col_idx, N, nnz)
+    st = load().som_bmu_finalize(
+        _dev(W, "W", torch.float32), _dev(norms, "norms", torch.float64, M), V, M, rp, ci, N, nnz,
+        _dev(bmu, "bmu", torch.int32, N), _dev(dist, "dist", torch.float64, N),
+        _dev(workspace, "workspace", torch.uint8), workspace.numel(), _cfg(tile_samples), _stream(W))
+    _check(st, "som_bmu_finalize")
+
+
+def input_flags(workspace, N: int, M: int, V: int, nnz: int) -> int:
+    """SOM_FLAG_* bits the last plan recorded (waits for the current stream)."""
+    out = ctypes.c_uint32(0)
+    st = load().som_bmu_input_flags(_dev(workspace, "workspace", torch.uint8), workspace.numel(), N, M, V, nnz,
+                                    ctypes.byref(out), _stream(workspace))
+    _check(st, "som_bmu_input_flags")
+    return int(out.value)
+
+
+def validate_csr_host(row_ptr, col_idx, V: int) -> None:
+    """Raises SomError(SOM_ERR_BAD_CSR) if a host CSR breaks the sorted, distinct, in-range rules."""
+    rp = np.ascontiguousarray(np.asarray(row_ptr), dtype=np.int32)
+    ci = np.ascontiguousarray(np.asarray(col_idx), dtype=np.int32)
+    N = rp.shape[0] - 1
+    st = load().som_validate_csr_host(rp.ctypes.data, ci.ctypes.data if ci.size else None, N, V)
+    _check(st, "som_validate_csr_host")

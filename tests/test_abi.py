@@ -1,0 +1,136 @@
+"""CPU tests of the C ABI: the library loads and exports every declared entry
+point, the workspace query, the host CSR validator, and every argument check
+that returns before anything reaches the GPU."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_2608_24067_amd.som as som
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_entry_points():
+    names = []
+    for fn in os.listdir(os.path.join(ROOT, "include")):
+        if fn.endswith(".h"):
+            text = open(os.path.join(ROOT, "include", fn)).read()
+            names += re.findall(r"^\s*(?:const\s+)?[a-z_0-9]+\s*\*?\s*(som_[a-z_0-9]+)\s*\(", text, re.M)
+    return sorted(set(names))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = som.load()
+    names = declared_entry_points()
+    assert set(names) == set(som.EXPORTS), names
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_workspace_bytes():
+    n = som.workspace_bytes(10_000, 256, 2000, 120_000)
+    assert n > 0 and n % 256 == 0
+    # grows with every size it depends on
+    assert som.workspace_bytes(20_000, 256, 2000, 120_000) > n
+    assert som.workspace_bytes(10_000, 4096, 2000, 120_000) > n
+    assert som.workspace_bytes(10_000, 256, 2000, 240_000) > n
+    lib = som.load()
+    assert lib.som_bmu_workspace_bytes(-1, 256, 2000, 0) == 0
+    assert lib.som_bmu_workspace_bytes(10, 0, 2000, 0) == 0
+    assert lib.som_bmu_workspace_bytes(10, (1 << 20) + 1, 2000, 0) == 0
+    assert lib.som_bmu_workspace_bytes(10, 1 << 20, 2000, 0) > 0
+
+
+def _status(rp, ci, V):
+    lib = som.load()
+    rp = np.ascontiguousarray(rp, dtype=np.int32)
+    ci = np.ascontiguousarray(ci, dtype=np.int32)
+    return lib.som_validate_csr_host(rp.ctypes.data, ci.ctypes.data if ci.size else None, rp.size - 1, V)
+
+
+def test_validate_csr_host():
+    assert _status([0, 2, 3], [1, 4, 0], 5) == som.SOM_OK
+    assert _status([0, 0, 0], [], 5) == som.SOM_OK           # empty rows are allowed
+    assert _status([0], [], 5) == som.SOM_OK                 # N = 0
+    assert _status([3, 5], [9, 9, 9, 1, 2], 5) == som.SOM_OK  # a slice: row_ptr need not start at 0
+    assert _status([0, 2, 1], [1, 2], 5) == som.SOM_ERR_BAD_CSR      # row_ptr decreases
+    assert _status([0, 2], [1, 5], 5) == som.SOM_ERR_BAD_CSR         # id == V
+    assert _status([0, 2], [-1, 2], 5) == som.SOM_ERR_BAD_CSR        # negative id
+    assert _status([0, 2], [3, 1], 5) == som.SOM_ERR_BAD_CSR         # unsorted
+    assert _status([0, 2], [3, 3], 5) == som.SOM_ERR_BAD_CSR         # repeated id
+    assert "ascending" in som.last_error()
+    assert _status([0, 1], [0], 0) == som.SOM_ERR_INVALID_ARG         # V < 1
+    with pytest.raises(som.SomError):
+        som.validate_csr_host([0, 2], [3, 3], 5)
+    som.validate_csr_host([0, 2], [1, 3], 5)
+
+
+def test_generated_workloads_are_valid_csr():
+    import synth
+    for seed, N, V in [(0, 5000, 2000), (1, 5000, 30000)]:
+        rp, ci = synth.make_csr(seed, N, V)
+        som.validate_csr_host(rp, ci, V)
+
+
+# Argument checks that fail before any HIP call (no GPU here). Pointers are fake
+# but never dereferenced: every call below must return an error status first.
+FAKE = ctypes.c_void_p(1 << 20)
+
+
+def _search(W=FAKE, norms=FAKE, V=100, M=64, rp=FAKE, ci=FAKE, N=10, nnz=50, bmu=FAKE, dist=FAKE, ws=FAKE,
+            ws_bytes=1 << 30, cfg=None):
+    lib = som.load()
+    return lib.som_bmu_search(W, norms, V, M, rp, ci, N, nnz, bmu, dist, ws, ws_bytes, cfg, None)
+
+
+def _cfg(ta, reserved0=0):
+    c = som._Config()
+    c.tile_samples = ta
+    c.reserved[0] = reserved0
+    return ctypes.pointer(c)
+
+
+@pytest.mark.parametrize("kwargs,status", [
+    (dict(M=0), som.SOM_ERR_INVALID_ARG),
+    (dict(M=(1 << 20) + 1), som.SOM_ERR_INVALID_ARG),
+    (dict(V=0), som.SOM_ERR_INVALID_ARG),
+    (dict(N=-1), som.SOM_ERR_INVALID_ARG),
+    (dict(nnz=-1), som.SOM_ERR_INVALID_ARG),
+    (dict(W=None), som.SOM_ERR_INVALID_ARG),
+    (dict(norms=None), som.SOM_ERR_INVALID_ARG),
+    (dict(rp=None), som.SOM_ERR_INVALID_ARG),
+    (dict(ci=None), som.SOM_ERR_INVALID_ARG),
+    (dict(bmu=None), som.SOM_ERR_INVALID_ARG),
+    (dict(dist=None), som.SOM_ERR_INVALID_ARG),
+    (dict(W=ctypes.c_void_p((1 << 20) + 2)), som.SOM_ERR_INVALID_ARG),  # W not 4-byte aligned
+    (dict(cfg=_cfg(7)), som.SOM_ERR_INVALID_ARG),
+    (dict(cfg=_cfg(16, reserved0=1)), som.SOM_ERR_INVALID_ARG),
+    (dict(ws=None), som.SOM_ERR_WORKSPACE),
+    (dict(ws=ctypes.c_void_p((1 << 20) + 64)), som.SOM_ERR_WORKSPACE),  # not 256-byte aligned
+    (dict(ws_bytes=1024), som.SOM_ERR_WORKSPACE),
+])
+def test_search_argument_checks(kwargs, status):
+    assert _search(**kwargs) == status
+    assert som.last_error() != ""
+
+
+def test_zero_samples_is_a_no_op():
+    # N == 0 succeeds without touching any pointer
+    assert _search(N=0, nnz=0, W=None, norms=None, rp=None, ci=None, bmu=None, dist=None, ws=None) == som.SOM_OK
+
+
+def test_phase_and_norms_argument_checks():
+    lib = som.load()
+    assert lib.som_codebook_norms(None, 10, 10, FAKE, None) == som.SOM_ERR_INVALID_ARG
+    assert lib.som_codebook_norms(FAKE, 10, 0, FAKE, None) == som.SOM_ERR_INVALID_ARG
+    assert lib.som_codebook_norms(FAKE, 0, 10, FAKE, None) == som.SOM_ERR_INVALID_ARG
+    assert lib.som_bmu_plan(FAKE, FAKE, 10, 50, 100, 64, FAKE, 100, None, None) == som.SOM_ERR_WORKSPACE
+    assert lib.som_bmu_sweep(FAKE, FAKE, 100, 64, 10, 50, FAKE, 100, None, None) == som.SOM_ERR_WORKSPACE
+    assert lib.som_bmu_finalize(FAKE, FAKE, 100, 64, FAKE, FAKE, 10, 50, FAKE, FAKE, FAKE, 100, None,
+                                None) == som.SOM_ERR_WORKSPACE
+    out = ctypes.c_uint32(7)
+    assert lib.som_bmu_input_flags(FAKE, 100, 10, 64, 100, 50, ctypes.byref(out), None) == som.SOM_ERR_WORKSPACE
+    assert lib.som_bmu_input_flags(FAKE, 100, 10, 64, 100, 50, None, None) == som.SOM_ERR_INVALID_ARG

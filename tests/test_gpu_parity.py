@@ -1,0 +1,162 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle.
+
+Sizes here finish on the oracle in seconds yet span several tiles, strips and
+neuron groups with ragged tails; the full-size workloads are in
+test_gpu_fullsize.py. Every input is seeded (synth).
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2608_24067_amd.som as som
+import synth
+from parity import compare, gpu_run, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+def case(seed, N, V, M, kind):
+    rp, ci = synth.make_csr(seed, N, V)
+    W = synth.codebook(seed, kind, V, M)
+    return rp, ci, W
+
+
+@pytest.mark.parametrize("V,M,kind", [
+    (2000, 256, synth.QUANTISED), (300, 1, synth.UNIFORM), (37, 5, synth.UNIFORM),
+    (1000, 1029, synth.UNIFORM), (64, 4096, synth.UNIFORM), (30000, 300, synth.UNIFORM),
+])
+def test_norms_match_oracle_bitwise(dev, V, M, kind):
+    # both sides add exact fp64 squares in ascending feature order
+    W = synth.codebook(7, kind, V, M)
+    n_gpu = som.codebook_norms(to_dev(W, dev), V, M).cpu().numpy()
+    n_ref = oracle.norms(W)
+    assert np.array_equal(n_gpu, n_ref)
+
+
+def test_tiny_workload_bit_exact(dev):
+    # the whole 16x16 workload (10,000 rows, V=2000, k/256): every index and distance exact
+    cfg = synth.CONFIGS["tiny"]
+    rp, ci, W = case(cfg.seed, cfg.N, cfg.V, cfg.M, cfg.kind)
+    b, d, _ = gpu_run(W, rp, ci, dev)
+    compare(W, rp, ci, b, d, exact=True, what="tiny")
+
+
+RAGGED = [
+    # (seed, N, V, M, kind): N off tile multiples, M off 4 / 256 / 1024 multiples
+    (21, 1, 50, 1, synth.QUANTISED),
+    (22, 17, 300, 5, synth.QUANTISED),
+    (23, 1000, 2000, 300, synth.QUANTISED),
+    (24, 333, 500, 1500, synth.QUANTISED),
+    (25, 2049, 1000, 1024, synth.UNIFORM),
+    (26, 300, 30000, 4099, synth.UNIFORM),
+    (27, 77, 30000, 2048, synth.UNIFORM),
+    (28, 520, 4000, 3, synth.UNIFORM),
+]
+
+
+@pytest.mark.parametrize("tile", [8, 16, 32])
+@pytest.mark.parametrize("seed,N,V,M,kind", RAGGED)
+def test_ragged_shapes(dev, seed, N, V, M, kind, tile):
+    rp, ci, W = case(seed, N, V, M, kind)
+    b, d, _ = gpu_run(W, rp, ci, dev, tile_samples=tile)
+    compare(W, rp, ci, b, d, exact=(kind == synth.QUANTISED), what=f"N={N} V={V} M={M} TA={tile}")
+
+
+def test_tile_size_and_repeat_invariance(dev):
+    # each sample's dot is its own ascending fp32 sum, so the tile size cannot change a bit
+    rp, ci, W = case(31, 3000, 30000, 2500, synth.UNIFORM)
+    runs = [gpu_run(W, rp, ci, dev, tile_samples=t)[:2] for t in (8, 16, 32, 16)]
+    for b, d in runs[1:]:
+        assert np.array_equal(b, runs[0][0]) and np.array_equal(d, runs[0][1])
+
+
+def test_permuting_samples_permutes_results(dev):
+    rp, ci, W = case(32, 700, 5000, 777, synth.UNIFORM)
+    b, d, _ = gpu_run(W, rp, ci, dev)
+    perm = np.random.default_rng(0).permutation(len(rp) - 1)
+    lens = np.diff(rp)[perm]
+    rp2 = np.zeros_like(rp)
+    rp2[1:] = np.cumsum(lens)
+    ci2 = np.concatenate([ci[rp[r]:rp[r + 1]] for r in perm])
+    b2, d2, _ = gpu_run(W, rp2, ci2, dev)
+    assert np.array_equal(b2, b[perm]) and np.array_equal(d2, d[perm])
+
+
+def test_constant_codebook_lowest_index(dev):
+    rp, ci, _ = case(33, 500, 800, 1500, synth.UNIFORM)
+    W = np.full((800, 1500), 0.25, dtype=np.float32)
+    b, d, _ = gpu_run(W, rp, ci, dev)
+    nnz = np.diff(rp).astype(np.float64)
+    assert (b == 0).all()
+    assert np.array_equal(d, nnz * 0.75 ** 2 + (800 - nnz) * 0.25 ** 2)
+
+
+def test_planted_and_tied_units(dev):
+    # a copy of sample s's input at j1 < j2 (different strips and groups): distance 0, lowest index wins
+    rp, ci, W = case(34, 200, 3000, 2100, synth.UNIFORM)
+    W = W.copy()
+    plants = {5: (5, 2097), 77: (1023, 1024), 150: (0, 2099)}
+    for s, (j1, j2) in plants.items():
+        for j in (j1, j2):
+            W[:, j] = 0.0
+            W[ci[rp[s]:rp[s + 1]], j] = 1.0
+    b, d, _ = gpu_run(W, rp, ci, dev)
+    for s, (j1, _) in plants.items():
+        assert b[s] == j1 and d[s] == 0.0
+    compare(W, rp, ci, b, d, exact=False, what="planted", rows=np.arange(0, 200, 7))
+
+
+def test_empty_rows_rank_by_norm(dev):
+    V, M = 400, 700
+    W = synth.codebook(35, synth.UNIFORM, V, M)
+    rp = np.array([0, 0, 3, 3, 3], dtype=np.int32)
+    ci = np.array([2, 10, 399], dtype=np.int32)
+    b, d, n = gpu_run(W, rp, ci, dev)
+    for s in (0, 2, 3):
+        assert b[s] == int(np.argmin(n)) and d[s] == n.min()
+    compare(W, rp, ci, b, d, exact=False, what="empty rows")
+
+
+def test_single_neuron(dev):
+    rp, ci, W = case(36, 100, 300, 1, synth.QUANTISED)
+    b, d, _ = gpu_run(W, rp, ci, dev)
+    assert (b == 0).all()
+    compare(W, rp, ci, b, d, exact=True, what="M=1")
+
+
+def test_batch_slice_offset_row_ptr(dev):
+    # row_ptr starting past 0, col_idx the base of the whole array
+    rp, ci, W = case(37, 600, 3000, 900, synth.QUANTISED)
+    b, d, _ = gpu_run(W, rp, ci, dev)
+    s0, s1 = 101, 437
+    bs, ds_, _ = gpu_run(W, rp[s0:s1 + 1], ci, dev)
+    assert np.array_equal(bs, b[s0:s1]) and np.array_equal(ds_, d[s0:s1])
+
+
+def test_phases_equal_search_and_flags_clean(dev):
+    rp, ci, W = case(38, 999, 3000, 1111, synth.UNIFORM)
+    Wd = to_dev(W, dev)
+    rpd, cid = to_dev(rp, dev), to_dev(ci, dev)
+    V, M, N, nnz = 3000, 1111, 999, int(rp[-1])
+    norms = som.codebook_norms(Wd, V, M)
+    b1, d1 = som.bmu_search(Wd, norms, rpd, cid, V, M, nnz=nnz)
+    ws = som.alloc_workspace(N, M, V, nnz, dev)
+    b2 = torch.empty(N, dtype=torch.int32, device=dev)
+    d2 = torch.empty(N, dtype=torch.float64, device=dev)
+    som.bmu_plan(rpd, cid, V, M, nnz, ws)
+    som.bmu_sweep(Wd, norms, V, M, N, nnz, ws)
+    som.bmu_finalize(Wd, norms, rpd, cid, V, M, nnz, b2, d2, ws)
+    assert som.input_flags(ws, N, M, V, nnz) == 0
+    assert torch.equal(b1, b2) and torch.equal(d1, d2)
+
+
+@pytest.mark.parametrize("name,rows", [("64", 4096), ("256", 1024), ("512", 256)])
+def test_workload_prefix(dev, name, rows):
+    # the first rows of a full-size workload (rows are drawn per (seed, row)), full map
+    cfg = synth.CONFIGS[name]
+    rp, ci = synth.make_csr(cfg.seed, rows, cfg.V)
+    W = synth.codebook(cfg.seed, cfg.kind, cfg.V, cfg.M)
+    b, d, _ = gpu_run(W, rp, ci, dev)
+    sample = np.linspace(0, rows - 1, 24).astype(int)
+    compare(W, rp, ci, b, d, exact=False, what=f"{name} prefix", rows=sample, nthreads=16)
