@@ -148,3 +148,32 @@ def tile_distinct(row_ptr: np.ndarray, col_idx: np.ndarray, TA: int = 16, nthrea
     if rc != 0 or (out < 0).any():
         raise ValueError("synth_tile_distinct failed")
     return out
+
+
+def codebook_to_device(seed: int, kind: int, V: int, M: int, device, chunk_bytes: int = 1 << 28,
+                       nthreads: int | None = None):
+    """The whole V x M codebook as a float32 device tensor, drawn on the host in row chunks.
+
+    Two pinned staging buffers alternate, so drawing the next chunk overlaps
+    the copy of the previous one; host memory stays at two chunks.
+    """
+    import torch
+
+    W = torch.empty((V, M), dtype=torch.float32, device=device)
+    rows = max(1, min(V, chunk_bytes // (4 * M)))
+    bufs = [torch.empty((rows, M), dtype=torch.float32, pin_memory=True) for _ in range(2)]
+    events = [None, None]
+    stream = torch.cuda.current_stream(device)
+    for n, v0 in enumerate(range(0, V, rows)):
+        v1 = min(V, v0 + rows)
+        k = n & 1
+        if events[k] is not None:
+            events[k].synchronize()
+        host = bufs[k][: v1 - v0]
+        codebook(seed, kind, V, M, v0, v1, 0, M, out=host.numpy(), nthreads=nthreads)
+        W[v0:v1].copy_(host, non_blocking=True)
+        ev = torch.cuda.Event()
+        ev.record(stream)
+        events[k] = ev
+    torch.cuda.synchronize(device)
+    return W
