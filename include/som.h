@@ -81,9 +81,10 @@ typedef enum {
 /*
  * Optional tuning of the search. Pass NULL for the defaults.
  *   tile_samples  samples per tile, TA (SpMM-tile kernel section): 8, 16 or
- *                 32; 0 selects 16. Results do not depend on it: each
+ *                 32; 0 selects 8. Results do not depend on it: each
  *                 sample's sum order is fixed by its own feature order.
- * The same config must be given to every phase of one search.
+ * The same config must be given to the workspace query and to every phase
+ * of one search.
  */
 typedef struct {
     int32_t tile_samples;
@@ -92,11 +93,13 @@ typedef struct {
 
 /*
  * Workspace bytes a search over N samples with nnz ids in total, on a map of
- * M neurons and V features, needs (for any tile_samples). Pure host
- * function; returns 0 if an argument is negative or M exceeds
- * SOM_MAX_NEURONS. The workspace must be 256-byte aligned device memory.
+ * M neurons and V features, needs under `config` (NULL = defaults). Pure
+ * host function; returns 0 if a size is out of range (see som_bmu_search)
+ * or the config is invalid. The workspace must be 256-byte aligned device
+ * memory. It holds the tile plan (8 bytes per id) and one 8-byte partial key
+ * per sample and strip of 512 neurons (256 when tile_samples > 8).
  */
-size_t som_bmu_workspace_bytes(int64_t N, int64_t M, int64_t V, int64_t nnz);
+size_t som_bmu_workspace_bytes(int64_t N, int64_t M, int64_t V, int64_t nnz, const som_bmu_config *config);
 
 /*
  * Per-neuron squared norms (Algorithm 2, step 6; the separate norm pass of
@@ -117,8 +120,8 @@ som_status som_codebook_norms(const float *W, int64_t V, int64_t M, double *norm
  *              plan inside the workspace; the kernels never read past it).
  *   bmu        device int32 [N], written: index of the best unit.
  *   dist       device fp64 [N], written: ||x_s - w_bmu||^2.
- *   workspace  device, >= som_bmu_workspace_bytes(N, M, V, nnz) bytes,
- *              256-byte aligned; its contents are scratch.
+ *   workspace  device, >= som_bmu_workspace_bytes(N, M, V, nnz, config)
+ *              bytes, 256-byte aligned; its contents are scratch.
  *   config     NULL or a som_bmu_config (host memory, read during the call).
  * Equivalent to som_bmu_plan, som_bmu_sweep, som_bmu_finalize in order.
  */
@@ -166,7 +169,7 @@ som_status som_bmu_finalize(const float *W, const double *norms, int64_t V, int6
  * saw a valid CSR.
  */
 som_status som_bmu_input_flags(const void *workspace, size_t workspace_bytes, int64_t N, int64_t M, int64_t V,
-                               int64_t nnz, uint32_t *flags, void *stream);
+                               int64_t nnz, const som_bmu_config *config, uint32_t *flags, void *stream);
 
 /*
  * Host check of the CSR input rules (corpus section: sorted descriptor ids

@@ -42,7 +42,7 @@ som_status tile_samples(const som_bmu_config *cfg, int *ta)
     for (int r : cfg->reserved)
         if (r != 0) return fail(SOM_ERR_INVALID_ARG, "som_bmu_config.reserved must be zero");
     if (cfg->tile_samples == 0) return SOM_OK;
-    if (cfg->tile_samples != 8 && cfg->tile_samples != 16 && cfg->tile_samples != 32)
+    if (!som::valid_tile(cfg->tile_samples))
         return fail(SOM_ERR_INVALID_ARG, "tile_samples must be 0, 8, 16 or 32 (got %d)", (int)cfg->tile_samples);
     *ta = cfg->tile_samples;
     return SOM_OK;
@@ -64,14 +64,13 @@ struct Carved {
     int2 *tiles;
     unsigned long long *keys;
     uint32_t *flags;
-    int64_t n_groups;
 };
 
-som_status carve(void *ws, size_t bytes, int64_t N, int64_t M, int64_t nnz, Carved *c)
+som_status carve(void *ws, size_t bytes, int64_t N, int64_t M, int64_t nnz, int ta, Carved *c)
 {
     if (!ws) return fail(SOM_ERR_WORKSPACE, "workspace is NULL");
     if (reinterpret_cast<uintptr_t>(ws) & 255) return fail(SOM_ERR_WORKSPACE, "workspace must be 256-byte aligned");
-    const som::Layout L = som::layout_for(N, M, nnz);
+    const som::Layout L = som::layout_for(N, M, nnz, ta);
     if (bytes < L.total)
         return fail(SOM_ERR_WORKSPACE, "workspace holds %zu bytes, the search needs %zu", bytes, L.total);
     char *b = static_cast<char *>(ws);
@@ -79,7 +78,6 @@ som_status carve(void *ws, size_t bytes, int64_t N, int64_t M, int64_t nnz, Carv
     c->tiles = reinterpret_cast<int2 *>(b + L.tiles);
     c->keys = reinterpret_cast<unsigned long long *>(b + L.keys);
     c->flags = reinterpret_cast<uint32_t *>(b + L.flags);
-    c->n_groups = L.n_groups;
     return SOM_OK;
 }
 
@@ -87,10 +85,14 @@ som_status carve(void *ws, size_t bytes, int64_t N, int64_t M, int64_t nnz, Carv
 
 extern "C" {
 
-size_t som_bmu_workspace_bytes(int64_t N, int64_t M, int64_t V, int64_t nnz)
+size_t som_bmu_workspace_bytes(int64_t N, int64_t M, int64_t V, int64_t nnz, const som_bmu_config *config)
 {
-    if (N < 0 || M < 1 || M > SOM_MAX_NEURONS || V < 1 || nnz < 0) return 0;
-    return som::layout_for(N, M, nnz).total;
+    if (N < 0 || N >= INT32_MAX || M < 1 || M > SOM_MAX_NEURONS || V < 1 || V > INT32_MAX || nnz < 0 ||
+        nnz > INT32_MAX)
+        return 0;
+    int ta;
+    if (tile_samples(config, &ta) != SOM_OK) return 0;
+    return som::layout_for(N, M, nnz, ta).total;
 }
 
 som_status som_codebook_norms(const float *W, int64_t V, int64_t M, double *norms, void *stream)
@@ -114,7 +116,7 @@ som_status som_bmu_plan(const int32_t *row_ptr, const int32_t *col_idx, int64_t 
     if (N == 0) return ok();
     if (!row_ptr || (nnz > 0 && !col_idx)) return fail(SOM_ERR_INVALID_ARG, "som_bmu_plan: null CSR pointer");
     Carved c;
-    if ((st = carve(workspace, workspace_bytes, N, M, nnz, &c)) != SOM_OK) return st;
+    if ((st = carve(workspace, workspace_bytes, N, M, nnz, ta, &c)) != SOM_OK) return st;
     hipStream_t s = static_cast<hipStream_t>(stream);
     hipError_t e = som::launch_clear_flags(c.flags, s);
     if (e != hipSuccess) return hip_fail(e, "som_bmu_plan: flag clear launch");
@@ -134,8 +136,8 @@ som_status som_bmu_sweep(const float *W, const double *norms, int64_t V, int64_t
     if (!W || !norms) return fail(SOM_ERR_INVALID_ARG, "som_bmu_sweep: null pointer");
     if (reinterpret_cast<uintptr_t>(W) & 3) return fail(SOM_ERR_INVALID_ARG, "W must be 4-byte aligned");
     Carved c;
-    if ((st = carve(workspace, workspace_bytes, N, M, nnz, &c)) != SOM_OK) return st;
-    hipError_t e = som::launch_sweep(ta, W, norms, M, N, V, nnz, c.plan, c.tiles, c.keys, c.n_groups,
+    if ((st = carve(workspace, workspace_bytes, N, M, nnz, ta, &c)) != SOM_OK) return st;
+    hipError_t e = som::launch_sweep(ta, W, norms, M, N, V, nnz, c.plan, c.tiles, c.keys,
                                      static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "som_bmu_sweep launch");
     return ok();
@@ -153,8 +155,8 @@ som_status som_bmu_finalize(const float *W, const double *norms, int64_t V, int6
     if (!W || !norms || !row_ptr || (nnz > 0 && !col_idx) || !bmu || !dist)
         return fail(SOM_ERR_INVALID_ARG, "som_bmu_finalize: null pointer");
     Carved c;
-    if ((st = carve(workspace, workspace_bytes, N, M, nnz, &c)) != SOM_OK) return st;
-    hipError_t e = som::launch_finalize(W, norms, V, M, row_ptr, col_idx, N, nnz, c.keys, c.n_groups, bmu, dist,
+    if ((st = carve(workspace, workspace_bytes, N, M, nnz, ta, &c)) != SOM_OK) return st;
+    hipError_t e = som::launch_finalize(ta, W, norms, V, M, row_ptr, col_idx, N, nnz, c.keys, bmu, dist,
                                         static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "som_bmu_finalize launch");
     return ok();
@@ -173,7 +175,7 @@ som_status som_bmu_search(const float *W, const double *norms, int64_t V, int64_
         return fail(SOM_ERR_INVALID_ARG, "som_bmu_search: null pointer");
     if (reinterpret_cast<uintptr_t>(W) & 3) return fail(SOM_ERR_INVALID_ARG, "W must be 4-byte aligned");
     Carved c;
-    if ((st = carve(workspace, workspace_bytes, N, M, nnz, &c)) != SOM_OK) return st;
+    if ((st = carve(workspace, workspace_bytes, N, M, nnz, ta, &c)) != SOM_OK) return st;
     if ((st = som_bmu_plan(row_ptr, col_idx, N, nnz, V, M, workspace, workspace_bytes, config, stream)) != SOM_OK)
         return st;
     if ((st = som_bmu_sweep(W, norms, V, M, N, nnz, workspace, workspace_bytes, config, stream)) != SOM_OK)
@@ -183,15 +185,17 @@ som_status som_bmu_search(const float *W, const double *norms, int64_t V, int64_
 }
 
 som_status som_bmu_input_flags(const void *workspace, size_t workspace_bytes, int64_t N, int64_t M, int64_t V,
-                               int64_t nnz, uint32_t *flags, void *stream)
+                               int64_t nnz, const som_bmu_config *config, uint32_t *flags, void *stream)
 {
     som_status st = check_dims(N, M, V, nnz);
     if (st != SOM_OK) return st;
+    int ta;
+    if ((st = tile_samples(config, &ta)) != SOM_OK) return st;
     if (!flags) return fail(SOM_ERR_INVALID_ARG, "som_bmu_input_flags: flags is NULL");
     *flags = 0;
     if (N == 0) return ok();
     Carved c;
-    if ((st = carve(const_cast<void *>(workspace), workspace_bytes, N, M, nnz, &c)) != SOM_OK) return st;
+    if ((st = carve(const_cast<void *>(workspace), workspace_bytes, N, M, nnz, ta, &c)) != SOM_OK) return st;
     hipStream_t s = static_cast<hipStream_t>(stream);
     hipError_t e = hipStreamSynchronize(s);
     if (e != hipSuccess) return hip_fail(e, "som_bmu_input_flags: stream synchronize");

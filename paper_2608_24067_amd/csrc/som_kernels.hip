@@ -3,17 +3,21 @@
 // Method (SpMM-tile kernel section; Algorithm 2, steps 4-7): samples are
 // grouped into tiles of TA consecutive rows; for each tile the distinct
 // feature ids of its rows form the tile's union, each id carrying a TA-bit
-// mask of the rows that hold it (k_plan). The sweep (k_sweep) gives each
-// wave a strip of 256 neurons (4 per lane) of one tile: it streams the
-// strip's segment of every union row once -- a coalesced 1 KiB read of the
+// mask of the rows that hold it (k_plan). In the sweep (k_sweep) a wave owns
+// one tile and one strip of 64*NPL neurons (NPL per lane): it streams the
+// strip's segment of every union row once -- a coalesced read of the
 // feature-major codebook W[v*M + i] -- and adds it into the register
 // accumulators of every sample whose mask bit is set. A sample's dot product
 // therefore is the fp32 sum of its own weights in ascending feature order,
 // whatever TA is. The argmin is fused: each lane ranks its neurons by
-// d = ||w||^2 - 2*dot in fp64, keeps the smallest 64-bit key per sample, and
-// the wave and workgroup reduce the keys; one key per (sample, group of 1024
-// neurons) leaves the kernel. k_finalize takes the smallest key per sample
-// and recomputes the winner's full squared distance.
+// d = ||w||^2 - 2*dot in fp64 and the wave reduces 64-bit keys per sample;
+// one key per (sample, strip) leaves the kernel. k_finalize takes the
+// smallest key per sample and recomputes the winner's full squared distance.
+//
+// The four waves of a sweep workgroup take four consecutive tiles of the same
+// strip, and blockIdx.y (the strip) is the slowest-varying dispatch index, so
+// the workgroups in flight all read the same narrow column range of the
+// codebook and its frequently used rows stay in L2.
 //
 // Keys: the order-preserving image of the fp64 pattern of d (sign flipped
 // for d >= 0, all bits flipped for d < 0), with its low 20 bits replaced by
@@ -30,6 +34,7 @@ namespace som {
 namespace {
 
 typedef unsigned long long u64;
+typedef float v4f __attribute__((ext_vector_type(4)));
 
 constexpr u64 kKeyNone = ~0ull;
 constexpr u64 kIndexMask = (1ull << 20) - 1;
@@ -43,12 +48,19 @@ __device__ __forceinline__ u64 rank_key(double d, unsigned i)
 
 __device__ __forceinline__ u64 min_u64(u64 a, u64 b) { return b < a ? b : a; }
 
+__device__ __forceinline__ int64_t clamp64(int64_t x, int64_t lo, int64_t hi) { return x < lo ? lo : (x > hi ? hi : x); }
+
+// The wave index as a scalar: threadIdx.x >> 6 is the same in every lane of a
+// wave, but the compiler cannot prove it, and without this every value derived
+// from it (tile index, plan entries, masks) would be treated as divergent.
+__device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }
+
 // ---- cross-lane helpers (DPP within a row of 16 lanes, readlane across rows)
 
 // dpp_ctrl codes: quad_perm [1,0,3,2] = 0xB1 (lane ^ 1), quad_perm [2,3,0,1] = 0x4E
 // (lane ^ 2), row_half_mirror = 0x141 (i <-> 7-i in each 8), row_mirror = 0x140
-// (i <-> 15-i in each 16). Applied in this order every lane of a row ends with the
-// row's minimum.
+// (i <-> 15-i in each 16). After the first k of these steps, every lane holds the
+// minimum of its aligned group of 2, 4, 8 or 16 lanes.
 template <int CTRL>
 __device__ __forceinline__ int dpp(int x)
 {
@@ -63,17 +75,19 @@ __device__ __forceinline__ u64 dpp64(u64 x)
     return ((u64)(unsigned)hi << 32) | (unsigned)lo;
 }
 
-__device__ __forceinline__ int wave_min_i32(int x)
+// Minimum over each aligned group of G lanes (G = 8, 16 or 32), in every lane of the group.
+template <int G>
+__device__ __forceinline__ int group_min_i32(int x)
 {
     x = min(x, dpp<0xB1>(x));
     x = min(x, dpp<0x4E>(x));
     x = min(x, dpp<0x141>(x));
-    x = min(x, dpp<0x140>(x));
-    const int a = __builtin_amdgcn_readlane(x, 0), b = __builtin_amdgcn_readlane(x, 16);
-    const int c = __builtin_amdgcn_readlane(x, 32), d = __builtin_amdgcn_readlane(x, 48);
-    return min(min(a, b), min(c, d));
+    if (G >= 16) x = min(x, dpp<0x140>(x));
+    if (G >= 32) x = min(x, __shfl_xor(x, 16));
+    return x;
 }
 
+// Minimum over the whole wave, as a scalar.
 __device__ __forceinline__ u64 wave_min_u64(u64 x)
 {
     x = min_u64(x, dpp64<0xB1>(x));
@@ -89,8 +103,6 @@ __device__ __forceinline__ u64 wave_min_u64(u64 x)
     }
     return r;
 }
-
-__device__ __forceinline__ int64_t clamp64(int64_t x, int64_t lo, int64_t hi) { return x < lo ? lo : (x > hi ? hi : x); }
 
 // ----------------------------------------------------------------- norms
 
@@ -126,76 +138,92 @@ __global__ void k_clear_flags(uint32_t *flags) { flags[threadIdx.x] = 0u; }
 // ------------------------------------------------------------------ plan
 
 constexpr int kPlanWaves = 4;
-constexpr int kPlanStage = 1024;  // ids of one tile staged in LDS per wave
+constexpr int kPlanStage = 2048;  // ids staged in LDS per wave
 
-// One wave per tile. Lane s < TA walks row t*TA+s; each step takes the smallest
-// current id over the lanes (the next union element, ascending), the ballot of the
-// lanes holding it (its sample mask), and advances those lanes: a TA-way merge of
-// sorted lists. Offsets are clamped to [row_ptr[0], row_ptr[0]+nnz) and to the
-// tile's own range, ids outside [0, V) are skipped, and a tile never writes more
-// than its own CSR span of plan entries, so no input can drive an access out of
-// bounds.
+// A wave plans 64/TA consecutive tiles at once: lane l works on row s = l % TA of
+// tile l / TA. Each step takes, per tile, the smallest current id over its TA
+// lanes (the next element of the union, ascending), the ballot of the lanes
+// holding it (its sample mask), and advances those lanes: a TA-way merge of
+// sorted lists per lane group. Offsets are clamped to [row_ptr[0], row_ptr[0]+nnz)
+// and to each tile's own range, ids outside [0, V) are skipped, and a tile never
+// writes more entries than its own CSR span, so no input can drive an access out
+// of bounds.
 template <int TA>
 __global__ __launch_bounds__(256) void k_plan(const int32_t *__restrict__ row_ptr, const int32_t *__restrict__ col_idx,
                                               int64_t N, int64_t nnz, int32_t V, int64_t n_tiles,
                                               uint2 *__restrict__ plan, int2 *__restrict__ tiles,
                                               uint32_t *__restrict__ flags)
 {
+    constexpr int G = 64 / TA;  // tiles per wave
     __shared__ int32_t stage[kPlanWaves][kPlanStage];
     const int lane = threadIdx.x & 63;
-    const int wv = threadIdx.x >> 6;
+    const int wv = wave_id();
+    const int grp = lane / TA;
+    const int sl = lane % TA;
     const int64_t base = row_ptr[0];
     uint32_t bad = 0;
 
-    for (int64_t t0 = (int64_t)blockIdx.x * kPlanWaves; t0 < n_tiles; t0 += (int64_t)gridDim.x * kPlanWaves) {
-        const int64_t t = t0 + wv;
+    for (int64_t tb = (int64_t)blockIdx.x * kPlanWaves * G; tb < n_tiles; tb += (int64_t)gridDim.x * kPlanWaves * G) {
+        const int64_t tw = tb + (int64_t)wv * G;  // first tile of this wave
+        const int64_t t = tw + grp;               // this lane's tile
         const bool live = t < n_tiles;
+        // the wave's CSR span, for staging
+        int64_t wlo = 0, whi = 0;
+        if (tw < n_tiles) {
+            const int64_t te = tw + G < n_tiles ? tw + G : n_tiles;
+            wlo = clamp64((int64_t)row_ptr[tw * TA] - base, 0, nnz);
+            whi = clamp64((int64_t)row_ptr[te * TA < N ? te * TA : N] - base, wlo, nnz);
+        }
         int64_t lo = 0, hi = 0, b = 0, e = 0;
         if (live) {
             const int64_t s0 = t * TA;
             const int64_t s1 = s0 + TA < N ? s0 + TA : N;
-            lo = clamp64((int64_t)row_ptr[s0] - base, 0, nnz);
-            hi = clamp64((int64_t)row_ptr[s1] - base, lo, nnz);
-            if (lane < TA && s0 + lane < N) {
-                const int64_t rb = (int64_t)row_ptr[s0 + lane] - base;
-                const int64_t re = (int64_t)row_ptr[s0 + lane + 1] - base;
+            lo = clamp64((int64_t)row_ptr[s0] - base, wlo, whi);
+            hi = clamp64((int64_t)row_ptr[s1] - base, lo, whi);
+            if (s0 + sl < N) {
+                const int64_t rb = (int64_t)row_ptr[s0 + sl] - base;
+                const int64_t re = (int64_t)row_ptr[s0 + sl + 1] - base;
                 if (re < rb || rb < lo || re > hi) bad |= SOM_FLAG_ROW_PTR;
                 b = clamp64(rb, lo, hi);
                 e = clamp64(re, b, hi);
             }
         }
-        const bool staged = live && (hi - lo) <= kPlanStage;
+        const bool staged = (whi - wlo) <= kPlanStage;  // wave-uniform
         if (staged)
-            for (int64_t q = lane; q < hi - lo; q += 64) stage[wv][q] = col_idx[base + lo + q];
+            for (int64_t q = lane; q < whi - wlo; q += 64) stage[wv][q] = col_idx[base + wlo + q];
         __syncthreads();
-        if (live) {
-            int64_t p = b;
-            int cur = INT_MAX;
-            // next valid id of this lane's row (INT_MAX when the row is done)
-            auto fetch = [&]() {
-                cur = INT_MAX;
-                while (p < e) {
-                    const int id = staged ? stage[wv][p - lo] : col_idx[base + p];
-                    if (id >= 0 && id < V) {
-                        cur = id;
-                        break;
-                    }
-                    bad |= SOM_FLAG_ID_RANGE;
-                    ++p;
-                }
-            };
-            fetch();
-            const int64_t cap = hi - lo;
-            int64_t k = 0;
-            while (true) {
-                const int m = wave_min_i32(cur);
-                if (m == INT_MAX) break;
-                if (k >= cap) {  // only reachable with repeated or unsorted ids
-                    bad |= SOM_FLAG_UNSORTED;
+
+        int64_t p = b;
+        int cur = INT_MAX;
+        // next valid id of this lane's row (INT_MAX once the row is done)
+        auto fetch = [&]() {
+            cur = INT_MAX;
+            while (p < e) {
+                const int id = staged ? stage[wv][p - wlo] : col_idx[base + p];
+                if (id >= 0 && id < V) {
+                    cur = id;
                     break;
                 }
-                const u64 mask = __ballot(cur == m);
-                if (lane == 0) plan[lo + k] = make_uint2((unsigned)m, (unsigned)mask);
+                bad |= SOM_FLAG_ID_RANGE;
+                ++p;
+            }
+        };
+        fetch();
+        const int64_t cap = hi - lo;
+        int64_t k = 0;  // union entries written for this lane's tile (equal across its group)
+        while (true) {
+            int m = group_min_i32<TA>(cur);
+            if (m != INT_MAX && k >= cap) {  // only reachable with repeated or unsorted ids
+                bad |= SOM_FLAG_UNSORTED;
+                p = e;
+                cur = INT_MAX;
+                m = INT_MAX;
+            }
+            if (__ballot(m != INT_MAX) == 0) break;
+            const u64 bal = __ballot(m != INT_MAX && cur == m);
+            const unsigned mask = (unsigned)((bal >> (grp * TA)) & (TA == 32 ? 0xFFFFFFFFull : ((1ull << TA) - 1)));
+            if (m != INT_MAX) {
+                if (sl == 0) plan[lo + k] = make_uint2((unsigned)m, mask);
                 ++k;
                 if (cur == m) {
                     ++p;
@@ -203,8 +231,8 @@ __global__ __launch_bounds__(256) void k_plan(const int32_t *__restrict__ row_pt
                     if (cur != INT_MAX && cur <= m) bad |= SOM_FLAG_UNSORTED;
                 }
             }
-            if (lane == 0) tiles[t] = make_int2((int)lo, (int)k);
         }
+        if (live && sl == 0) tiles[t] = make_int2((int)lo, (int)k);
         __syncthreads();
     }
     if (bad) atomicOr(flags, bad);
@@ -212,128 +240,128 @@ __global__ __launch_bounds__(256) void k_plan(const int32_t *__restrict__ row_pt
 
 // ----------------------------------------------------------------- sweep
 
-// One workgroup = 4 waves = one tile x 1024 neurons (blockIdx.y selects the group
-// of neurons, blockIdx.x strides over tiles, so the workgroups in flight share
-// one group of codebook columns). Lane l of wave w owns neurons
-// i0 = group*1024 + w*256 + 4*l .. i0+3. Lanes past M load a valid address and
-// are never ranked.
-// The plan is read defensively: offsets, counts and ids are clamped to the
-// workspace and the codebook, so even a workspace the plan never wrote cannot
+// Workgroup = 4 waves = 4 consecutive tiles x one strip (blockIdx.y) of 64*NPL
+// neurons; lane l owns neurons i0 = strip*64*NPL + NPL*l .. i0+NPL-1. VEC: M is a
+// multiple of NPL and W 16-byte aligned, so each lane's NPL weights of a row are
+// NPL/4 aligned 16-byte loads; lanes past M load a valid address and are never
+// ranked. The plan is read defensively (offsets, counts and ids clamped to the
+// workspace and the codebook), so even a workspace the plan never wrote cannot
 // drive an access out of bounds.
-template <int TA, bool VEC>
+template <int TA, int NPL, bool VEC>
 __global__ __launch_bounds__(256) void k_sweep(const float *__restrict__ W, const double *__restrict__ norms,
                                                int64_t M, int64_t N, int64_t V, int64_t nnz,
                                                const uint2 *__restrict__ plan, const int2 *__restrict__ tiles,
                                                int64_t n_tiles, u64 *__restrict__ keys)
 {
-    __shared__ u64 red[kSweepWaves][TA];
+    constexpr int U = 4;  // codebook rows in flight per wave
     const int lane = threadIdx.x & 63;
-    const int wv = threadIdx.x >> 6;
-    const int64_t g = blockIdx.y;
-    const int64_t i0 = g * kGroupNeurons + (int64_t)wv * kStripNeurons + (int64_t)lane * kNeuronsPerLane;
+    const int wv = wave_id();
+    const int64_t strip = blockIdx.y;
+    const int64_t i0 = strip * (64 * NPL) + (int64_t)lane * NPL;
 
-    // load columns: clamped so that every lane reads inside row v
-    int64_t col[4];
+    int64_t col[NPL];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) col[j] = VEC ? (i0 < M ? i0 : M - 4) + j : (i0 + j < M ? i0 + j : M - 1);
-    double nrm[4];
+    for (int j = 0; j < NPL; ++j) col[j] = VEC ? (i0 < M ? i0 : M - NPL) + j : (i0 + j < M ? i0 + j : M - 1);
+    double nrm[NPL];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) nrm[j] = norms[col[j]];
+    for (int j = 0; j < NPL; ++j) nrm[j] = norms[col[j]];
+    const unsigned vmax = (unsigned)(V - 1);
 
-    for (int64_t t = blockIdx.x; t < n_tiles; t += gridDim.x) {
+    for (int64_t tg = blockIdx.x; tg * 4 < n_tiles; tg += gridDim.x) {
+        const int64_t t = tg * 4 + wv;
+        if (t >= n_tiles) break;  // wave-uniform; this kernel has no barriers
         const int2 te = tiles[t];
         const int64_t off = clamp64(te.x, 0, nnz);
         const uint2 *ent = plan + off;
         const int cnt = (int)clamp64(te.y, 0, nnz - off);
-        const unsigned vmax = (unsigned)(V - 1);
 
-        float acc[TA][4];
+        float acc[TA][NPL];
 #pragma unroll
         for (int s = 0; s < TA; ++s)
 #pragma unroll
-            for (int j = 0; j < 4; ++j) acc[s][j] = 0.0f;
+            for (int j = 0; j < NPL; ++j) acc[s][j] = 0.0f;
 
-        auto row_load = [&](unsigned id, float w[4]) {
+        auto row_load = [&](unsigned id, float w[NPL]) {
             const float *r = W + (size_t)(id < vmax ? id : vmax) * (size_t)M;
             if (VEC) {
-                const float4 q = *reinterpret_cast<const float4 *>(r + col[0]);
-                w[0] = q.x;
-                w[1] = q.y;
-                w[2] = q.z;
-                w[3] = q.w;
+#pragma unroll
+                for (int j = 0; j < NPL; j += 4) {
+                    const v4f q = *reinterpret_cast<const v4f *>(r + col[j]);
+                    w[j] = q.x;
+                    w[j + 1] = q.y;
+                    w[j + 2] = q.z;
+                    w[j + 3] = q.w;
+                }
             } else {
 #pragma unroll
-                for (int j = 0; j < 4; ++j) w[j] = r[col[j]];
+                for (int j = 0; j < NPL; ++j) w[j] = r[col[j]];
             }
         };
-        auto row_add = [&](unsigned mask, const float w[4]) {
+        // The mask is wave-uniform: each bit is a scalar branch. The empty volatile
+        // asm keeps the compiler from turning the branch into unconditional adds
+        // and selects.
+        auto row_add = [&](unsigned mask, const float w[NPL]) {
 #pragma unroll
             for (int s = 0; s < TA; ++s) {
                 if (mask & (1u << s)) {
 #pragma unroll
-                    for (int j = 0; j < 4; ++j) acc[s][j] += w[j];
+                    for (int j = 0; j < NPL; ++j) acc[s][j] += w[j];
+                    asm volatile("");
                 }
             }
         };
 
         int k = 0;
-        for (; k + 4 <= cnt; k += 4) {
-            uint2 en[4];
-            float w[4][4];
+        for (; k + U <= cnt; k += U) {
+            uint2 en[U];
+            float w[U][NPL];
 #pragma unroll
-            for (int u = 0; u < 4; ++u) en[u] = ent[k + u];
+            for (int u = 0; u < U; ++u) en[u] = ent[k + u];
 #pragma unroll
-            for (int u = 0; u < 4; ++u) row_load(en[u].x, w[u]);
+            for (int u = 0; u < U; ++u) row_load(en[u].x, w[u]);
 #pragma unroll
-            for (int u = 0; u < 4; ++u) row_add(en[u].y, w[u]);
+            for (int u = 0; u < U; ++u) row_add(en[u].y, w[u]);
         }
         for (; k < cnt; ++k) {
             const uint2 en = ent[k];
-            float w[4];
+            float w[NPL];
             row_load(en.x, w);
             row_add(en.y, w);
         }
 
-        // fused argmin: d = ||w||^2 - 2*dot (fp64, one rounding), keyed
+        // fused argmin: d = ||w||^2 - 2*dot (fp64, one rounding), keyed; lane s keeps sample s
+        u64 mine = kKeyNone;
 #pragma unroll
         for (int s = 0; s < TA; ++s) {
             u64 best = kKeyNone;
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
+            for (int j = 0; j < NPL; ++j) {
                 const double d = fma(-2.0, (double)acc[s][j], nrm[j]);
                 const u64 key = (i0 + j < M) ? rank_key(d, (unsigned)(i0 + j)) : kKeyNone;
                 best = min_u64(best, key);
             }
             best = wave_min_u64(best);
-            if (lane == 0) red[wv][s] = best;
+            if (lane == s) mine = best;
         }
-        __syncthreads();
-        if (threadIdx.x < TA) {
-            const int s = threadIdx.x;
-            u64 m = red[0][s];
-#pragma unroll
-            for (int w = 1; w < kSweepWaves; ++w) m = min_u64(m, red[w][s]);
-            const int64_t row = t * TA + s;
-            if (row < N) keys[g * N + row] = m;
-        }
-        __syncthreads();
+        const int64_t row = t * TA + lane;
+        if (lane < TA && row < N) keys[strip * N + row] = mine;
     }
 }
 
 // -------------------------------------------------------------- finalize
 
-// One thread per sample: smallest key over the groups, then the winner's distance
+// One thread per sample: smallest key over the strips, then the winner's distance
 // from the sample's own ids, summed in the same order and precision as the sweep.
 __global__ __launch_bounds__(256) void k_finalize(const float *__restrict__ W, const double *__restrict__ norms,
                                                   int32_t V, int64_t M, const int32_t *__restrict__ row_ptr,
                                                   const int32_t *__restrict__ col_idx, int64_t N, int64_t nnz,
-                                                  const u64 *__restrict__ keys, int64_t n_groups,
+                                                  const u64 *__restrict__ keys, int64_t n_strips,
                                                   int32_t *__restrict__ bmu, double *__restrict__ dist)
 {
     const int64_t base = row_ptr[0];
     for (int64_t s = (int64_t)blockIdx.x * 256 + threadIdx.x; s < N; s += (int64_t)gridDim.x * 256) {
         u64 best = kKeyNone;
-        for (int64_t g = 0; g < n_groups; ++g) best = min_u64(best, keys[g * N + s]);
+        for (int64_t g = 0; g < n_strips; ++g) best = min_u64(best, keys[g * N + s]);
         int64_t b = (int64_t)(best & kIndexMask);
         if (b >= M) b = M - 1;
         const int64_t rb = clamp64((int64_t)row_ptr[s] - base, 0, nnz);
@@ -372,56 +400,58 @@ hipError_t launch_clear_flags(uint32_t *flags, hipStream_t st)
 hipError_t launch_plan(int ta, const int32_t *row_ptr, const int32_t *col_idx, int64_t N, int64_t nnz, int64_t V,
                        uint2 *plan, int2 *tiles, uint32_t *flags, hipStream_t st)
 {
-    const int64_t n_tiles = (N + ta - 1) / ta;
-    int64_t blocks = (n_tiles + kPlanWaves - 1) / kPlanWaves;
+    const int64_t nt = n_tiles(N, ta);
+    const int64_t per_block = (int64_t)kPlanWaves * (64 / ta);
+    int64_t blocks = (nt + per_block - 1) / per_block;
     if (blocks > (1 << 22)) blocks = 1 << 22;
     const dim3 grid((unsigned)blocks), block(256);
     switch (ta) {
-    case 8: hipLaunchKernelGGL(k_plan<8>, grid, block, 0, st, row_ptr, col_idx, N, nnz, (int32_t)V, n_tiles, plan, tiles, flags); break;
-    case 16: hipLaunchKernelGGL(k_plan<16>, grid, block, 0, st, row_ptr, col_idx, N, nnz, (int32_t)V, n_tiles, plan, tiles, flags); break;
-    case 32: hipLaunchKernelGGL(k_plan<32>, grid, block, 0, st, row_ptr, col_idx, N, nnz, (int32_t)V, n_tiles, plan, tiles, flags); break;
+    case 8: hipLaunchKernelGGL(k_plan<8>, grid, block, 0, st, row_ptr, col_idx, N, nnz, (int32_t)V, nt, plan, tiles, flags); break;
+    case 16: hipLaunchKernelGGL(k_plan<16>, grid, block, 0, st, row_ptr, col_idx, N, nnz, (int32_t)V, nt, plan, tiles, flags); break;
+    case 32: hipLaunchKernelGGL(k_plan<32>, grid, block, 0, st, row_ptr, col_idx, N, nnz, (int32_t)V, nt, plan, tiles, flags); break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
 }
 
-template <int TA>
+template <int TA, int NPL>
 static void sweep_ta(bool vec, dim3 grid, hipStream_t st, const float *W, const double *norms, int64_t M, int64_t N,
-                     int64_t V, int64_t nnz, const uint2 *plan, const int2 *tiles, int64_t n_tiles, u64 *keys)
+                     int64_t V, int64_t nnz, const uint2 *plan, const int2 *tiles, int64_t nt, u64 *keys)
 {
     if (vec)
-        hipLaunchKernelGGL((k_sweep<TA, true>), grid, dim3(256), 0, st, W, norms, M, N, V, nnz, plan, tiles, n_tiles,
+        hipLaunchKernelGGL((k_sweep<TA, NPL, true>), grid, dim3(256), 0, st, W, norms, M, N, V, nnz, plan, tiles, nt,
                            keys);
     else
-        hipLaunchKernelGGL((k_sweep<TA, false>), grid, dim3(256), 0, st, W, norms, M, N, V, nnz, plan, tiles,
-                           n_tiles, keys);
+        hipLaunchKernelGGL((k_sweep<TA, NPL, false>), grid, dim3(256), 0, st, W, norms, M, N, V, nnz, plan, tiles, nt,
+                           keys);
 }
 
 hipError_t launch_sweep(int ta, const float *W, const double *norms, int64_t M, int64_t N, int64_t V, int64_t nnz,
-                        const uint2 *plan, const int2 *tiles, unsigned long long *keys, int64_t n_groups,
-                        hipStream_t st)
+                        const uint2 *plan, const int2 *tiles, unsigned long long *keys, hipStream_t st)
 {
-    const int64_t n_tiles = (N + ta - 1) / ta;
-    int64_t gx = n_tiles > (1 << 22) ? (1 << 22) : n_tiles;
-    const dim3 grid((unsigned)gx, (unsigned)n_groups);
-    const bool vec = (M % 4 == 0) && ((reinterpret_cast<uintptr_t>(W) & 15) == 0);
+    const int64_t nt = n_tiles(N, ta);
+    int64_t gx = (nt + 3) / 4;
+    if (gx > (1 << 22)) gx = 1 << 22;
+    const dim3 grid((unsigned)gx, (unsigned)n_strips(M, ta));
+    const int npl = neurons_per_lane(ta);
+    const bool vec = (M % npl == 0) && ((reinterpret_cast<uintptr_t>(W) & 15) == 0);
     switch (ta) {
-    case 8: sweep_ta<8>(vec, grid, st, W, norms, M, N, V, nnz, plan, tiles, n_tiles, keys); break;
-    case 16: sweep_ta<16>(vec, grid, st, W, norms, M, N, V, nnz, plan, tiles, n_tiles, keys); break;
-    case 32: sweep_ta<32>(vec, grid, st, W, norms, M, N, V, nnz, plan, tiles, n_tiles, keys); break;
+    case 8: sweep_ta<8, 8>(vec, grid, st, W, norms, M, N, V, nnz, plan, tiles, nt, keys); break;
+    case 16: sweep_ta<16, 4>(vec, grid, st, W, norms, M, N, V, nnz, plan, tiles, nt, keys); break;
+    case 32: sweep_ta<32, 4>(vec, grid, st, W, norms, M, N, V, nnz, plan, tiles, nt, keys); break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
 }
 
-hipError_t launch_finalize(const float *W, const double *norms, int64_t V, int64_t M, const int32_t *row_ptr,
+hipError_t launch_finalize(int ta, const float *W, const double *norms, int64_t V, int64_t M, const int32_t *row_ptr,
                            const int32_t *col_idx, int64_t N, int64_t nnz, const unsigned long long *keys,
-                           int64_t n_groups, int32_t *bmu, double *dist, hipStream_t st)
+                           int32_t *bmu, double *dist, hipStream_t st)
 {
     int64_t blocks = (N + 255) / 256;
     if (blocks > (1 << 22)) blocks = 1 << 22;
     hipLaunchKernelGGL(k_finalize, dim3((unsigned)blocks), dim3(256), 0, st, W, norms, (int32_t)V, M, row_ptr,
-                       col_idx, N, nnz, keys, n_groups, bmu, dist);
+                       col_idx, N, nnz, keys, n_strips(M, ta), bmu, dist);
     return hipGetLastError();
 }
 

@@ -54,14 +54,14 @@ def load():
     lib = ctypes.CDLL(_LIB_PATH)
     i64, vp, sz = ctypes.c_int64, ctypes.c_void_p, ctypes.c_size_t
     cfgp = ctypes.POINTER(_Config)
-    lib.som_bmu_workspace_bytes.argtypes = [i64, i64, i64, i64]
+    lib.som_bmu_workspace_bytes.argtypes = [i64, i64, i64, i64, cfgp]
     lib.som_bmu_workspace_bytes.restype = sz
     lib.som_codebook_norms.argtypes = [vp, i64, i64, vp, vp]
     lib.som_bmu_search.argtypes = [vp, vp, i64, i64, vp, vp, i64, i64, vp, vp, vp, sz, cfgp, vp]
     lib.som_bmu_plan.argtypes = [vp, vp, i64, i64, i64, i64, vp, sz, cfgp, vp]
     lib.som_bmu_sweep.argtypes = [vp, vp, i64, i64, i64, i64, vp, sz, cfgp, vp]
     lib.som_bmu_finalize.argtypes = [vp, vp, i64, i64, vp, vp, i64, i64, vp, vp, vp, sz, cfgp, vp]
-    lib.som_bmu_input_flags.argtypes = [vp, sz, i64, i64, i64, i64, ctypes.POINTER(ctypes.c_uint32), vp]
+    lib.som_bmu_input_flags.argtypes = [vp, sz, i64, i64, i64, i64, cfgp, ctypes.POINTER(ctypes.c_uint32), vp]
     lib.som_validate_csr_host.argtypes = [vp, vp, i64, i64]
     for name in ("som_codebook_norms", "som_bmu_search", "som_bmu_plan", "som_bmu_sweep", "som_bmu_finalize",
                  "som_bmu_input_flags", "som_validate_csr_host"):
@@ -105,15 +105,15 @@ def _cfg(tile_samples: int):
     return ctypes.byref(c)
 
 
-def workspace_bytes(N: int, M: int, V: int, nnz: int) -> int:
-    n = load().som_bmu_workspace_bytes(N, M, V, nnz)
+def workspace_bytes(N: int, M: int, V: int, nnz: int, tile_samples: int = 0) -> int:
+    n = load().som_bmu_workspace_bytes(N, M, V, nnz, _cfg(tile_samples))
     if n == 0:
-        raise ValueError("som_bmu_workspace_bytes: invalid sizes")
+        raise ValueError("som_bmu_workspace_bytes: invalid sizes or config")
     return n
 
 
-def alloc_workspace(N: int, M: int, V: int, nnz: int, device) -> torch.Tensor:
-    return torch.empty(workspace_bytes(N, M, V, nnz), dtype=torch.uint8, device=device)
+def alloc_workspace(N: int, M: int, V: int, nnz: int, device, tile_samples: int = 0) -> torch.Tensor:
+    return torch.empty(workspace_bytes(N, M, V, nnz, tile_samples), dtype=torch.uint8, device=device)
 
 
 def codebook_norms(W: torch.Tensor, V: int, M: int, out: torch.Tensor | None = None) -> torch.Tensor:
@@ -153,7 +153,7 @@ def bmu_search(W, norms, row_ptr, col_idx, V: int, M: int, nnz: int | None = Non
     if dist is None:
         dist = torch.empty(N, dtype=torch.float64, device=dev)
     if workspace is None:
-        workspace = alloc_workspace(N, M, V, nnz, dev)
+        workspace = alloc_workspace(N, M, V, nnz, dev, tile_samples)
     if W.numel() != V * M:
         raise ValueError("W must hold V*M elements")
     rp, ci = _csr(row_ptr, col_idx, N, nnz)
@@ -194,11 +194,11 @@ def bmu_finalize(W, norms, row_ptr, col_idx, V: int, M: int, nnz: int, bmu, dist
     _check(st, "som_bmu_finalize")
 
 
-def input_flags(workspace, N: int, M: int, V: int, nnz: int) -> int:
+def input_flags(workspace, N: int, M: int, V: int, nnz: int, tile_samples: int = 0) -> int:
     """SOM_FLAG_* bits the last plan recorded (waits for the current stream)."""
     out = ctypes.c_uint32(0)
     st = load().som_bmu_input_flags(_dev(workspace, "workspace", torch.uint8), workspace.numel(), N, M, V, nnz,
-                                    ctypes.byref(out), _stream(workspace))
+                                    _cfg(tile_samples), ctypes.byref(out), _stream(workspace))
     _check(st, "som_bmu_input_flags")
     return int(out.value)
 

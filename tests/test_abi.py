@@ -38,10 +38,13 @@ def test_workspace_bytes():
     assert som.workspace_bytes(10_000, 4096, 2000, 120_000) > n
     assert som.workspace_bytes(10_000, 256, 2000, 240_000) > n
     lib = som.load()
-    assert lib.som_bmu_workspace_bytes(-1, 256, 2000, 0) == 0
-    assert lib.som_bmu_workspace_bytes(10, 0, 2000, 0) == 0
-    assert lib.som_bmu_workspace_bytes(10, (1 << 20) + 1, 2000, 0) == 0
-    assert lib.som_bmu_workspace_bytes(10, 1 << 20, 2000, 0) > 0
+    assert lib.som_bmu_workspace_bytes(-1, 256, 2000, 0, None) == 0
+    assert lib.som_bmu_workspace_bytes(10, 0, 2000, 0, None) == 0
+    assert lib.som_bmu_workspace_bytes(10, (1 << 20) + 1, 2000, 0, None) == 0
+    assert lib.som_bmu_workspace_bytes(10, 1 << 20, 2000, 0, None) > 0
+    assert lib.som_bmu_workspace_bytes(10, 256, 2000, 0, _cfg(7)) == 0
+    # larger tiles use narrower strips, hence more partial keys
+    assert som.workspace_bytes(10_000, 4096, 2000, 0, 16) > som.workspace_bytes(10_000, 4096, 2000, 0, 8)
 
 
 def _status(rp, ci, V):
@@ -132,5 +135,5 @@ def test_phase_and_norms_argument_checks():
     assert lib.som_bmu_finalize(FAKE, FAKE, 100, 64, FAKE, FAKE, 10, 50, FAKE, FAKE, FAKE, 100, None,
                                 None) == som.SOM_ERR_WORKSPACE
     out = ctypes.c_uint32(7)
-    assert lib.som_bmu_input_flags(FAKE, 100, 10, 64, 100, 50, ctypes.byref(out), None) == som.SOM_ERR_WORKSPACE
-    assert lib.som_bmu_input_flags(FAKE, 100, 10, 64, 100, 50, None, None) == som.SOM_ERR_INVALID_ARG
+    assert lib.som_bmu_input_flags(FAKE, 100, 10, 64, 100, 50, None, ctypes.byref(out), None) == som.SOM_ERR_WORKSPACE
+    assert lib.som_bmu_input_flags(FAKE, 100, 10, 64, 100, 50, None, None, None) == som.SOM_ERR_INVALID_ARG
