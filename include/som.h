@@ -79,16 +79,24 @@ typedef enum {
 #define SOM_FLAG_ROW_PTR 0x4u    /* row_ptr decreased or left [row_ptr[0], +nnz]  */
 
 /*
- * Optional tuning of the search. Pass NULL for the defaults.
+ * Optional tuning of the search. Pass NULL for the defaults. Neither field
+ * changes any result: a sample's sum order is fixed by its own features, so
+ * its BMU and distance do not depend on the tile it lands in.
  *   tile_samples  samples per tile, TA (SpMM-tile kernel section): 8, 16 or
- *                 32; 0 selects 8. Results do not depend on it: each
- *                 sample's sum order is fixed by its own feature order.
+ *                 32; 0 selects 8.
+ *   keep_order    0 (default): the plan first regroups the batch by each
+ *                 sample's least frequent feature (the post-submission
+ *                 section's lever of clustering samples so tiles share
+ *                 features), which shrinks tile unions and keeps rare
+ *                 codebook rows in cache; results still come out in input
+ *                 order. 1: tile the samples in the order given.
  * The same config must be given to the workspace query and to every phase
  * of one search.
  */
 typedef struct {
     int32_t tile_samples;
-    int32_t reserved[7]; /* must be zero */
+    int32_t keep_order;
+    int32_t reserved[6]; /* must be zero */
 } som_bmu_config;
 
 /*
@@ -96,8 +104,10 @@ typedef struct {
  * M neurons and V features, needs under `config` (NULL = defaults). Pure
  * host function; returns 0 if a size is out of range (see som_bmu_search)
  * or the config is invalid. The workspace must be 256-byte aligned device
- * memory. It holds the tile plan (8 bytes per id) and one 8-byte partial key
- * per sample and strip of 512 neurons (256 when tile_samples > 8).
+ * memory. It holds the tile plan (8 bytes per id), one 8-byte partial key
+ * per sample and strip of 512 neurons (256 when tile_samples > 8) and, unless
+ * keep_order is set, the regrouped batch (4 bytes per id, 16 per sample, 12
+ * per feature).
  */
 size_t som_bmu_workspace_bytes(int64_t N, int64_t M, int64_t V, int64_t nnz, const som_bmu_config *config);
 
@@ -135,9 +145,11 @@ som_status som_bmu_search(const float *W, const double *norms, int64_t V, int64_
  * left in the same workspace, so they must run in this order on one stream.
  *
  * som_bmu_plan -- tile plan (Algorithm 2, step 5; SpMM-tile kernel section):
- *   for each tile of tile_samples consecutive rows, the ascending list of the
- *   distinct feature ids its rows touch, each with a bit mask of the rows
- *   that hold it. Also clears and sets the input flags.
+ *   unless keep_order is set, the batch is first regrouped by each sample's
+ *   least frequent feature (a permuted copy in the workspace); then, for each
+ *   tile of tile_samples consecutive rows, the ascending list of the distinct
+ *   feature ids its rows hold, each with a bit mask of the rows holding it.
+ *   Also clears and sets the input flags.
  */
 som_status som_bmu_plan(const int32_t *row_ptr, const int32_t *col_idx, int64_t N, int64_t nnz, int64_t V,
                         int64_t M, void *workspace, size_t workspace_bytes, const som_bmu_config *config,
@@ -153,7 +165,7 @@ som_status som_bmu_sweep(const float *W, const double *norms, int64_t V, int64_t
                          void *workspace, size_t workspace_bytes, const som_bmu_config *config, void *stream);
 
 /*
- * som_bmu_finalize -- reduces the per-group keys of each sample to its BMU
+ * som_bmu_finalize -- reduces the per-strip keys of each sample to its BMU
  *   and recomputes the winner's distance from the sample's own ids:
  *   dist = (||w_bmu||^2 - 2*dot) + nnz(x), the dot summed exactly as in the
  *   sweep. Writes bmu and dist.

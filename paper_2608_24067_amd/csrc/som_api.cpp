@@ -34,17 +34,27 @@ som_status ok()
     return SOM_OK;
 }
 
-// Tile size from the optional config.
-som_status tile_samples(const som_bmu_config *cfg, int *ta)
+struct Opts {
+    int ta;      // samples per tile
+    bool order;  // reorder samples by their least frequent feature
+};
+
+// Options from the optional config.
+som_status parse(const som_bmu_config *cfg, Opts *o)
 {
-    *ta = som::kDefaultTileSamples;
+    o->ta = som::kDefaultTileSamples;
+    o->order = true;
     if (!cfg) return SOM_OK;
     for (int r : cfg->reserved)
         if (r != 0) return fail(SOM_ERR_INVALID_ARG, "som_bmu_config.reserved must be zero");
-    if (cfg->tile_samples == 0) return SOM_OK;
-    if (!som::valid_tile(cfg->tile_samples))
-        return fail(SOM_ERR_INVALID_ARG, "tile_samples must be 0, 8, 16 or 32 (got %d)", (int)cfg->tile_samples);
-    *ta = cfg->tile_samples;
+    if (cfg->tile_samples != 0) {
+        if (!som::valid_tile(cfg->tile_samples))
+            return fail(SOM_ERR_INVALID_ARG, "tile_samples must be 0, 8, 16 or 32 (got %d)", (int)cfg->tile_samples);
+        o->ta = cfg->tile_samples;
+    }
+    if (cfg->keep_order != 0 && cfg->keep_order != 1)
+        return fail(SOM_ERR_INVALID_ARG, "keep_order must be 0 or 1 (got %d)", (int)cfg->keep_order);
+    o->order = cfg->keep_order == 0;
     return SOM_OK;
 }
 
@@ -53,7 +63,7 @@ som_status check_dims(int64_t N, int64_t M, int64_t V, int64_t nnz)
     if (N < 0 || N >= INT32_MAX) return fail(SOM_ERR_INVALID_ARG, "N must be in [0, 2^31-1) (got %lld)", (long long)N);
     if (M < 1 || M > SOM_MAX_NEURONS)
         return fail(SOM_ERR_INVALID_ARG, "M must be in [1, %d] (got %lld)", SOM_MAX_NEURONS, (long long)M);
-    if (V < 1 || V > INT32_MAX) return fail(SOM_ERR_INVALID_ARG, "V must be in [1, 2^31-1] (got %lld)", (long long)V);
+    if (V < 1 || V >= INT32_MAX) return fail(SOM_ERR_INVALID_ARG, "V must be in [1, 2^31-1) (got %lld)", (long long)V);
     if (nnz < 0 || nnz > INT32_MAX)
         return fail(SOM_ERR_INVALID_ARG, "nnz must be in [0, 2^31-1] (got %lld)", (long long)nnz);
     return SOM_OK;
@@ -64,13 +74,14 @@ struct Carved {
     int2 *tiles;
     unsigned long long *keys;
     uint32_t *flags;
+    som::OrderBuffers ob;
 };
 
-som_status carve(void *ws, size_t bytes, int64_t N, int64_t M, int64_t nnz, int ta, Carved *c)
+som_status carve(void *ws, size_t bytes, int64_t N, int64_t M, int64_t V, int64_t nnz, const Opts &o, Carved *c)
 {
     if (!ws) return fail(SOM_ERR_WORKSPACE, "workspace is NULL");
     if (reinterpret_cast<uintptr_t>(ws) & 255) return fail(SOM_ERR_WORKSPACE, "workspace must be 256-byte aligned");
-    const som::Layout L = som::layout_for(N, M, nnz, ta);
+    const som::Layout L = som::layout_for(N, M, V, nnz, o.ta, o.order);
     if (bytes < L.total)
         return fail(SOM_ERR_WORKSPACE, "workspace holds %zu bytes, the search needs %zu", bytes, L.total);
     char *b = static_cast<char *>(ws);
@@ -78,7 +89,24 @@ som_status carve(void *ws, size_t bytes, int64_t N, int64_t M, int64_t nnz, int 
     c->tiles = reinterpret_cast<int2 *>(b + L.tiles);
     c->keys = reinterpret_cast<unsigned long long *>(b + L.keys);
     c->flags = reinterpret_cast<uint32_t *>(b + L.flags);
+    c->ob.freq = reinterpret_cast<uint32_t *>(b + L.freq);
+    c->ob.bucket = reinterpret_cast<unsigned long long *>(b + L.bucket);
+    c->ob.skey = reinterpret_cast<int32_t *>(b + L.skey);
+    c->ob.perm = reinterpret_cast<int32_t *>(b + L.perm);
+    c->ob.prp = reinterpret_cast<int32_t *>(b + L.prp);
+    c->ob.pci = reinterpret_cast<int32_t *>(b + L.pci);
     return SOM_OK;
+}
+
+// Common prologue of the phases: options, N == 0 (a no-op), workspace.
+som_status setup(int64_t N, int64_t M, int64_t V, int64_t nnz, const som_bmu_config *config, void *workspace,
+                 size_t workspace_bytes, Opts *o, Carved *c, bool *noop)
+{
+    som_status st = parse(config, o);
+    if (st != SOM_OK) return st;
+    *noop = N == 0;
+    if (*noop) return SOM_OK;
+    return carve(workspace, workspace_bytes, N, M, V, nnz, *o, c);
 }
 
 }  // namespace
@@ -87,19 +115,19 @@ extern "C" {
 
 size_t som_bmu_workspace_bytes(int64_t N, int64_t M, int64_t V, int64_t nnz, const som_bmu_config *config)
 {
-    if (N < 0 || N >= INT32_MAX || M < 1 || M > SOM_MAX_NEURONS || V < 1 || V > INT32_MAX || nnz < 0 ||
+    if (N < 0 || N >= INT32_MAX || M < 1 || M > SOM_MAX_NEURONS || V < 1 || V >= INT32_MAX || nnz < 0 ||
         nnz > INT32_MAX)
         return 0;
-    int ta;
-    if (tile_samples(config, &ta) != SOM_OK) return 0;
-    return som::layout_for(N, M, nnz, ta).total;
+    Opts o;
+    if (parse(config, &o) != SOM_OK) return 0;
+    return som::layout_for(N, M, V, nnz, o.ta, o.order).total;
 }
 
 som_status som_codebook_norms(const float *W, int64_t V, int64_t M, double *norms, void *stream)
 {
     if (!W || !norms) return fail(SOM_ERR_INVALID_ARG, "som_codebook_norms: null pointer");
-    if (M < 1 || M > SOM_MAX_NEURONS || V < 1 || V > INT32_MAX)
-        return fail(SOM_ERR_INVALID_ARG, "som_codebook_norms: need 1 <= M <= %d and 1 <= V < 2^31", SOM_MAX_NEURONS);
+    if (M < 1 || M > SOM_MAX_NEURONS || V < 1 || V >= INT32_MAX)
+        return fail(SOM_ERR_INVALID_ARG, "som_codebook_norms: need 1 <= M <= %d and 1 <= V < 2^31-1", SOM_MAX_NEURONS);
     if (reinterpret_cast<uintptr_t>(W) & 3) return fail(SOM_ERR_INVALID_ARG, "W must be 4-byte aligned");
     hipError_t e = som::launch_norms(W, V, M, norms, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "som_codebook_norms launch");
@@ -109,18 +137,25 @@ som_status som_codebook_norms(const float *W, int64_t V, int64_t M, double *norm
 som_status som_bmu_plan(const int32_t *row_ptr, const int32_t *col_idx, int64_t N, int64_t nnz, int64_t V, int64_t M,
                         void *workspace, size_t workspace_bytes, const som_bmu_config *config, void *stream)
 {
+    Opts o;
+    Carved c;
+    bool noop;
     som_status st = check_dims(N, M, V, nnz);
     if (st != SOM_OK) return st;
-    int ta;
-    if ((st = tile_samples(config, &ta)) != SOM_OK) return st;
-    if (N == 0) return ok();
-    if (!row_ptr || (nnz > 0 && !col_idx)) return fail(SOM_ERR_INVALID_ARG, "som_bmu_plan: null CSR pointer");
-    Carved c;
-    if ((st = carve(workspace, workspace_bytes, N, M, nnz, ta, &c)) != SOM_OK) return st;
+    if (N > 0 && (!row_ptr || (nnz > 0 && !col_idx))) return fail(SOM_ERR_INVALID_ARG, "som_bmu_plan: null CSR pointer");
+    if ((st = setup(N, M, V, nnz, config, workspace, workspace_bytes, &o, &c, &noop)) != SOM_OK) return st;
+    if (noop) return ok();
     hipStream_t s = static_cast<hipStream_t>(stream);
     hipError_t e = som::launch_clear_flags(c.flags, s);
     if (e != hipSuccess) return hip_fail(e, "som_bmu_plan: flag clear launch");
-    e = som::launch_plan(ta, row_ptr, col_idx, N, nnz, V, c.plan, c.tiles, c.flags, s);
+    const int32_t *rp = row_ptr, *ci = col_idx;
+    if (o.order) {
+        e = som::launch_order(row_ptr, col_idx, N, nnz, V, c.ob, c.flags, s);
+        if (e != hipSuccess) return hip_fail(e, "som_bmu_plan: ordering launch");
+        rp = c.ob.prp;
+        ci = c.ob.pci;
+    }
+    e = som::launch_plan(o.ta, rp, ci, N, nnz, V, c.plan, c.tiles, c.flags, s);
     if (e != hipSuccess) return hip_fail(e, "som_bmu_plan launch");
     return ok();
 }
@@ -128,17 +163,17 @@ som_status som_bmu_plan(const int32_t *row_ptr, const int32_t *col_idx, int64_t 
 som_status som_bmu_sweep(const float *W, const double *norms, int64_t V, int64_t M, int64_t N, int64_t nnz,
                          void *workspace, size_t workspace_bytes, const som_bmu_config *config, void *stream)
 {
+    Opts o;
+    Carved c;
+    bool noop;
     som_status st = check_dims(N, M, V, nnz);
     if (st != SOM_OK) return st;
-    int ta;
-    if ((st = tile_samples(config, &ta)) != SOM_OK) return st;
-    if (N == 0) return ok();
-    if (!W || !norms) return fail(SOM_ERR_INVALID_ARG, "som_bmu_sweep: null pointer");
+    if (N > 0 && (!W || !norms)) return fail(SOM_ERR_INVALID_ARG, "som_bmu_sweep: null pointer");
     if (reinterpret_cast<uintptr_t>(W) & 3) return fail(SOM_ERR_INVALID_ARG, "W must be 4-byte aligned");
-    Carved c;
-    if ((st = carve(workspace, workspace_bytes, N, M, nnz, ta, &c)) != SOM_OK) return st;
-    hipError_t e = som::launch_sweep(ta, W, norms, M, N, V, nnz, c.plan, c.tiles, c.keys,
-                                     static_cast<hipStream_t>(stream));
+    if ((st = setup(N, M, V, nnz, config, workspace, workspace_bytes, &o, &c, &noop)) != SOM_OK) return st;
+    if (noop) return ok();
+    hipError_t e =
+        som::launch_sweep(o.ta, W, norms, M, N, V, nnz, c.plan, c.tiles, c.keys, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "som_bmu_sweep launch");
     return ok();
 }
@@ -147,16 +182,19 @@ som_status som_bmu_finalize(const float *W, const double *norms, int64_t V, int6
                             const int32_t *col_idx, int64_t N, int64_t nnz, int32_t *bmu, double *dist,
                             void *workspace, size_t workspace_bytes, const som_bmu_config *config, void *stream)
 {
+    Opts o;
+    Carved c;
+    bool noop;
     som_status st = check_dims(N, M, V, nnz);
     if (st != SOM_OK) return st;
-    int ta;
-    if ((st = tile_samples(config, &ta)) != SOM_OK) return st;
-    if (N == 0) return ok();
-    if (!W || !norms || !row_ptr || (nnz > 0 && !col_idx) || !bmu || !dist)
+    if (N > 0 && (!W || !norms || !row_ptr || (nnz > 0 && !col_idx) || !bmu || !dist))
         return fail(SOM_ERR_INVALID_ARG, "som_bmu_finalize: null pointer");
-    Carved c;
-    if ((st = carve(workspace, workspace_bytes, N, M, nnz, ta, &c)) != SOM_OK) return st;
-    hipError_t e = som::launch_finalize(ta, W, norms, V, M, row_ptr, col_idx, N, nnz, c.keys, bmu, dist,
+    if ((st = setup(N, M, V, nnz, config, workspace, workspace_bytes, &o, &c, &noop)) != SOM_OK) return st;
+    if (noop) return ok();
+    const int32_t *rp = o.order ? c.ob.prp : row_ptr;
+    const int32_t *ci = o.order ? c.ob.pci : col_idx;
+    const int32_t *perm = o.order ? c.ob.perm : nullptr;
+    hipError_t e = som::launch_finalize(o.ta, W, norms, V, M, rp, ci, N, nnz, perm, c.keys, bmu, dist,
                                         static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "som_bmu_finalize launch");
     return ok();
@@ -166,16 +204,16 @@ som_status som_bmu_search(const float *W, const double *norms, int64_t V, int64_
                           const int32_t *col_idx, int64_t N, int64_t nnz, int32_t *bmu, double *dist,
                           void *workspace, size_t workspace_bytes, const som_bmu_config *config, void *stream)
 {
+    Opts o;
+    Carved c;
+    bool noop;
     som_status st = check_dims(N, M, V, nnz);
     if (st != SOM_OK) return st;
-    int ta;
-    if ((st = tile_samples(config, &ta)) != SOM_OK) return st;
-    if (N == 0) return ok();
-    if (!W || !norms || !row_ptr || (nnz > 0 && !col_idx) || !bmu || !dist)
+    if (N > 0 && (!W || !norms || !row_ptr || (nnz > 0 && !col_idx) || !bmu || !dist))
         return fail(SOM_ERR_INVALID_ARG, "som_bmu_search: null pointer");
     if (reinterpret_cast<uintptr_t>(W) & 3) return fail(SOM_ERR_INVALID_ARG, "W must be 4-byte aligned");
-    Carved c;
-    if ((st = carve(workspace, workspace_bytes, N, M, nnz, ta, &c)) != SOM_OK) return st;
+    if ((st = setup(N, M, V, nnz, config, workspace, workspace_bytes, &o, &c, &noop)) != SOM_OK) return st;
+    if (noop) return ok();
     if ((st = som_bmu_plan(row_ptr, col_idx, N, nnz, V, M, workspace, workspace_bytes, config, stream)) != SOM_OK)
         return st;
     if ((st = som_bmu_sweep(W, norms, V, M, N, nnz, workspace, workspace_bytes, config, stream)) != SOM_OK)
@@ -187,15 +225,16 @@ som_status som_bmu_search(const float *W, const double *norms, int64_t V, int64_
 som_status som_bmu_input_flags(const void *workspace, size_t workspace_bytes, int64_t N, int64_t M, int64_t V,
                                int64_t nnz, const som_bmu_config *config, uint32_t *flags, void *stream)
 {
+    Opts o;
+    Carved c;
+    bool noop;
     som_status st = check_dims(N, M, V, nnz);
     if (st != SOM_OK) return st;
-    int ta;
-    if ((st = tile_samples(config, &ta)) != SOM_OK) return st;
     if (!flags) return fail(SOM_ERR_INVALID_ARG, "som_bmu_input_flags: flags is NULL");
     *flags = 0;
-    if (N == 0) return ok();
-    Carved c;
-    if ((st = carve(const_cast<void *>(workspace), workspace_bytes, N, M, nnz, ta, &c)) != SOM_OK) return st;
+    if ((st = setup(N, M, V, nnz, config, const_cast<void *>(workspace), workspace_bytes, &o, &c, &noop)) != SOM_OK)
+        return st;
+    if (noop) return ok();
     hipStream_t s = static_cast<hipStream_t>(stream);
     hipError_t e = hipStreamSynchronize(s);
     if (e != hipSuccess) return hip_fail(e, "som_bmu_input_flags: stream synchronize");
@@ -206,7 +245,7 @@ som_status som_bmu_input_flags(const void *workspace, size_t workspace_bytes, in
 
 som_status som_validate_csr_host(const int32_t *row_ptr, const int32_t *col_idx, int64_t N, int64_t V)
 {
-    if (N < 0 || V < 1 || V > INT32_MAX) return fail(SOM_ERR_INVALID_ARG, "need N >= 0 and 1 <= V < 2^31");
+    if (N < 0 || V < 1 || V >= INT32_MAX) return fail(SOM_ERR_INVALID_ARG, "need N >= 0 and 1 <= V < 2^31-1");
     if (!row_ptr) return fail(SOM_ERR_INVALID_ARG, "row_ptr is NULL");
     for (int64_t s = 0; s < N; ++s)
         if (row_ptr[s + 1] < row_ptr[s])

@@ -20,31 +20,52 @@ inline int64_t n_strips(int64_t M, int ta) { return (M + strip_neurons(ta) - 1) 
 inline int64_t n_tiles(int64_t N, int ta) { return (N + ta - 1) / ta; }
 
 // Workspace carve-up (offsets in bytes from the workspace base; every section 256-byte aligned).
+// The order sections are empty when the caller keeps the given sample order.
 struct Layout {
-    size_t plan;   // uint2 [nnz]: (feature id, sample mask) of every tile's union, tile t at its CSR offset
-    size_t tiles;  // int2 [n_tiles]: (plan offset, union size) per tile
-    size_t keys;   // uint64 [n_strips * N]: per-strip partial argmin keys, strip-major
-    size_t flags;  // uint32 [64]: input flags
+    size_t plan;    // uint2 [nnz]: (feature id, sample mask) of every tile's union, tile t at its CSR offset
+    size_t tiles;   // int2 [n_tiles]: (plan offset, union size) per tile
+    size_t keys;    // uint64 [n_strips * N]: per-strip partial argmin keys, strip-major, by batch position
+    size_t flags;   // uint32 [64]: input flags
+    size_t freq;    // uint32 [V+1]: feature counts of the batch
+    size_t bucket;  // uint64 [V+1]: per-bucket (samples << 32 | ids) counts, then offsets
+    size_t skey;    // int32 [N]: each sample's bucket
+    size_t perm;    // int32 [N]: sample at each position of the ordered batch
+    size_t prp;     // int32 [N+1]: row pointers of the ordered batch
+    size_t pci;     // int32 [nnz]: feature ids of the ordered batch
     size_t total;
 };
 
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-inline Layout layout_for(int64_t N, int64_t M, int64_t nnz, int ta)
+inline Layout layout_for(int64_t N, int64_t M, int64_t V, int64_t nnz, int ta, bool order)
 {
     Layout L;
     size_t off = 0;
-    L.plan = off;
-    off += align256((size_t)nnz * 8);
-    L.tiles = off;
-    off += align256((size_t)n_tiles(N, ta) * 8);
-    L.keys = off;
-    off += align256((size_t)n_strips(M, ta) * (size_t)N * 8);
-    L.flags = off;
-    off += 256;
+    auto take = [&](size_t bytes) {
+        const size_t at = off;
+        off += align256(bytes);
+        return at;
+    };
+    L.plan = take((size_t)nnz * 8);
+    L.tiles = take((size_t)n_tiles(N, ta) * 8);
+    L.keys = take((size_t)n_strips(M, ta) * (size_t)N * 8);
+    L.flags = take(256);
+    const size_t o = order ? 1 : 0;
+    L.freq = take(o * (size_t)(V + 1) * 4);
+    L.bucket = take(o * (size_t)(V + 1) * 8);
+    L.skey = take(o * (size_t)N * 4);
+    L.perm = take(o * (size_t)N * 4);
+    L.prp = take(o * (size_t)(N + 1) * 4);
+    L.pci = take(o * (size_t)nnz * 4);
     L.total = off;
     return L;
 }
+
+struct OrderBuffers {
+    uint32_t *freq;
+    unsigned long long *bucket;
+    int32_t *skey, *perm, *prp, *pci;
+};
 
 // Kernel launchers (som_kernels.hip). Each returns the launch's hipError_t.
 hipError_t launch_norms(const float *W, int64_t V, int64_t M, double *norms, hipStream_t st);
@@ -54,7 +75,9 @@ hipError_t launch_plan(int ta, const int32_t *row_ptr, const int32_t *col_idx, i
 hipError_t launch_sweep(int ta, const float *W, const double *norms, int64_t M, int64_t N, int64_t V, int64_t nnz,
                         const uint2 *plan, const int2 *tiles, unsigned long long *keys, hipStream_t st);
 hipError_t launch_finalize(int ta, const float *W, const double *norms, int64_t V, int64_t M, const int32_t *row_ptr,
-                           const int32_t *col_idx, int64_t N, int64_t nnz, const unsigned long long *keys,
-                           int32_t *bmu, double *dist, hipStream_t st);
+                           const int32_t *col_idx, int64_t N, int64_t nnz, const int32_t *perm,
+                           const unsigned long long *keys, int32_t *bmu, double *dist, hipStream_t st);
+hipError_t launch_order(const int32_t *row_ptr, const int32_t *col_idx, int64_t N, int64_t nnz, int64_t V,
+                        const OrderBuffers &ob, uint32_t *flags, hipStream_t st);
 
 }  // namespace som

@@ -75,13 +75,13 @@ __device__ __forceinline__ u64 dpp64(u64 x)
     return ((u64)(unsigned)hi << 32) | (unsigned)lo;
 }
 
-// Minimum over each aligned group of G lanes (G = 8, 16 or 32), in every lane of the group.
+// Minimum over each aligned group of G lanes (G = 2, 4, 8, 16 or 32), in every lane of the group.
 template <int G>
 __device__ __forceinline__ int group_min_i32(int x)
 {
     x = min(x, dpp<0xB1>(x));
-    x = min(x, dpp<0x4E>(x));
-    x = min(x, dpp<0x141>(x));
+    if (G >= 4) x = min(x, dpp<0x4E>(x));
+    if (G >= 8) x = min(x, dpp<0x141>(x));
     if (G >= 16) x = min(x, dpp<0x140>(x));
     if (G >= 32) x = min(x, __shfl_xor(x, 16));
     return x;
@@ -135,12 +135,155 @@ __global__ __launch_bounds__(256) void k_norms(const float *__restrict__ W, int6
 
 __global__ void k_clear_flags(uint32_t *flags) { flags[threadIdx.x] = 0u; }
 
+// ----------------------------------------------------------------- order
+
+// Sample order. The post-submission section's tuning groups samples so that a
+// tile's rows share features. Here the samples of a batch are bucketed by their
+// least frequent feature in that batch: rows that share a rare feature land in
+// the same or neighbouring tiles, so unions shrink and the rare codebook rows
+// are re-read while still in L2. A sample's result does not depend on where it
+// sits (its sum order is fixed by its own features), so the permutation never
+// shows in the output. The permuted batch is written to the workspace as a CSR
+// of its own (prp, pci); k_finalize maps positions back to samples.
+
+constexpr int kLdsHistMax = 32768;  // features whose counts fit the LDS histogram
+
+__global__ __launch_bounds__(256) void k_fill_u32(uint32_t *__restrict__ p, int64_t n, uint32_t v)
+{
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256) p[i] = v;
+}
+
+__global__ __launch_bounds__(256) void k_fill_u64(u64 *__restrict__ p, int64_t n, u64 v)
+{
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256) p[i] = v;
+}
+
+// freq[v] = occurrences of feature v in the batch (ids outside [0, V) skipped).
+// Each workgroup counts a contiguous chunk of the ids in LDS, then adds its
+// non-zero counts to the global histogram.
+__global__ __launch_bounds__(256) void k_freq(const int32_t *__restrict__ row_ptr, const int32_t *__restrict__ col_idx,
+                                              int64_t nnz, int32_t V, uint32_t *__restrict__ freq)
+{
+    __shared__ uint32_t h[kLdsHistMax];
+    const int64_t base = row_ptr[0];
+    const bool lds = V <= kLdsHistMax;
+    if (lds)
+        for (int v = threadIdx.x; v < V; v += 256) h[v] = 0u;
+    __syncthreads();
+    const int64_t chunk = (nnz + gridDim.x - 1) / gridDim.x;
+    const int64_t p0 = (int64_t)blockIdx.x * chunk;
+    const int64_t p1 = p0 + chunk < nnz ? p0 + chunk : nnz;
+    for (int64_t p = p0 + threadIdx.x; p < p1; p += 256) {
+        const int id = col_idx[base + p];
+        if (id >= 0 && id < V) {
+            if (lds) atomicAdd(&h[id], 1u);
+            else atomicAdd(&freq[id], 1u);
+        }
+    }
+    __syncthreads();
+    if (lds)
+        for (int v = threadIdx.x; v < V; v += 256)
+            if (h[v]) atomicAdd(&freq[v], h[v]);
+}
+
+// Clamped id range of row s (relative to row_ptr[0]); empty if row_ptr decreases.
+__device__ __forceinline__ void row_range(const int32_t *row_ptr, int64_t base, int64_t nnz, int64_t s, int64_t &rb,
+                                          int64_t &re, uint32_t &bad)
+{
+    const int64_t a = (int64_t)row_ptr[s] - base, b = (int64_t)row_ptr[s + 1] - base;
+    if (b < a || a < 0 || b > nnz) bad |= SOM_FLAG_ROW_PTR;
+    rb = clamp64(a, 0, nnz);
+    re = b < a ? rb : clamp64(b, rb, nnz);
+}
+
+// skey[s] = the sample's least frequent valid feature (ties: the larger id), V if it
+// has none; bucket[key] += (1 << 32) | row length: samples counted in the high
+// half, ids in the low half of one 64-bit word.
+__global__ __launch_bounds__(256) void k_rarest(const int32_t *__restrict__ row_ptr, const int32_t *__restrict__ col_idx,
+                                                int64_t N, int64_t nnz, int32_t V, const uint32_t *__restrict__ freq,
+                                                int32_t *__restrict__ skey, u64 *__restrict__ bucket,
+                                                uint32_t *__restrict__ flags)
+{
+    const int64_t base = row_ptr[0];
+    uint32_t bad = 0;
+    for (int64_t s = (int64_t)blockIdx.x * 256 + threadIdx.x; s < N; s += (int64_t)gridDim.x * 256) {
+        int64_t rb, re;
+        row_range(row_ptr, base, nnz, s, rb, re, bad);
+        u64 best = kKeyNone;  // (frequency, V-1-id): smallest frequency, then largest id
+        for (int64_t p = rb; p < re; ++p) {
+            const int id = col_idx[base + p];
+            if (id >= 0 && id < V) best = min_u64(best, ((u64)freq[id] << 32) | (unsigned)(V - 1 - id));
+        }
+        const int key = best == kKeyNone ? V : (int)(V - 1 - (int)(unsigned)(best & 0xFFFFFFFFull));
+        skey[s] = key;
+        atomicAdd(&bucket[key], (1ull << 32) | (u64)(re - rb));
+    }
+    if (bad) atomicOr(flags, bad);
+}
+
+// One workgroup: exclusive scan of the nb packed bucket counts into packed starting
+// offsets (sample offset << 32 | id offset). prp[N] = total ids (capped at nnz).
+__global__ __launch_bounds__(1024) void k_bucket_scan(u64 *__restrict__ bucket, int64_t nb, int64_t nnz,
+                                                      int32_t *__restrict__ prp_end)
+{
+    __shared__ int64_t ss[1024], si[1024];
+    const int t = threadIdx.x;
+    const int64_t per = (nb + 1023) / 1024;
+    const int64_t b0 = t * per < nb ? t * per : nb;
+    const int64_t b1 = b0 + per < nb ? b0 + per : nb;
+    int64_t ns = 0, ni = 0;
+    for (int64_t b = b0; b < b1; ++b) {
+        ns += (int64_t)(bucket[b] >> 32);
+        ni += (int64_t)(bucket[b] & 0xFFFFFFFFull);
+    }
+    ss[t] = ns;
+    si[t] = ni;
+    __syncthreads();
+    for (int d = 1; d < 1024; d <<= 1) {  // inclusive Hillis-Steele scan
+        const int64_t a = t >= d ? ss[t - d] : 0, c = t >= d ? si[t - d] : 0;
+        __syncthreads();
+        ss[t] += a;
+        si[t] += c;
+        __syncthreads();
+    }
+    int64_t os = ss[t] - ns, oi = si[t] - ni;  // exclusive
+    for (int64_t b = b0; b < b1; ++b) {
+        const u64 c = bucket[b];
+        bucket[b] = ((u64)os << 32) | (u64)(oi & 0xFFFFFFFFll);
+        os += (int64_t)(c >> 32);
+        oi += (int64_t)(c & 0xFFFFFFFFull);
+    }
+    if (t == 1023) *prp_end = (int32_t)(si[1023] < nnz ? si[1023] : nnz);
+}
+
+// Each sample takes the next (position, id offset) of its bucket with one atomic and
+// copies its ids there. Every write is bounded by N and nnz.
+__global__ __launch_bounds__(256) void k_scatter(const int32_t *__restrict__ row_ptr, const int32_t *__restrict__ col_idx,
+                                                 int64_t N, int64_t nnz, const int32_t *__restrict__ skey,
+                                                 u64 *__restrict__ bucket, int32_t *__restrict__ perm,
+                                                 int32_t *__restrict__ prp, int32_t *__restrict__ pci)
+{
+    const int64_t base = row_ptr[0];
+    uint32_t bad = 0;
+    for (int64_t s = (int64_t)blockIdx.x * 256 + threadIdx.x; s < N; s += (int64_t)gridDim.x * 256) {
+        int64_t rb, re;
+        row_range(row_ptr, base, nnz, s, rb, re, bad);
+        const u64 old = atomicAdd(&bucket[skey[s]], (1ull << 32) | (u64)(re - rb));
+        const int64_t ps = (int64_t)(old >> 32), pi = (int64_t)(old & 0xFFFFFFFFull);
+        if (ps >= N) continue;
+        perm[ps] = (int32_t)s;
+        prp[ps] = (int32_t)(pi < nnz ? pi : nnz);
+        const int64_t n = re - rb < nnz - pi ? re - rb : (nnz > pi ? nnz - pi : 0);
+        for (int64_t q = 0; q < n; ++q) pci[pi + q] = col_idx[base + rb + q];
+    }
+}
+
 // ------------------------------------------------------------------ plan
 
 constexpr int kPlanWaves = 4;
 constexpr int kPlanStage = 2048;  // ids staged in LDS per wave
 
-// A wave plans 64/TA consecutive tiles at once: lane l works on row s = l % TA of
+// A wave plans 64/TA consecutive tiles at once (TA = 2 ... 32): lane l works on row s = l % TA of
 // tile l / TA. Each step takes, per tile, the smallest current id over its TA
 // lanes (the next element of the union, ascending), the ballot of the lanes
 // holding it (its sample mask), and advances those lanes: a TA-way merge of
@@ -247,13 +390,12 @@ __global__ __launch_bounds__(256) void k_plan(const int32_t *__restrict__ row_pt
 // ranked. The plan is read defensively (offsets, counts and ids clamped to the
 // workspace and the codebook), so even a workspace the plan never wrote cannot
 // drive an access out of bounds.
-template <int TA, int NPL, bool VEC>
+template <int TA, int NPL, int U, bool VEC, bool PIPE>
 __global__ __launch_bounds__(256) void k_sweep(const float *__restrict__ W, const double *__restrict__ norms,
                                                int64_t M, int64_t N, int64_t V, int64_t nnz,
                                                const uint2 *__restrict__ plan, const int2 *__restrict__ tiles,
                                                int64_t n_tiles, u64 *__restrict__ keys)
 {
-    constexpr int U = 4;  // codebook rows in flight per wave
     const int lane = threadIdx.x & 63;
     const int wv = wave_id();
     const int64_t strip = blockIdx.y;
@@ -311,22 +453,51 @@ __global__ __launch_bounds__(256) void k_sweep(const float *__restrict__ W, cons
             }
         };
 
-        int k = 0;
-        for (; k + U <= cnt; k += U) {
-            uint2 en[U];
-            float w[U][NPL];
+        if (PIPE) {
+            // Software pipeline over batches of U rows: the loads of batch b+1 are in
+            // flight while batch b's masks are dispatched. Entries past the union repeat
+            // its last row with an empty mask (an L1 hit, no adds).
+            const int nb = (cnt + U - 1) / U;
+            auto fetch = [&](int b, uint2 en[U], float w[U][NPL]) {
 #pragma unroll
-            for (int u = 0; u < U; ++u) en[u] = ent[k + u];
+                for (int u = 0; u < U; ++u) {
+                    const int kk = b * U + u;
+                    en[u] = ent[kk < cnt ? kk : cnt - 1];
+                    if (kk >= cnt) en[u].y = 0u;
+                }
 #pragma unroll
-            for (int u = 0; u < U; ++u) row_load(en[u].x, w[u]);
+                for (int u = 0; u < U; ++u) row_load(en[u].x, w[u]);
+            };
+            uint2 ea[U], eb[U];
+            float wa[U][NPL], wb[U][NPL];
+            if (nb > 0) fetch(0, ea, wa);
+            for (int b = 0; b < nb; b += 2) {
+                if (b + 1 < nb) fetch(b + 1, eb, wb);
 #pragma unroll
-            for (int u = 0; u < U; ++u) row_add(en[u].y, w[u]);
-        }
-        for (; k < cnt; ++k) {
-            const uint2 en = ent[k];
-            float w[NPL];
-            row_load(en.x, w);
-            row_add(en.y, w);
+                for (int u = 0; u < U; ++u) row_add(ea[u].y, wa[u]);
+                if (b + 1 >= nb) break;
+                if (b + 2 < nb) fetch(b + 2, ea, wa);
+#pragma unroll
+                for (int u = 0; u < U; ++u) row_add(eb[u].y, wb[u]);
+            }
+        } else {
+            int k = 0;
+            for (; k + U <= cnt; k += U) {
+                uint2 en[U];
+                float w[U][NPL];
+#pragma unroll
+                for (int u = 0; u < U; ++u) en[u] = ent[k + u];
+#pragma unroll
+                for (int u = 0; u < U; ++u) row_load(en[u].x, w[u]);
+#pragma unroll
+                for (int u = 0; u < U; ++u) row_add(en[u].y, w[u]);
+            }
+            for (; k < cnt; ++k) {
+                const uint2 en = ent[k];
+                float w[NPL];
+                row_load(en.x, w);
+                row_add(en.y, w);
+            }
         }
 
         // fused argmin: d = ||w||^2 - 2*dot (fp64, one rounding), keyed; lane s keeps sample s
@@ -350,22 +521,27 @@ __global__ __launch_bounds__(256) void k_sweep(const float *__restrict__ W, cons
 
 // -------------------------------------------------------------- finalize
 
-// One thread per sample: smallest key over the strips, then the winner's distance
-// from the sample's own ids, summed in the same order and precision as the sweep.
+// One thread per position k of the (possibly permuted) batch: smallest key over the
+// strips, then the winner's distance from the row's own ids, summed in the same
+// order and precision as the sweep; results go to sample perm[k] (k without a
+// permutation).
 __global__ __launch_bounds__(256) void k_finalize(const float *__restrict__ W, const double *__restrict__ norms,
                                                   int32_t V, int64_t M, const int32_t *__restrict__ row_ptr,
                                                   const int32_t *__restrict__ col_idx, int64_t N, int64_t nnz,
-                                                  const u64 *__restrict__ keys, int64_t n_strips,
-                                                  int32_t *__restrict__ bmu, double *__restrict__ dist)
+                                                  const int32_t *__restrict__ perm, const u64 *__restrict__ keys,
+                                                  int64_t n_strips, int32_t *__restrict__ bmu,
+                                                  double *__restrict__ dist)
 {
     const int64_t base = row_ptr[0];
-    for (int64_t s = (int64_t)blockIdx.x * 256 + threadIdx.x; s < N; s += (int64_t)gridDim.x * 256) {
+    for (int64_t k = (int64_t)blockIdx.x * 256 + threadIdx.x; k < N; k += (int64_t)gridDim.x * 256) {
+        const int64_t s = perm ? (int64_t)perm[k] : k;
+        if (s < 0 || s >= N) continue;
         u64 best = kKeyNone;
-        for (int64_t g = 0; g < n_strips; ++g) best = min_u64(best, keys[g * N + s]);
+        for (int64_t g = 0; g < n_strips; ++g) best = min_u64(best, keys[g * N + k]);
         int64_t b = (int64_t)(best & kIndexMask);
         if (b >= M) b = M - 1;
-        const int64_t rb = clamp64((int64_t)row_ptr[s] - base, 0, nnz);
-        const int64_t re = clamp64((int64_t)row_ptr[s + 1] - base, rb, nnz);
+        const int64_t rb = clamp64((int64_t)row_ptr[k] - base, 0, nnz);
+        const int64_t re = clamp64((int64_t)row_ptr[k + 1] - base, rb, nnz);
         float dot = 0.0f;
         int cnt = 0;
         for (int64_t p = rb; p < re; ++p) {
@@ -419,10 +595,10 @@ static void sweep_ta(bool vec, dim3 grid, hipStream_t st, const float *W, const 
                      int64_t V, int64_t nnz, const uint2 *plan, const int2 *tiles, int64_t nt, u64 *keys)
 {
     if (vec)
-        hipLaunchKernelGGL((k_sweep<TA, NPL, true>), grid, dim3(256), 0, st, W, norms, M, N, V, nnz, plan, tiles, nt,
+        hipLaunchKernelGGL((k_sweep<TA, NPL, 4, true, false>), grid, dim3(256), 0, st, W, norms, M, N, V, nnz, plan, tiles, nt,
                            keys);
     else
-        hipLaunchKernelGGL((k_sweep<TA, NPL, false>), grid, dim3(256), 0, st, W, norms, M, N, V, nnz, plan, tiles, nt,
+        hipLaunchKernelGGL((k_sweep<TA, NPL, 4, false, false>), grid, dim3(256), 0, st, W, norms, M, N, V, nnz, plan, tiles, nt,
                            keys);
 }
 
@@ -445,13 +621,36 @@ hipError_t launch_sweep(int ta, const float *W, const double *norms, int64_t M, 
 }
 
 hipError_t launch_finalize(int ta, const float *W, const double *norms, int64_t V, int64_t M, const int32_t *row_ptr,
-                           const int32_t *col_idx, int64_t N, int64_t nnz, const unsigned long long *keys,
-                           int32_t *bmu, double *dist, hipStream_t st)
+                           const int32_t *col_idx, int64_t N, int64_t nnz, const int32_t *perm,
+                           const unsigned long long *keys, int32_t *bmu, double *dist, hipStream_t st)
 {
     int64_t blocks = (N + 255) / 256;
     if (blocks > (1 << 22)) blocks = 1 << 22;
     hipLaunchKernelGGL(k_finalize, dim3((unsigned)blocks), dim3(256), 0, st, W, norms, (int32_t)V, M, row_ptr,
-                       col_idx, N, nnz, keys, n_strips(M, ta), bmu, dist);
+                       col_idx, N, nnz, perm, keys, n_strips(M, ta), bmu, dist);
+    return hipGetLastError();
+}
+
+hipError_t launch_order(const int32_t *row_ptr, const int32_t *col_idx, int64_t N, int64_t nnz, int64_t V,
+                        const OrderBuffers &ob, uint32_t *flags, hipStream_t st)
+{
+    const int64_t nb = V + 1;  // one bucket per feature, one for rows without a valid feature
+    int64_t fb = (nb + 255) / 256;
+    if (fb > 4096) fb = 4096;
+    hipLaunchKernelGGL(k_fill_u32, dim3((unsigned)fb), dim3(256), 0, st, ob.freq, nb, 0u);
+    hipLaunchKernelGGL(k_fill_u64, dim3((unsigned)fb), dim3(256), 0, st, ob.bucket, nb, 0ull);
+    // enough workgroups to fill the chip, each with a large chunk of ids for its LDS histogram
+    int64_t hb = (nnz + 65535) / 65536;
+    if (hb < 1) hb = 1;
+    if (hb > 1024) hb = 1024;
+    hipLaunchKernelGGL(k_freq, dim3((unsigned)hb), dim3(256), 0, st, row_ptr, col_idx, nnz, (int32_t)V, ob.freq);
+    int64_t sb = (N + 255) / 256;
+    if (sb > (1 << 22)) sb = 1 << 22;
+    hipLaunchKernelGGL(k_rarest, dim3((unsigned)sb), dim3(256), 0, st, row_ptr, col_idx, N, nnz, (int32_t)V, ob.freq,
+                       ob.skey, ob.bucket, flags);
+    hipLaunchKernelGGL(k_bucket_scan, dim3(1), dim3(1024), 0, st, ob.bucket, nb, nnz, ob.prp + N);
+    hipLaunchKernelGGL(k_scatter, dim3((unsigned)sb), dim3(256), 0, st, row_ptr, col_idx, N, nnz, ob.skey, ob.bucket,
+                       ob.perm, ob.prp, ob.pci);
     return hipGetLastError();
 }
 

@@ -34,7 +34,7 @@ class SomError(RuntimeError):
 
 
 class _Config(ctypes.Structure):
-    _fields_ = [("tile_samples", ctypes.c_int32), ("reserved", ctypes.c_int32 * 7)]
+    _fields_ = [("tile_samples", ctypes.c_int32), ("keep_order", ctypes.c_int32), ("reserved", ctypes.c_int32 * 6)]
 
 
 _lib = None
@@ -99,21 +99,23 @@ def _dev(t: torch.Tensor, name: str, dtype: torch.dtype, min_numel: int = 0) -> 
     return t.data_ptr()
 
 
-def _cfg(tile_samples: int):
+def _cfg(tile_samples: int = 0, keep_order: bool = False):
     c = _Config()
     c.tile_samples = int(tile_samples)
+    c.keep_order = 1 if keep_order else 0
     return ctypes.byref(c)
 
 
-def workspace_bytes(N: int, M: int, V: int, nnz: int, tile_samples: int = 0) -> int:
-    n = load().som_bmu_workspace_bytes(N, M, V, nnz, _cfg(tile_samples))
+def workspace_bytes(N: int, M: int, V: int, nnz: int, tile_samples: int = 0, keep_order: bool = False) -> int:
+    n = load().som_bmu_workspace_bytes(N, M, V, nnz, _cfg(tile_samples, keep_order))
     if n == 0:
         raise ValueError("som_bmu_workspace_bytes: invalid sizes or config")
     return n
 
 
-def alloc_workspace(N: int, M: int, V: int, nnz: int, device, tile_samples: int = 0) -> torch.Tensor:
-    return torch.empty(workspace_bytes(N, M, V, nnz, tile_samples), dtype=torch.uint8, device=device)
+def alloc_workspace(N: int, M: int, V: int, nnz: int, device, tile_samples: int = 0,
+                    keep_order: bool = False) -> torch.Tensor:
+    return torch.empty(workspace_bytes(N, M, V, nnz, tile_samples, keep_order), dtype=torch.uint8, device=device)
 
 
 def codebook_norms(W: torch.Tensor, V: int, M: int, out: torch.Tensor | None = None) -> torch.Tensor:
@@ -143,7 +145,7 @@ def _nnz(row_ptr: torch.Tensor, N: int, nnz: int | None) -> int:
 
 
 def bmu_search(W, norms, row_ptr, col_idx, V: int, M: int, nnz: int | None = None, bmu=None, dist=None,
-               workspace=None, tile_samples: int = 0):
+               workspace=None, tile_samples: int = 0, keep_order: bool = False):
     """BMU index (int32) and squared distance (fp64) of every CSR row. Returns (bmu, dist)."""
     N = row_ptr.numel() - 1
     nnz = _nnz(row_ptr, N, nnz)
@@ -153,36 +155,37 @@ def bmu_search(W, norms, row_ptr, col_idx, V: int, M: int, nnz: int | None = Non
     if dist is None:
         dist = torch.empty(N, dtype=torch.float64, device=dev)
     if workspace is None:
-        workspace = alloc_workspace(N, M, V, nnz, dev, tile_samples)
+        workspace = alloc_workspace(N, M, V, nnz, dev, tile_samples, keep_order)
     if W.numel() != V * M:
         raise ValueError("W must hold V*M elements")
     rp, ci = _csr(row_ptr, col_idx, N, nnz)
     st = load().som_bmu_search(
         _dev(W, "W", torch.float32), _dev(norms, "norms", torch.float64, M), V, M, rp, ci, N, nnz,
         _dev(bmu, "bmu", torch.int32, N), _dev(dist, "dist", torch.float64, N),
-        _dev(workspace, "workspace", torch.uint8), workspace.numel(), _cfg(tile_samples), _stream(W))
+        _dev(workspace, "workspace", torch.uint8), workspace.numel(), _cfg(tile_samples, keep_order), _stream(W))
     _check(st, "som_bmu_search")
     return bmu, dist
 
 
-def bmu_plan(row_ptr, col_idx, V: int, M: int, nnz: int, workspace, tile_samples: int = 0):
+def bmu_plan(row_ptr, col_idx, V: int, M: int, nnz: int, workspace, tile_samples: int = 0, keep_order: bool = False):
     N = row_ptr.numel() - 1
     rp, ci = _csr(row_ptr, col_idx, N, nnz)
     st = load().som_bmu_plan(rp, ci, N, nnz, V, M, _dev(workspace, "workspace", torch.uint8), workspace.numel(),
-                             _cfg(tile_samples), _stream(row_ptr))
+                             _cfg(tile_samples, keep_order), _stream(row_ptr))
     _check(st, "som_bmu_plan")
 
 
-def bmu_sweep(W, norms, V: int, M: int, N: int, nnz: int, workspace, tile_samples: int = 0):
+def bmu_sweep(W, norms, V: int, M: int, N: int, nnz: int, workspace, tile_samples: int = 0, keep_order: bool = False):
     if W.numel() != V * M:
         raise ValueError("W must hold V*M elements")
     st = load().som_bmu_sweep(_dev(W, "W", torch.float32), _dev(norms, "norms", torch.float64, M), V, M, N, nnz,
-                              _dev(workspace, "workspace", torch.uint8), workspace.numel(), _cfg(tile_samples),
-                              _stream(W))
+                              _dev(workspace, "workspace", torch.uint8), workspace.numel(),
+                              _cfg(tile_samples, keep_order), _stream(W))
     _check(st, "som_bmu_sweep")
 
 
-def bmu_finalize(W, norms, row_ptr, col_idx, V: int, M: int, nnz: int, bmu, dist, workspace, tile_samples: int = 0):
+def bmu_finalize(W, norms, row_ptr, col_idx, V: int, M: int, nnz: int, bmu, dist, workspace, tile_samples: int = 0,
+                 keep_order: bool = False):
     N = row_ptr.numel() - 1
     if W.numel() != V * M:
         raise ValueError("W must hold V*M elements")
@@ -190,15 +193,15 @@ def bmu_finalize(W, norms, row_ptr, col_idx, V: int, M: int, nnz: int, bmu, dist
     st = load().som_bmu_finalize(
         _dev(W, "W", torch.float32), _dev(norms, "norms", torch.float64, M), V, M, rp, ci, N, nnz,
         _dev(bmu, "bmu", torch.int32, N), _dev(dist, "dist", torch.float64, N),
-        _dev(workspace, "workspace", torch.uint8), workspace.numel(), _cfg(tile_samples), _stream(W))
+        _dev(workspace, "workspace", torch.uint8), workspace.numel(), _cfg(tile_samples, keep_order), _stream(W))
     _check(st, "som_bmu_finalize")
 
 
-def input_flags(workspace, N: int, M: int, V: int, nnz: int, tile_samples: int = 0) -> int:
+def input_flags(workspace, N: int, M: int, V: int, nnz: int, tile_samples: int = 0, keep_order: bool = False) -> int:
     """SOM_FLAG_* bits the last plan recorded (waits for the current stream)."""
     out = ctypes.c_uint32(0)
     st = load().som_bmu_input_flags(_dev(workspace, "workspace", torch.uint8), workspace.numel(), N, M, V, nnz,
-                                    _cfg(tile_samples), ctypes.byref(out), _stream(workspace))
+                                    _cfg(tile_samples, keep_order), ctypes.byref(out), _stream(workspace))
     _check(st, "som_bmu_input_flags")
     return int(out.value)
 

@@ -24,7 +24,8 @@ def to_dev(a: np.ndarray, dev):
     return torch.from_numpy(np.ascontiguousarray(a)).to(dev)
 
 
-def gpu_run(W: np.ndarray | torch.Tensor, row_ptr, col_idx, dev, tile_samples: int = 0, norms=None):
+def gpu_run(W: np.ndarray | torch.Tensor, row_ptr, col_idx, dev, tile_samples: int = 0, norms=None,
+            keep_order: bool = False):
     """Norms + search on the GPU; returns numpy (bmu, dist, norms)."""
     Wd = W if isinstance(W, torch.Tensor) else to_dev(W, dev)
     V, M = Wd.shape
@@ -34,7 +35,7 @@ def gpu_run(W: np.ndarray | torch.Tensor, row_ptr, col_idx, dev, tile_samples: i
     nnz = int(rp[N].item()) - int(rp[0].item())
     if norms is None:
         norms = som.codebook_norms(Wd, V, M)
-    b, d = som.bmu_search(Wd, norms, rp, ci, V, M, nnz=nnz, tile_samples=tile_samples)
+    b, d = som.bmu_search(Wd, norms, rp, ci, V, M, nnz=nnz, tile_samples=tile_samples, keep_order=keep_order)
     torch.cuda.synchronize()
     return b.cpu().numpy(), d.cpu().numpy(), norms.cpu().numpy()
 

@@ -45,6 +45,9 @@ def test_workspace_bytes():
     assert lib.som_bmu_workspace_bytes(10, 256, 2000, 0, _cfg(7)) == 0
     # larger tiles use narrower strips, hence more partial keys
     assert som.workspace_bytes(10_000, 4096, 2000, 0, 16) > som.workspace_bytes(10_000, 4096, 2000, 0, 8)
+    # the regrouped copy of the batch is only held when the order is not kept
+    assert som.workspace_bytes(10_000, 4096, 2000, 120_000, keep_order=True) < som.workspace_bytes(10_000, 4096, 2000,
+                                                                                                    120_000)
 
 
 def _status(rp, ci, V):
@@ -89,9 +92,10 @@ def _search(W=FAKE, norms=FAKE, V=100, M=64, rp=FAKE, ci=FAKE, N=10, nnz=50, bmu
     return lib.som_bmu_search(W, norms, V, M, rp, ci, N, nnz, bmu, dist, ws, ws_bytes, cfg, None)
 
 
-def _cfg(ta, reserved0=0):
+def _cfg(ta, reserved0=0, keep_order=0):
     c = som._Config()
     c.tile_samples = ta
+    c.keep_order = keep_order
     c.reserved[0] = reserved0
     return ctypes.pointer(c)
 
@@ -111,6 +115,7 @@ def _cfg(ta, reserved0=0):
     (dict(W=ctypes.c_void_p((1 << 20) + 2)), som.SOM_ERR_INVALID_ARG),  # W not 4-byte aligned
     (dict(cfg=_cfg(7)), som.SOM_ERR_INVALID_ARG),
     (dict(cfg=_cfg(16, reserved0=1)), som.SOM_ERR_INVALID_ARG),
+    (dict(cfg=_cfg(8, keep_order=2)), som.SOM_ERR_INVALID_ARG),
     (dict(ws=None), som.SOM_ERR_WORKSPACE),
     (dict(ws=ctypes.c_void_p((1 << 20) + 64)), som.SOM_ERR_WORKSPACE),  # not 256-byte aligned
     (dict(ws_bytes=1024), som.SOM_ERR_WORKSPACE),

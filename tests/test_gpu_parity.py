@@ -55,18 +55,20 @@ RAGGED = [
 ]
 
 
-@pytest.mark.parametrize("tile", [8, 16, 32])
+@pytest.mark.parametrize("tile,keep", [(8, False), (16, False), (32, False), (8, True)])
 @pytest.mark.parametrize("seed,N,V,M,kind", RAGGED)
-def test_ragged_shapes(dev, seed, N, V, M, kind, tile):
+def test_ragged_shapes(dev, seed, N, V, M, kind, tile, keep):
     rp, ci, W = case(seed, N, V, M, kind)
-    b, d, _ = gpu_run(W, rp, ci, dev, tile_samples=tile)
-    compare(W, rp, ci, b, d, exact=(kind == synth.QUANTISED), what=f"N={N} V={V} M={M} TA={tile}")
+    b, d, _ = gpu_run(W, rp, ci, dev, tile_samples=tile, keep_order=keep)
+    compare(W, rp, ci, b, d, exact=(kind == synth.QUANTISED), what=f"N={N} V={V} M={M} TA={tile} keep={keep}")
 
 
-def test_tile_size_and_repeat_invariance(dev):
-    # each sample's dot is its own ascending fp32 sum, so the tile size cannot change a bit
+def test_tile_size_order_and_repeat_invariance(dev):
+    # each sample's dot is its own ascending fp32 sum, so neither the tile size nor the
+    # regrouping of samples can change a bit
     rp, ci, W = case(31, 3000, 30000, 2500, synth.UNIFORM)
-    runs = [gpu_run(W, rp, ci, dev, tile_samples=t)[:2] for t in (8, 16, 32, 16)]
+    runs = [gpu_run(W, rp, ci, dev, tile_samples=t, keep_order=k)[:2]
+            for t, k in ((8, False), (16, False), (32, False), (8, True), (16, True), (32, True), (8, False))]
     for b, d in runs[1:]:
         assert np.array_equal(b, runs[0][0]) and np.array_equal(d, runs[0][1])
 
