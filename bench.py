@@ -152,7 +152,7 @@ def main():
     norms = torch.empty(M, dtype=torch.float64, device=dev)
     bmu = torch.empty(N, dtype=torch.int32, device=dev)
     dist = torch.empty(N, dtype=torch.float64, device=dev)
-    ws = som.alloc_workspace(N, M, V, nnz, dev)
+    ws = som.alloc_workspace(N, M, V, nnz, dev, tile_samples=args.tile)
     torch.cuda.synchronize()
     log(f"inputs resident: codebook {4 * V * M / 1e9:.2f} GB, workspace {ws.numel() / 1e9:.2f} GB "
         f"({time.perf_counter() - t0:.1f} s)")
@@ -180,7 +180,7 @@ def main():
         som.bmu_sweep(W, norms, V, M, N, nnz, ws, tile_samples=args.tile)
         if ev is not None:
             ev[3].record()
-        som.bmu_finalize(W, norms, rp, ci, V, M, nnz, bmu, dist, ws, tile_samples=args.tile)
+        som.bmu_finalize(norms, rp, V, M, nnz, bmu, dist, ws, tile_samples=args.tile)
         if ev is not None:
             ev[4].record()
 
@@ -196,7 +196,7 @@ def main():
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t_start
     log(f"timed {args.steps} steps in {elapsed:.3f} s")
-    if som.input_flags(ws, N, M, V, nnz) != 0:
+    if som.input_flags(ws, N, M, V, nnz, tile_samples=args.tile) != 0:
         raise RuntimeError("the device flagged the generated CSR as invalid")
 
     phase_ms = {p: float(np.mean([e[i].elapsed_time(e[i + 1]) for e in events])) for i, p in enumerate(phases)}
@@ -223,7 +223,8 @@ def main():
         "dtype": "f32 sums, f64 norms and distances",
         "data": "synthetic (seeded stand-in for the MEDLINE/MeSH corpus)",
         "config": {"workload": workload, "map": f"{cfg.edge}x{cfg.edge}", "M": M, "V": V, "N": N, "nnz": nnz,
-                   "tile_samples": args.tile or 16, "parallelism": "single GPU"},
+                   "tile_samples": args.tile or som.DEFAULT_TILE_SAMPLES,
+                   "keep_order": False, "alg_tile_samples": ALG_TILE, "parallelism": "single GPU"},
         "effective_codebook_GBps": eff_gbps,
         "effective_pct_of_hbm_peak": 100.0 * eff_gbps / HBM_PEAK_GBPS,
         "effective_codebook_bytes_per_step": alg_bytes,

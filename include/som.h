@@ -83,7 +83,7 @@ typedef enum {
  * changes any result: a sample's sum order is fixed by its own features, so
  * its BMU and distance do not depend on the tile it lands in.
  *   tile_samples  samples per tile, TA (SpMM-tile kernel section): 8, 16 or
- *                 32; 0 selects 8.
+ *                 32; 0 selects SOM_DEFAULT_TILE_SAMPLES.
  *   keep_order    0 (default): the plan first regroups the batch by each
  *                 sample's least frequent feature (the post-submission
  *                 section's lever of clustering samples so tiles share
@@ -93,6 +93,8 @@ typedef enum {
  * The same config must be given to the workspace query and to every phase
  * of one search.
  */
+#define SOM_DEFAULT_TILE_SAMPLES 8
+
 typedef struct {
     int32_t tile_samples;
     int32_t keep_order;
@@ -159,21 +161,22 @@ som_status som_bmu_plan(const int32_t *row_ptr, const int32_t *col_idx, int64_t 
  * som_bmu_sweep -- the fused sweep (Algorithm 2, steps 4, 6, 7): streams each
  *   planned codebook row once per tile and neuron strip, accumulates every
  *   sample's dot product in registers, ranks d_i = ||w_i||^2 - 2*dot_i and
- *   keeps, per sample and group of neurons, the smallest 64-bit key.
+ *   keeps, per sample and group of neurons, the smallest 64-bit key and the
+ *   fp32 dot product of the neuron it names.
  */
 som_status som_bmu_sweep(const float *W, const double *norms, int64_t V, int64_t M, int64_t N, int64_t nnz,
                          void *workspace, size_t workspace_bytes, const som_bmu_config *config, void *stream);
 
 /*
  * som_bmu_finalize -- reduces the per-strip keys of each sample to its BMU
- *   and recomputes the winner's distance from the sample's own ids:
- *   dist = (||w_bmu||^2 - 2*dot) + nnz(x), the dot summed exactly as in the
- *   sweep. Writes bmu and dist.
+ *   and forms the winner's full squared distance from the dot product the
+ *   sweep kept with the winning key: dist = (||w_bmu||^2 - 2*dot) + nnz(x).
+ *   Reads only the workspace, norms and row_ptr (for nnz(x)); writes bmu and
+ *   dist.
  */
-som_status som_bmu_finalize(const float *W, const double *norms, int64_t V, int64_t M, const int32_t *row_ptr,
-                            const int32_t *col_idx, int64_t N, int64_t nnz, int32_t *bmu, double *dist,
-                            void *workspace, size_t workspace_bytes, const som_bmu_config *config,
-                            void *stream);
+som_status som_bmu_finalize(const double *norms, int64_t V, int64_t M, const int32_t *row_ptr, int64_t N, int64_t nnz,
+                            int32_t *bmu, double *dist, void *workspace, size_t workspace_bytes,
+                            const som_bmu_config *config, void *stream);
 
 /*
  * Input flags (SOM_FLAG_*) the last plan on this workspace recorded. Waits

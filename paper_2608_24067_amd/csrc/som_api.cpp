@@ -73,6 +73,7 @@ struct Carved {
     uint2 *plan;
     int2 *tiles;
     unsigned long long *keys;
+    float *dots;
     uint32_t *flags;
     som::OrderBuffers ob;
 };
@@ -88,6 +89,7 @@ som_status carve(void *ws, size_t bytes, int64_t N, int64_t M, int64_t V, int64_
     c->plan = reinterpret_cast<uint2 *>(b + L.plan);
     c->tiles = reinterpret_cast<int2 *>(b + L.tiles);
     c->keys = reinterpret_cast<unsigned long long *>(b + L.keys);
+    c->dots = reinterpret_cast<float *>(b + L.dots);
     c->flags = reinterpret_cast<uint32_t *>(b + L.flags);
     c->ob.freq = reinterpret_cast<uint32_t *>(b + L.freq);
     c->ob.bucket = reinterpret_cast<unsigned long long *>(b + L.bucket);
@@ -173,28 +175,27 @@ som_status som_bmu_sweep(const float *W, const double *norms, int64_t V, int64_t
     if ((st = setup(N, M, V, nnz, config, workspace, workspace_bytes, &o, &c, &noop)) != SOM_OK) return st;
     if (noop) return ok();
     hipError_t e =
-        som::launch_sweep(o.ta, W, norms, M, N, V, nnz, c.plan, c.tiles, c.keys, static_cast<hipStream_t>(stream));
+        som::launch_sweep(o.ta, W, norms, M, N, V, nnz, c.plan, c.tiles, c.keys, c.dots,
+                         static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "som_bmu_sweep launch");
     return ok();
 }
 
-som_status som_bmu_finalize(const float *W, const double *norms, int64_t V, int64_t M, const int32_t *row_ptr,
-                            const int32_t *col_idx, int64_t N, int64_t nnz, int32_t *bmu, double *dist,
-                            void *workspace, size_t workspace_bytes, const som_bmu_config *config, void *stream)
+som_status som_bmu_finalize(const double *norms, int64_t V, int64_t M, const int32_t *row_ptr, int64_t N, int64_t nnz,
+                            int32_t *bmu, double *dist, void *workspace, size_t workspace_bytes,
+                            const som_bmu_config *config, void *stream)
 {
     Opts o;
     Carved c;
     bool noop;
     som_status st = check_dims(N, M, V, nnz);
     if (st != SOM_OK) return st;
-    if (N > 0 && (!W || !norms || !row_ptr || (nnz > 0 && !col_idx) || !bmu || !dist))
-        return fail(SOM_ERR_INVALID_ARG, "som_bmu_finalize: null pointer");
+    if (N > 0 && (!norms || !row_ptr || !bmu || !dist)) return fail(SOM_ERR_INVALID_ARG, "som_bmu_finalize: null pointer");
     if ((st = setup(N, M, V, nnz, config, workspace, workspace_bytes, &o, &c, &noop)) != SOM_OK) return st;
     if (noop) return ok();
     const int32_t *rp = o.order ? c.ob.prp : row_ptr;
-    const int32_t *ci = o.order ? c.ob.pci : col_idx;
     const int32_t *perm = o.order ? c.ob.perm : nullptr;
-    hipError_t e = som::launch_finalize(o.ta, W, norms, V, M, rp, ci, N, nnz, perm, c.keys, bmu, dist,
+    hipError_t e = som::launch_finalize(o.ta, norms, M, rp, N, nnz, perm, c.keys, c.dots, bmu, dist,
                                         static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "som_bmu_finalize launch");
     return ok();
@@ -218,8 +219,7 @@ som_status som_bmu_search(const float *W, const double *norms, int64_t V, int64_
         return st;
     if ((st = som_bmu_sweep(W, norms, V, M, N, nnz, workspace, workspace_bytes, config, stream)) != SOM_OK)
         return st;
-    return som_bmu_finalize(W, norms, V, M, row_ptr, col_idx, N, nnz, bmu, dist, workspace, workspace_bytes, config,
-                            stream);
+    return som_bmu_finalize(norms, V, M, row_ptr, N, nnz, bmu, dist, workspace, workspace_bytes, config, stream);
 }
 
 som_status som_bmu_input_flags(const void *workspace, size_t workspace_bytes, int64_t N, int64_t M, int64_t V,

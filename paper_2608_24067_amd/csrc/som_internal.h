@@ -5,10 +5,12 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include "som.h"
+
 namespace som {
 
 // Tile sizes (samples per tile) the library is built for, and the default.
-constexpr int kDefaultTileSamples = 8;
+constexpr int kDefaultTileSamples = SOM_DEFAULT_TILE_SAMPLES;
 inline bool valid_tile(int ta) { return ta == 8 || ta == 16 || ta == 32; }
 
 // Neurons per lane of the sweep: 8 (two 16-byte loads per codebook row) for tiles of 8
@@ -22,10 +24,11 @@ inline int64_t n_tiles(int64_t N, int ta) { return (N + ta - 1) / ta; }
 // Workspace carve-up (offsets in bytes from the workspace base; every section 256-byte aligned).
 // The order sections are empty when the caller keeps the given sample order.
 struct Layout {
+    size_t flags;   // uint32 [64]: input flags
     size_t plan;    // uint2 [nnz]: (feature id, sample mask) of every tile's union, tile t at its CSR offset
     size_t tiles;   // int2 [n_tiles]: (plan offset, union size) per tile
     size_t keys;    // uint64 [n_strips * N]: per-strip partial argmin keys, strip-major, by batch position
-    size_t flags;   // uint32 [64]: input flags
+    size_t dots;    // float [n_strips * N]: fp32 dot product of the neuron each key names
     size_t freq;    // uint32 [V+1]: feature counts of the batch
     size_t bucket;  // uint64 [V+1]: per-bucket (samples << 32 | ids) counts, then offsets
     size_t skey;    // int32 [N]: each sample's bucket
@@ -46,10 +49,11 @@ inline Layout layout_for(int64_t N, int64_t M, int64_t V, int64_t nnz, int ta, b
         off += align256(bytes);
         return at;
     };
+    L.flags = take(256);  // first, so that its place does not depend on the sizes or the config
     L.plan = take((size_t)nnz * 8);
     L.tiles = take((size_t)n_tiles(N, ta) * 8);
     L.keys = take((size_t)n_strips(M, ta) * (size_t)N * 8);
-    L.flags = take(256);
+    L.dots = take((size_t)n_strips(M, ta) * (size_t)N * 4);
     const size_t o = order ? 1 : 0;
     L.freq = take(o * (size_t)(V + 1) * 4);
     L.bucket = take(o * (size_t)(V + 1) * 8);
@@ -73,10 +77,10 @@ hipError_t launch_clear_flags(uint32_t *flags, hipStream_t st);
 hipError_t launch_plan(int ta, const int32_t *row_ptr, const int32_t *col_idx, int64_t N, int64_t nnz, int64_t V,
                        uint2 *plan, int2 *tiles, uint32_t *flags, hipStream_t st);
 hipError_t launch_sweep(int ta, const float *W, const double *norms, int64_t M, int64_t N, int64_t V, int64_t nnz,
-                        const uint2 *plan, const int2 *tiles, unsigned long long *keys, hipStream_t st);
-hipError_t launch_finalize(int ta, const float *W, const double *norms, int64_t V, int64_t M, const int32_t *row_ptr,
-                           const int32_t *col_idx, int64_t N, int64_t nnz, const int32_t *perm,
-                           const unsigned long long *keys, int32_t *bmu, double *dist, hipStream_t st);
+                        const uint2 *plan, const int2 *tiles, unsigned long long *keys, float *dots, hipStream_t st);
+hipError_t launch_finalize(int ta, const double *norms, int64_t M, const int32_t *row_ptr, int64_t N, int64_t nnz,
+                           const int32_t *perm, const unsigned long long *keys, const float *dots, int32_t *bmu,
+                           double *dist, hipStream_t st);
 hipError_t launch_order(const int32_t *row_ptr, const int32_t *col_idx, int64_t N, int64_t nnz, int64_t V,
                         const OrderBuffers &ob, uint32_t *flags, hipStream_t st);
 

@@ -146,7 +146,8 @@ __global__ void k_clear_flags(uint32_t *flags) { flags[threadIdx.x] = 0u; }
 // shows in the output. The permuted batch is written to the workspace as a CSR
 // of its own (prp, pci); k_finalize maps positions back to samples.
 
-constexpr int kLdsHistMax = 32768;  // features whose counts fit the LDS histogram
+constexpr int kLdsHistMax = 32768;          // features whose counts fit the LDS histogram
+constexpr int64_t kFreqSample = 1ll << 25;  // ids counted: the ordering needs only a rough rarity rank
 
 __global__ __launch_bounds__(256) void k_fill_u32(uint32_t *__restrict__ p, int64_t n, uint32_t v)
 {
@@ -158,9 +159,9 @@ __global__ __launch_bounds__(256) void k_fill_u64(u64 *__restrict__ p, int64_t n
     for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256) p[i] = v;
 }
 
-// freq[v] = occurrences of feature v in the batch (ids outside [0, V) skipped).
-// Each workgroup counts a contiguous chunk of the ids in LDS, then adds its
-// non-zero counts to the global histogram.
+// freq[v] = occurrences of feature v among the batch's first kFreqSample ids (all of
+// them for smaller batches; ids outside [0, V) skipped). Each workgroup counts a
+// contiguous chunk in LDS, then adds its non-zero counts to the global histogram.
 __global__ __launch_bounds__(256) void k_freq(const int32_t *__restrict__ row_ptr, const int32_t *__restrict__ col_idx,
                                               int64_t nnz, int32_t V, uint32_t *__restrict__ freq)
 {
@@ -256,12 +257,11 @@ __global__ __launch_bounds__(1024) void k_bucket_scan(u64 *__restrict__ bucket, 
     if (t == 1023) *prp_end = (int32_t)(si[1023] < nnz ? si[1023] : nnz);
 }
 
-// Each sample takes the next (position, id offset) of its bucket with one atomic and
-// copies its ids there. Every write is bounded by N and nnz.
-__global__ __launch_bounds__(256) void k_scatter(const int32_t *__restrict__ row_ptr, const int32_t *__restrict__ col_idx,
-                                                 int64_t N, int64_t nnz, const int32_t *__restrict__ skey,
-                                                 u64 *__restrict__ bucket, int32_t *__restrict__ perm,
-                                                 int32_t *__restrict__ prp, int32_t *__restrict__ pci)
+// Each sample takes the next (position, id offset) of its bucket with one atomic.
+// Positions past N (only reachable with invalid row pointers) are dropped.
+__global__ __launch_bounds__(256) void k_place(const int32_t *__restrict__ row_ptr, int64_t N, int64_t nnz,
+                                               const int32_t *__restrict__ skey, u64 *__restrict__ bucket,
+                                               int32_t *__restrict__ perm, int32_t *__restrict__ prp)
 {
     const int64_t base = row_ptr[0];
     uint32_t bad = 0;
@@ -273,8 +273,36 @@ __global__ __launch_bounds__(256) void k_scatter(const int32_t *__restrict__ row
         if (ps >= N) continue;
         perm[ps] = (int32_t)s;
         prp[ps] = (int32_t)(pi < nnz ? pi : nnz);
-        const int64_t n = re - rb < nnz - pi ? re - rb : (nnz > pi ? nnz - pi : 0);
-        for (int64_t q = 0; q < n; ++q) pci[pi + q] = col_idx[base + rb + q];
+    }
+}
+
+// Position k copies the ids of sample perm[k] to pci[prp[k] ...]: consecutive threads
+// write consecutive rows. Sample indices and offsets are re-checked, so positions
+// never placed (invalid input only) cannot drive an access out of bounds.
+__global__ __launch_bounds__(256) void k_gather(const int32_t *__restrict__ row_ptr, const int32_t *__restrict__ col_idx,
+                                                int64_t N, int64_t nnz, const int32_t *__restrict__ perm,
+                                                const int32_t *__restrict__ prp, int32_t *__restrict__ pci)
+{
+    const int64_t base = row_ptr[0];
+    uint32_t bad = 0;
+    for (int64_t k = (int64_t)blockIdx.x * 256 + threadIdx.x; k < N; k += (int64_t)gridDim.x * 256) {
+        const int64_t s = perm[k];
+        if (s < 0 || s >= N) continue;
+        int64_t rb, re;
+        row_range(row_ptr, base, nnz, s, rb, re, bad);
+        const int64_t dst = clamp64(prp[k], 0, nnz);
+        const int64_t n = re - rb < nnz - dst ? re - rb : nnz - dst;
+        const int32_t *src = col_idx + base + rb;
+        int32_t *out = pci + dst;
+        // the first 16 ids: all loads issued before the first store
+        int32_t v[16];
+#pragma unroll
+        for (int q = 0; q < 16; ++q)
+            if (q < n) v[q] = src[q];
+#pragma unroll
+        for (int q = 0; q < 16; ++q)
+            if (q < n) out[q] = v[q];
+        for (int64_t q = 16; q < n; ++q) out[q] = src[q];
     }
 }
 
@@ -384,26 +412,30 @@ __global__ __launch_bounds__(256) void k_plan(const int32_t *__restrict__ row_pt
 // ----------------------------------------------------------------- sweep
 
 // Workgroup = 4 waves = 4 consecutive tiles x one strip (blockIdx.y) of 64*NPL
-// neurons; lane l owns neurons i0 = strip*64*NPL + NPL*l .. i0+NPL-1. VEC: M is a
-// multiple of NPL and W 16-byte aligned, so each lane's NPL weights of a row are
-// NPL/4 aligned 16-byte loads; lanes past M load a valid address and are never
-// ranked. The plan is read defensively (offsets, counts and ids clamped to the
-// workspace and the codebook), so even a workspace the plan never wrote cannot
-// drive an access out of bounds.
-template <int TA, int NPL, int U, bool VEC, bool PIPE>
+// neurons; each lane owns NPL of them, in groups of four (see nid below). VEC: M is
+// a multiple of 4 and W 16-byte aligned, so each group is one aligned 16-byte load;
+// groups past M load a valid address and are never ranked. The plan is read
+// defensively (offsets, counts and ids clamped to the workspace and the codebook),
+// so even a workspace the plan never wrote cannot drive an access out of bounds.
+template <int TA, int NPL, int U, bool VEC>
 __global__ __launch_bounds__(256) void k_sweep(const float *__restrict__ W, const double *__restrict__ norms,
                                                int64_t M, int64_t N, int64_t V, int64_t nnz,
                                                const uint2 *__restrict__ plan, const int2 *__restrict__ tiles,
-                                               int64_t n_tiles, u64 *__restrict__ keys)
+                                               int64_t n_tiles, u64 *__restrict__ keys, float *__restrict__ dots)
 {
     const int lane = threadIdx.x & 63;
     const int wv = wave_id();
     const int64_t strip = blockIdx.y;
-    const int64_t i0 = strip * (64 * NPL) + (int64_t)lane * NPL;
-
-    int64_t col[NPL];
+    // Element j of lane l is neuron strip*64*NPL + (j/4)*256 + 4l + j%4: each group of
+    // four is one 16-byte load, and the 64 lanes' loads of a group cover one
+    // contiguous KiB of the row.
+    int64_t nid[NPL], col[NPL];
 #pragma unroll
-    for (int j = 0; j < NPL; ++j) col[j] = VEC ? (i0 < M ? i0 : M - NPL) + j : (i0 + j < M ? i0 + j : M - 1);
+    for (int j = 0; j < NPL; ++j) {
+        nid[j] = strip * (64 * NPL) + (int64_t)(j / 4) * 256 + (int64_t)lane * 4 + (j % 4);
+        const int64_t g = nid[j] - (j % 4);  // first neuron of the 16-byte group
+        col[j] = VEC ? (g < M ? g : M - 4) + (j % 4) : (nid[j] < M ? nid[j] : M - 1);
+    }
     double nrm[NPL];
 #pragma unroll
     for (int j = 0; j < NPL; ++j) nrm[j] = norms[col[j]];
@@ -415,7 +447,9 @@ __global__ __launch_bounds__(256) void k_sweep(const float *__restrict__ W, cons
         const int2 te = tiles[t];
         const int64_t off = clamp64(te.x, 0, nnz);
         const uint2 *ent = plan + off;
-        const int cnt = (int)clamp64(te.y, 0, nnz - off);
+        // a tile's union never reaches the next tile's span
+        const int64_t nxt = t + 1 < n_tiles ? clamp64(tiles[t + 1].x, off, nnz) : nnz;
+        const int cnt = (int)clamp64(te.y, 0, nxt - off);
 
         float acc[TA][NPL];
 #pragma unroll
@@ -453,106 +487,90 @@ __global__ __launch_bounds__(256) void k_sweep(const float *__restrict__ W, cons
             }
         };
 
-        if (PIPE) {
-            // Software pipeline over batches of U rows: the loads of batch b+1 are in
-            // flight while batch b's masks are dispatched. Entries past the union repeat
-            // its last row with an empty mask (an L1 hit, no adds).
-            const int nb = (cnt + U - 1) / U;
-            auto fetch = [&](int b, uint2 en[U], float w[U][NPL]) {
+        int k = 0;
+        for (; k + U <= cnt; k += U) {
+            uint2 en[U];
+            float w[U][NPL];
 #pragma unroll
-                for (int u = 0; u < U; ++u) {
-                    const int kk = b * U + u;
-                    en[u] = ent[kk < cnt ? kk : cnt - 1];
-                    if (kk >= cnt) en[u].y = 0u;
-                }
+            for (int u = 0; u < U; ++u) en[u] = ent[k + u];
 #pragma unroll
-                for (int u = 0; u < U; ++u) row_load(en[u].x, w[u]);
-            };
-            uint2 ea[U], eb[U];
-            float wa[U][NPL], wb[U][NPL];
-            if (nb > 0) fetch(0, ea, wa);
-            for (int b = 0; b < nb; b += 2) {
-                if (b + 1 < nb) fetch(b + 1, eb, wb);
+            for (int u = 0; u < U; ++u) row_load(en[u].x, w[u]);
 #pragma unroll
-                for (int u = 0; u < U; ++u) row_add(ea[u].y, wa[u]);
-                if (b + 1 >= nb) break;
-                if (b + 2 < nb) fetch(b + 2, ea, wa);
-#pragma unroll
-                for (int u = 0; u < U; ++u) row_add(eb[u].y, wb[u]);
-            }
-        } else {
-            int k = 0;
-            for (; k + U <= cnt; k += U) {
-                uint2 en[U];
-                float w[U][NPL];
-#pragma unroll
-                for (int u = 0; u < U; ++u) en[u] = ent[k + u];
-#pragma unroll
-                for (int u = 0; u < U; ++u) row_load(en[u].x, w[u]);
-#pragma unroll
-                for (int u = 0; u < U; ++u) row_add(en[u].y, w[u]);
-            }
-            for (; k < cnt; ++k) {
-                const uint2 en = ent[k];
-                float w[NPL];
-                row_load(en.x, w);
-                row_add(en.y, w);
-            }
+            for (int u = 0; u < U; ++u) row_add(en[u].y, w[u]);
+        }
+        for (; k < cnt; ++k) {
+            const uint2 en = ent[k];
+            float w[NPL];
+            row_load(en.x, w);
+            row_add(en.y, w);
         }
 
-        // fused argmin: d = ||w||^2 - 2*dot (fp64, one rounding), keyed; lane s keeps sample s
+        // fused argmin: d = ||w||^2 - 2*dot (fp64, one rounding), keyed. Each lane keeps
+        // its best key and that neuron's dot product; lane s then holds sample s's
+        // smallest key over the strip and the dot product of the lane that owns it
+        // (neuron index mod 256 = 4 * lane + j % 4).
         u64 mine = kKeyNone;
+        float mine_dot = 0.0f;
 #pragma unroll
         for (int s = 0; s < TA; ++s) {
             u64 best = kKeyNone;
+            float bdot = 0.0f;
 #pragma unroll
             for (int j = 0; j < NPL; ++j) {
                 const double d = fma(-2.0, (double)acc[s][j], nrm[j]);
-                const u64 key = (i0 + j < M) ? rank_key(d, (unsigned)(i0 + j)) : kKeyNone;
-                best = min_u64(best, key);
+                const u64 key = (nid[j] < M) ? rank_key(d, (unsigned)nid[j]) : kKeyNone;
+                if (key < best) {
+                    best = key;
+                    bdot = acc[s][j];
+                }
             }
             best = wave_min_u64(best);
-            if (lane == s) mine = best;
+            const int owner = (int)((best & 255) >> 2);
+            const float dot = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(bdot), owner));
+            if (lane == s) {
+                mine = best;
+                mine_dot = dot;
+            }
         }
         const int64_t row = t * TA + lane;
-        if (lane < TA && row < N) keys[strip * N + row] = mine;
+        if (lane < TA && row < N) {
+            keys[strip * N + row] = mine;
+            dots[strip * N + row] = mine_dot;
+        }
     }
 }
 
 // -------------------------------------------------------------- finalize
 
 // One thread per position k of the (possibly permuted) batch: smallest key over the
-// strips, then the winner's distance from the row's own ids, summed in the same
-// order and precision as the sweep; results go to sample perm[k] (k without a
-// permutation).
-__global__ __launch_bounds__(256) void k_finalize(const float *__restrict__ W, const double *__restrict__ norms,
-                                                  int32_t V, int64_t M, const int32_t *__restrict__ row_ptr,
-                                                  const int32_t *__restrict__ col_idx, int64_t N, int64_t nnz,
+// strips; the winner's dot product comes from the sweep (the same fp32 sum of the
+// row's weights in ascending feature order), so the full squared distance is
+// (||w||^2 - 2*dot) + nnz. Results go to sample perm[k] (k without a permutation).
+__global__ __launch_bounds__(256) void k_finalize(const double *__restrict__ norms, int64_t M,
+                                                  const int32_t *__restrict__ row_ptr, int64_t N, int64_t nnz,
                                                   const int32_t *__restrict__ perm, const u64 *__restrict__ keys,
-                                                  int64_t n_strips, int32_t *__restrict__ bmu,
-                                                  double *__restrict__ dist)
+                                                  const float *__restrict__ dots, int64_t n_strips,
+                                                  int32_t *__restrict__ bmu, double *__restrict__ dist)
 {
     const int64_t base = row_ptr[0];
     for (int64_t k = (int64_t)blockIdx.x * 256 + threadIdx.x; k < N; k += (int64_t)gridDim.x * 256) {
         const int64_t s = perm ? (int64_t)perm[k] : k;
         if (s < 0 || s >= N) continue;
         u64 best = kKeyNone;
-        for (int64_t g = 0; g < n_strips; ++g) best = min_u64(best, keys[g * N + k]);
+        int64_t gb = 0;
+        for (int64_t g = 0; g < n_strips; ++g) {
+            const u64 key = keys[g * N + k];
+            if (key < best) {
+                best = key;
+                gb = g;
+            }
+        }
         int64_t b = (int64_t)(best & kIndexMask);
         if (b >= M) b = M - 1;
         const int64_t rb = clamp64((int64_t)row_ptr[k] - base, 0, nnz);
         const int64_t re = clamp64((int64_t)row_ptr[k + 1] - base, rb, nnz);
-        float dot = 0.0f;
-        int cnt = 0;
-        for (int64_t p = rb; p < re; ++p) {
-            const int id = col_idx[base + p];
-            if (id >= 0 && id < V) {
-                dot += W[(size_t)id * (size_t)M + (size_t)b];
-                ++cnt;
-            }
-        }
         bmu[s] = (int32_t)b;
-        dist[s] = fma(-2.0, (double)dot, norms[b]) + (double)cnt;
+        dist[s] = fma(-2.0, (double)dots[gb * N + k], norms[b]) + (double)(re - rb);
     }
 }
 
@@ -592,42 +610,41 @@ hipError_t launch_plan(int ta, const int32_t *row_ptr, const int32_t *col_idx, i
 
 template <int TA, int NPL>
 static void sweep_ta(bool vec, dim3 grid, hipStream_t st, const float *W, const double *norms, int64_t M, int64_t N,
-                     int64_t V, int64_t nnz, const uint2 *plan, const int2 *tiles, int64_t nt, u64 *keys)
+                     int64_t V, int64_t nnz, const uint2 *plan, const int2 *tiles, int64_t nt, u64 *keys, float *dots)
 {
     if (vec)
-        hipLaunchKernelGGL((k_sweep<TA, NPL, 4, true, false>), grid, dim3(256), 0, st, W, norms, M, N, V, nnz, plan, tiles, nt,
-                           keys);
+        hipLaunchKernelGGL((k_sweep<TA, NPL, 4, true>), grid, dim3(256), 0, st, W, norms, M, N, V, nnz, plan, tiles, nt,
+                           keys, dots);
     else
-        hipLaunchKernelGGL((k_sweep<TA, NPL, 4, false, false>), grid, dim3(256), 0, st, W, norms, M, N, V, nnz, plan, tiles, nt,
-                           keys);
+        hipLaunchKernelGGL((k_sweep<TA, NPL, 4, false>), grid, dim3(256), 0, st, W, norms, M, N, V, nnz, plan, tiles, nt,
+                           keys, dots);
 }
 
 hipError_t launch_sweep(int ta, const float *W, const double *norms, int64_t M, int64_t N, int64_t V, int64_t nnz,
-                        const uint2 *plan, const int2 *tiles, unsigned long long *keys, hipStream_t st)
+                        const uint2 *plan, const int2 *tiles, unsigned long long *keys, float *dots, hipStream_t st)
 {
     const int64_t nt = n_tiles(N, ta);
     int64_t gx = (nt + 3) / 4;
     if (gx > (1 << 22)) gx = 1 << 22;
     const dim3 grid((unsigned)gx, (unsigned)n_strips(M, ta));
-    const int npl = neurons_per_lane(ta);
-    const bool vec = (M % npl == 0) && ((reinterpret_cast<uintptr_t>(W) & 15) == 0);
+    const bool vec = (M % 4 == 0) && ((reinterpret_cast<uintptr_t>(W) & 15) == 0);
     switch (ta) {
-    case 8: sweep_ta<8, 8>(vec, grid, st, W, norms, M, N, V, nnz, plan, tiles, nt, keys); break;
-    case 16: sweep_ta<16, 4>(vec, grid, st, W, norms, M, N, V, nnz, plan, tiles, nt, keys); break;
-    case 32: sweep_ta<32, 4>(vec, grid, st, W, norms, M, N, V, nnz, plan, tiles, nt, keys); break;
+    case 8: sweep_ta<8, 8>(vec, grid, st, W, norms, M, N, V, nnz, plan, tiles, nt, keys, dots); break;
+    case 16: sweep_ta<16, 4>(vec, grid, st, W, norms, M, N, V, nnz, plan, tiles, nt, keys, dots); break;
+    case 32: sweep_ta<32, 4>(vec, grid, st, W, norms, M, N, V, nnz, plan, tiles, nt, keys, dots); break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
 }
 
-hipError_t launch_finalize(int ta, const float *W, const double *norms, int64_t V, int64_t M, const int32_t *row_ptr,
-                           const int32_t *col_idx, int64_t N, int64_t nnz, const int32_t *perm,
-                           const unsigned long long *keys, int32_t *bmu, double *dist, hipStream_t st)
+hipError_t launch_finalize(int ta, const double *norms, int64_t M, const int32_t *row_ptr, int64_t N, int64_t nnz,
+                           const int32_t *perm, const unsigned long long *keys, const float *dots, int32_t *bmu,
+                           double *dist, hipStream_t st)
 {
     int64_t blocks = (N + 255) / 256;
     if (blocks > (1 << 22)) blocks = 1 << 22;
-    hipLaunchKernelGGL(k_finalize, dim3((unsigned)blocks), dim3(256), 0, st, W, norms, (int32_t)V, M, row_ptr,
-                       col_idx, N, nnz, perm, keys, n_strips(M, ta), bmu, dist);
+    hipLaunchKernelGGL(k_finalize, dim3((unsigned)blocks), dim3(256), 0, st, norms, M, row_ptr, N, nnz, perm, keys, dots,
+                       n_strips(M, ta), bmu, dist);
     return hipGetLastError();
 }
 
@@ -640,17 +657,20 @@ hipError_t launch_order(const int32_t *row_ptr, const int32_t *col_idx, int64_t 
     hipLaunchKernelGGL(k_fill_u32, dim3((unsigned)fb), dim3(256), 0, st, ob.freq, nb, 0u);
     hipLaunchKernelGGL(k_fill_u64, dim3((unsigned)fb), dim3(256), 0, st, ob.bucket, nb, 0ull);
     // enough workgroups to fill the chip, each with a large chunk of ids for its LDS histogram
-    int64_t hb = (nnz + 65535) / 65536;
+    const int64_t counted = nnz < kFreqSample ? nnz : kFreqSample;
+    int64_t hb = (counted + 65535) / 65536;
     if (hb < 1) hb = 1;
     if (hb > 1024) hb = 1024;
-    hipLaunchKernelGGL(k_freq, dim3((unsigned)hb), dim3(256), 0, st, row_ptr, col_idx, nnz, (int32_t)V, ob.freq);
+    hipLaunchKernelGGL(k_freq, dim3((unsigned)hb), dim3(256), 0, st, row_ptr, col_idx, counted, (int32_t)V, ob.freq);
     int64_t sb = (N + 255) / 256;
     if (sb > (1 << 22)) sb = 1 << 22;
     hipLaunchKernelGGL(k_rarest, dim3((unsigned)sb), dim3(256), 0, st, row_ptr, col_idx, N, nnz, (int32_t)V, ob.freq,
                        ob.skey, ob.bucket, flags);
     hipLaunchKernelGGL(k_bucket_scan, dim3(1), dim3(1024), 0, st, ob.bucket, nb, nnz, ob.prp + N);
-    hipLaunchKernelGGL(k_scatter, dim3((unsigned)sb), dim3(256), 0, st, row_ptr, col_idx, N, nnz, ob.skey, ob.bucket,
-                       ob.perm, ob.prp, ob.pci);
+    hipLaunchKernelGGL(k_place, dim3((unsigned)sb), dim3(256), 0, st, row_ptr, N, nnz, ob.skey, ob.bucket, ob.perm,
+                       ob.prp);
+    hipLaunchKernelGGL(k_gather, dim3((unsigned)sb), dim3(256), 0, st, row_ptr, col_idx, N, nnz, ob.perm, ob.prp,
+                       ob.pci);
     return hipGetLastError();
 }
 

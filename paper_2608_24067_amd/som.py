@@ -19,6 +19,7 @@ _LIB_PATH = os.path.join(_HERE, "libsom.so")
 
 SOM_OK, SOM_ERR_INVALID_ARG, SOM_ERR_BAD_CSR, SOM_ERR_WORKSPACE, SOM_ERR_HIP = range(5)
 MAX_NEURONS = 1 << 20
+DEFAULT_TILE_SAMPLES = 8
 FLAG_ID_RANGE, FLAG_UNSORTED, FLAG_ROW_PTR = 0x1, 0x2, 0x4
 
 EXPORTS = (
@@ -60,7 +61,7 @@ def load():
     lib.som_bmu_search.argtypes = [vp, vp, i64, i64, vp, vp, i64, i64, vp, vp, vp, sz, cfgp, vp]
     lib.som_bmu_plan.argtypes = [vp, vp, i64, i64, i64, i64, vp, sz, cfgp, vp]
     lib.som_bmu_sweep.argtypes = [vp, vp, i64, i64, i64, i64, vp, sz, cfgp, vp]
-    lib.som_bmu_finalize.argtypes = [vp, vp, i64, i64, vp, vp, i64, i64, vp, vp, vp, sz, cfgp, vp]
+    lib.som_bmu_finalize.argtypes = [vp, i64, i64, vp, i64, i64, vp, vp, vp, sz, cfgp, vp]
     lib.som_bmu_input_flags.argtypes = [vp, sz, i64, i64, i64, i64, cfgp, ctypes.POINTER(ctypes.c_uint32), vp]
     lib.som_validate_csr_host.argtypes = [vp, vp, i64, i64]
     for name in ("som_codebook_norms", "som_bmu_search", "som_bmu_plan", "som_bmu_sweep", "som_bmu_finalize",
@@ -184,16 +185,13 @@ def bmu_sweep(W, norms, V: int, M: int, N: int, nnz: int, workspace, tile_sample
     _check(st, "som_bmu_sweep")
 
 
-def bmu_finalize(W, norms, row_ptr, col_idx, V: int, M: int, nnz: int, bmu, dist, workspace, tile_samples: int = 0,
+def bmu_finalize(norms, row_ptr, V: int, M: int, nnz: int, bmu, dist, workspace, tile_samples: int = 0,
                  keep_order: bool = False):
     N = row_ptr.numel() - 1
-    if W.numel() != V * M:
-        raise ValueError("W must hold V*M elements")
-    rp, ci = _csr(row_ptr, col_idx, N, nnz)
     st = load().som_bmu_finalize(
-        _dev(W, "W", torch.float32), _dev(norms, "norms", torch.float64, M), V, M, rp, ci, N, nnz,
+        _dev(norms, "norms", torch.float64, M), V, M, _dev(row_ptr, "row_ptr", torch.int32, N + 1), N, nnz,
         _dev(bmu, "bmu", torch.int32, N), _dev(dist, "dist", torch.float64, N),
-        _dev(workspace, "workspace", torch.uint8), workspace.numel(), _cfg(tile_samples, keep_order), _stream(W))
+        _dev(workspace, "workspace", torch.uint8), workspace.numel(), _cfg(tile_samples, keep_order), _stream(norms))
     _check(st, "som_bmu_finalize")
 
 

@@ -30,6 +30,13 @@ def test_library_exports_every_declared_symbol():
         assert hasattr(lib, n), n
 
 
+def test_header_constants_match_binding():
+    text = open(os.path.join(ROOT, "include", "som.h")).read()
+    assert re.search(r"^#define SOM_DEFAULT_TILE_SAMPLES (\d+)$", text, re.M).group(1) == str(som.DEFAULT_TILE_SAMPLES)
+    assert re.search(r"^#define SOM_MAX_NEURONS \(1 << (\d+)\)$", text, re.M).group(1) == "20"
+    assert som.MAX_NEURONS == 1 << 20
+
+
 def test_workspace_bytes():
     n = som.workspace_bytes(10_000, 256, 2000, 120_000)
     assert n > 0 and n % 256 == 0
@@ -137,8 +144,10 @@ def test_phase_and_norms_argument_checks():
     assert lib.som_codebook_norms(FAKE, 0, 10, FAKE, None) == som.SOM_ERR_INVALID_ARG
     assert lib.som_bmu_plan(FAKE, FAKE, 10, 50, 100, 64, FAKE, 100, None, None) == som.SOM_ERR_WORKSPACE
     assert lib.som_bmu_sweep(FAKE, FAKE, 100, 64, 10, 50, FAKE, 100, None, None) == som.SOM_ERR_WORKSPACE
-    assert lib.som_bmu_finalize(FAKE, FAKE, 100, 64, FAKE, FAKE, 10, 50, FAKE, FAKE, FAKE, 100, None,
+    assert lib.som_bmu_finalize(FAKE, 100, 64, FAKE, 10, 50, FAKE, FAKE, FAKE, 100, None,
                                 None) == som.SOM_ERR_WORKSPACE
+    assert lib.som_bmu_finalize(None, 100, 64, FAKE, 10, 50, FAKE, FAKE, FAKE, 100, None,
+                                None) == som.SOM_ERR_INVALID_ARG
     out = ctypes.c_uint32(7)
     assert lib.som_bmu_input_flags(FAKE, 100, 10, 64, 100, 50, None, ctypes.byref(out), None) == som.SOM_ERR_WORKSPACE
     assert lib.som_bmu_input_flags(FAKE, 100, 10, 64, 100, 50, None, None, None) == som.SOM_ERR_INVALID_ARG

@@ -148,7 +148,7 @@ def test_phases_equal_search_and_flags_clean(dev):
     d2 = torch.empty(N, dtype=torch.float64, device=dev)
     som.bmu_plan(rpd, cid, V, M, nnz, ws)
     som.bmu_sweep(Wd, norms, V, M, N, nnz, ws)
-    som.bmu_finalize(Wd, norms, rpd, cid, V, M, nnz, b2, d2, ws)
+    som.bmu_finalize(norms, rpd, V, M, nnz, b2, d2, ws)
     assert som.input_flags(ws, N, M, V, nnz) == 0
     assert torch.equal(b1, b2) and torch.equal(d1, d2)
 
