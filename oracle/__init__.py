@@ -13,10 +13,15 @@ contiguous blocks, each block is evaluated by the single-threaded oracle
 merged with the same rule (smallest distance, then lowest index), so the
 merged answer equals one oracle call over the whole map.
 
+``bmu2`` returns the two best units per sample in the order (distance,
+index) -- the pair the paper's fused sweep produces (Figure 2 caption), which
+defines the topographic error -- plus the third distance, for margin checks.
+
 Parity status: pinned (see tests/test_oracle_pins.py) by exact integer
-arithmetic on quantised codebooks, scipy's cdist on both layouts, the
-expanded form of Eq. (1), planted and constant codebooks, and a mutation
-check that each plausible slip in oracle.c fails a pin.
+arithmetic on quantised codebooks (ranks 1-3 by a pure-Python sort for the
+two-best oracle), scipy's cdist on both layouts, the expanded form of Eq. (1),
+planted, tied and constant codebooks, and a mutation check that each
+plausible slip in oracle.c fails a pin.
 """
 from __future__ import annotations
 
@@ -53,6 +58,8 @@ def load(path: str | None = None):
     i64, vp = ctypes.c_int64, ctypes.c_void_p
     lib.som_bmu_oracle_host.argtypes = [vp, i64, i64, i64, i64, vp, vp, i64, vp, vp, vp]
     lib.som_bmu_oracle_host.restype = ctypes.c_int
+    lib.som_bmu2_oracle_host.argtypes = [vp, i64, i64, i64, i64, vp, vp, i64, vp, vp, vp, vp, vp]
+    lib.som_bmu2_oracle_host.restype = ctypes.c_int
     lib.som_norms_oracle_host.argtypes = [vp, i64, i64, i64, i64, vp]
     lib.som_norms_oracle_host.restype = ctypes.c_int
     return lib
@@ -97,6 +104,30 @@ def bmu(W: np.ndarray, row_ptr: np.ndarray, col_idx: np.ndarray, i0: int = 0, li
     return out_b, out_d, out_d2
 
 
+def bmu2(W: np.ndarray, row_ptr: np.ndarray, col_idx: np.ndarray, i0: int = 0, lib=None):
+    """The two best units of every CSR row over the neuron block W, ranked by (distance, index).
+
+    Returns (bmu, dist, bmu2, dist2, dist3): ranks 1 and 2 with global indices
+    (bmu2 = -1, dist2 = +inf for a one-neuron block) and the rank-3 distance.
+    """
+    ldw = _block_view(W)
+    V, B = W.shape
+    row_ptr = np.ascontiguousarray(row_ptr, dtype=np.int32)
+    col_idx = np.ascontiguousarray(col_idx, dtype=np.int32)
+    N = row_ptr.shape[0] - 1
+    b1 = np.empty(N, dtype=np.int32)
+    d1 = np.empty(N, dtype=np.float64)
+    b2 = np.empty(N, dtype=np.int32)
+    d2 = np.empty(N, dtype=np.float64)
+    d3 = np.empty(N, dtype=np.float64)
+    rc = _lib(lib).som_bmu2_oracle_host(W.ctypes.data, ldw, V, i0, i0 + B, row_ptr.ctypes.data,
+                                        col_idx.ctypes.data if col_idx.size else None, N, b1.ctypes.data,
+                                        d1.ctypes.data, b2.ctypes.data, d2.ctypes.data, d3.ctypes.data)
+    if rc != OK:
+        raise ValueError(f"som_bmu2_oracle_host returned {rc}")
+    return b1, d1, b2, d2, d3
+
+
 def norms(W: np.ndarray, lib=None) -> np.ndarray:
     """n_i = sum_v w_{v,i}^2 (fp64, v ascending) for every column of W."""
     ldw = _block_view(W)
@@ -126,6 +157,44 @@ def merge_blocks(parts):
         d = np.where(better, pd, d)
         d2 = new_d2
     return b, d, d2
+
+
+def merge_blocks2(parts):
+    """Merge per-block bmu2() results (any block order).
+
+    A unit in the global first two is among its own block's first two, so
+    ranks 1 and 2 are the first two of all blocks' first-two lists in the
+    order (distance, index); the k-th smallest distance of the whole map is
+    the k-th smallest of all blocks' first three distances.
+    """
+    cd = np.stack([p[1] for p in parts] + [p[3] for p in parts], axis=1)
+    cb = np.stack([p[0] for p in parts] + [p[2] for p in parts], axis=1).astype(np.int64)
+    cb = np.where(cb < 0, np.iinfo(np.int64).max, cb)  # an absent rank 2 sorts last
+    order = np.lexsort((cb, cd), axis=-1)
+    rows = np.arange(cd.shape[0])
+    b1 = cb[rows, order[:, 0]]
+    b2 = cb[rows, order[:, 1]]
+    dist_all = np.sort(np.stack([p[k] for p in parts for k in (1, 3, 4)], axis=1), axis=1)
+    d1, d2, d3 = dist_all[:, 0], dist_all[:, 1], dist_all[:, 2]
+    b2 = np.where(np.isinf(d2), -1, b2)
+    return b1.astype(np.int32), d1, b2.astype(np.int32), d2, d3
+
+
+def bmu2_streamed(block_fn: Callable[[int, int], np.ndarray], M: int, row_ptr: np.ndarray, col_idx: np.ndarray,
+                  block: int = 4096, nthreads: int = 1, lib=None):
+    """bmu2() over a whole map whose codebook is produced block by block (see bmu_streamed)."""
+    starts = list(range(0, M, block))
+
+    def run(i0):
+        i1 = min(M, i0 + block)
+        return bmu2(block_fn(i0, i1), row_ptr, col_idx, i0=i0, lib=lib)
+
+    if nthreads <= 1:
+        parts = [run(i0) for i0 in starts]
+    else:
+        with ThreadPoolExecutor(max_workers=nthreads) as ex:
+            parts = list(ex.map(run, starts))
+    return merge_blocks2(parts)
 
 
 def bmu_streamed(block_fn: Callable[[int, int], np.ndarray], M: int, row_ptr: np.ndarray, col_idx: np.ndarray,

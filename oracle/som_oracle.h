@@ -50,6 +50,20 @@ int som_bmu_oracle_host(const float *W, int64_t ldw, int64_t V, int64_t i0, int6
                         const int32_t *col_idx, int64_t N, int32_t *bmu, double *dist, double *dist2);
 
 /*
+ * The two best units over the same block, in the order (D_i, i): smallest
+ * distance first, the lower index first among equal distances (the tie-break
+ * above applied to every rank). The paper's fused sweep returns the two best
+ * units of each sample (Figure 2 caption); the second one defines the
+ * topographic error (Background, quality measures).
+ *   bmu, dist    rank 1, as som_bmu_oracle_host.
+ *   bmu2, dist2  rank 2 (global index); -1 and +inf if the block holds one neuron.
+ *   dist3        D of rank 3 (+inf if fewer than three neurons). May be NULL.
+ */
+int som_bmu2_oracle_host(const float *W, int64_t ldw, int64_t V, int64_t i0, int64_t i1, const int32_t *row_ptr,
+                         const int32_t *col_idx, int64_t N, int32_t *bmu, double *dist, int32_t *bmu2, double *dist2,
+                         double *dist3);
+
+/*
  * Per-neuron squared norms n_i = sum_v w_{v,i}^2 in fp64, v ascending, for
  * i in [i0, i1): norms[i - i0]. Same W layout as above.
  */

@@ -227,6 +227,79 @@ def check_error_codes(lib):
              None) == oracle.BAD_ARG
 
 
+# ------------------------------------------------- the two best units (top-2)
+
+def exact_ranks(Dint_row):
+    """Units in the order (distance, index) from exact integer distances: pure Python sort."""
+    return sorted(range(len(Dint_row)), key=lambda i: (int(Dint_row[i]), i))
+
+
+def check_top2_exact_integer(lib):
+    """Quantised codebook: ranks 1-3 from an exact int64 brute force and a Python sort on (D, i)."""
+    rp, ci, W = small_case(seed=22, N=60, V=200, M=37)
+    K = np.rint(W * 256).astype(np.int64)
+    X = dense_x(rp, ci, W.shape[0])
+    Dint = ((256 * X[:, :, None] - K[None, :, :]) ** 2).sum(axis=1)
+    b1, d1, b2, d2, d3 = oracle.bmu2(W, rp, ci, lib=lib)
+    for s in range(len(b1)):
+        r = exact_ranks(Dint[s])
+        assert (int(b1[s]), int(b2[s])) == (r[0], r[1]), f"sample {s}: ranks differ"
+        assert (d1[s] * 65536.0, d2[s] * 65536.0, d3[s] * 65536.0) == tuple(float(Dint[s, i]) for i in r[:3])
+
+
+def check_top2_ties_and_small_maps(lib):
+    """Three identical best prototypes at indices 9, 2, 5 rank 2 then 5 (d3 = 0 too); a planted
+    near-copy one feature away is the runner-up at distance 1; one and two neurons give -1 / +inf."""
+    rp, ci, W = small_case(seed=23, kind=synth.UNIFORM, N=8, V=120, M=20)
+    s = 3
+    ids = ci[rp[s]:rp[s + 1]]
+    Wt = W.copy()
+    for j in (9, 2, 5):
+        Wt[:, j] = 0.0
+        Wt[ids, j] = 1.0
+    b1, d1, b2, d2, d3 = oracle.bmu2(Wt, rp[s:s + 2], ci, lib=lib)
+    assert (int(b1[0]), int(b2[0])) == (2, 5) and d1[0] == d2[0] == d3[0] == 0.0
+    Wp = W.copy()
+    Wp[:, 11] = 0.0
+    Wp[ids, 11] = 1.0                   # exact copy of the input: distance 0
+    Wp[:, 4] = Wp[:, 11]
+    Wp[ids[0], 4] = 0.0                 # one active feature dropped: distance 1
+    b1, d1, b2, d2, d3 = oracle.bmu2(Wp, rp[s:s + 2], ci, lib=lib)
+    assert (int(b1[0]), float(d1[0]), int(b2[0]), float(d2[0])) == (11, 0.0, 4, 1.0) and d3[0] > 1.0
+    one = oracle.bmu2(np.ascontiguousarray(W[:, 7:8]), rp, ci, i0=7, lib=lib)
+    assert (one[0] == 7).all() and (one[2] == -1).all() and np.isinf(one[3]).all() and np.isinf(one[4]).all()
+    two = oracle.bmu2(np.ascontiguousarray(W[:, 7:9]), rp, ci, i0=7, lib=lib)
+    assert set(zip(two[0].tolist(), two[2].tolist())) <= {(7, 8), (8, 7)} and np.isinf(two[4]).all()
+
+
+def check_top2_cdist_and_top1(lib):
+    """Continuous codebook: scipy's distances sorted agree; rank 1 and the second distance equal
+    what the single-best oracle returns for the same rows."""
+    rp, ci, W = small_case(seed=24, kind=synth.UNIFORM, N=45, V=260, M=48)
+    X = dense_x(rp, ci, W.shape[0]).astype(np.float64)
+    D = cdist(X, np.ascontiguousarray(W.T).astype(np.float64), "sqeuclidean")
+    b1, d1, b2, d2, d3 = oracle.bmu2(W, rp, ci, lib=lib)
+    order = np.argsort(D, axis=1, kind="stable")
+    assert np.array_equal(b1, order[:, 0]) and np.array_equal(b2, order[:, 1])
+    srt = np.sort(D, axis=1)
+    for got, k in ((d1, 0), (d2, 1), (d3, 2)):
+        assert np.allclose(got, srt[:, k], rtol=1e-12, atol=0)
+    t1 = oracle.bmu(W, rp, ci, lib=lib)
+    assert np.array_equal(t1[0], b1) and np.array_equal(t1[1], d1) and np.array_equal(t1[2], d2)
+
+
+def check_top2_blocks(lib):
+    """Streamed over small neuron blocks and merged, ranks 1-3 equal one whole call."""
+    rp, ci, W = small_case(seed=25, N=40, V=150, M=45)
+    Wd = W.copy()
+    Wd[:, 30] = Wd[:, 3]  # an exact duplicate across blocks: the tie must still go to 3
+    whole = oracle.bmu2(Wd, rp, ci, lib=lib)
+    streamed = oracle.bmu2_streamed(lambda i0, i1: np.ascontiguousarray(Wd[:, i0:i1]), 45, rp, ci, block=6,
+                                    nthreads=2, lib=lib)
+    for a, b in zip(whole, streamed):
+        assert np.array_equal(a, b)
+
+
 ALL_CHECKS = [
     check_exact_integer_direct,
     check_cdist_node_major,
@@ -240,4 +313,8 @@ ALL_CHECKS = [
     check_offset_rows_and_blocks,
     check_norms,
     check_error_codes,
+    check_top2_exact_integer,
+    check_top2_ties_and_small_maps,
+    check_top2_cdist_and_top1,
+    check_top2_blocks,
 ]
