@@ -107,9 +107,9 @@ typedef struct {
  * host function; returns 0 if a size is out of range (see som_bmu_search)
  * or the config is invalid. The workspace must be 256-byte aligned device
  * memory. It holds the tile plan (8 bytes per id), one 8-byte partial key
- * per sample and strip of 512 neurons (256 when tile_samples > 8) and, unless
- * keep_order is set, the regrouped batch (4 bytes per id, 16 per sample, 12
- * per feature).
+ * and one 4-byte dot product per sample and strip of 512 neurons (256 when
+ * tile_samples > 8) and, unless keep_order is set, the regrouped batch (4
+ * bytes per id, 16 per sample, 12 per feature).
  */
 size_t som_bmu_workspace_bytes(int64_t N, int64_t M, int64_t V, int64_t nnz, const som_bmu_config *config);
 
@@ -177,6 +177,41 @@ som_status som_bmu_sweep(const float *W, const double *norms, int64_t V, int64_t
 som_status som_bmu_finalize(const double *norms, int64_t V, int64_t M, const int32_t *row_ptr, int64_t N, int64_t nnz,
                             int32_t *bmu, double *dist, void *workspace, size_t workspace_bytes,
                             const som_bmu_config *config, void *stream);
+
+/*
+ * The two best units per sample in the same fused sweep (SpMM-tile kernel
+ * section, Figure 2 caption; the pair defines the topographic error of the
+ * quality measures). Units are ranked by their distance, then by index:
+ *   bmu, dist    as som_bmu_search.
+ *   bmu2, dist2  device int32 [N] / fp64 [N], written: the next unit in that
+ *                order and its full squared distance; -1 and +inf if M == 1.
+ * The workspace must hold som_bmu2_workspace_bytes(N, M, V, nnz, config)
+ * bytes: the single-best workspace plus a second key and dot product per
+ * sample and strip. A two-best workspace also serves every single-best call
+ * and som_bmu_input_flags with the same config.
+ */
+size_t som_bmu2_workspace_bytes(int64_t N, int64_t M, int64_t V, int64_t nnz, const som_bmu_config *config);
+
+som_status som_bmu2_search(const float *W, const double *norms, int64_t V, int64_t M, const int32_t *row_ptr,
+                           const int32_t *col_idx, int64_t N, int64_t nnz, int32_t *bmu, double *dist, int32_t *bmu2,
+                           double *dist2, void *workspace, size_t workspace_bytes, const som_bmu_config *config,
+                           void *stream);
+
+/*
+ * Its phases: som_bmu_plan (shared with the single-best search), then
+ *   som_bmu2_sweep -- the fused sweep keeping, per sample and strip, the two
+ *     smallest keys and their neurons' dot products;
+ *   som_bmu2_finalize -- the two smallest keys over the strips, with their
+ *     full squared distances.
+ * Same arguments and ordering rules as the single-best phases, on a two-best
+ * workspace.
+ */
+som_status som_bmu2_sweep(const float *W, const double *norms, int64_t V, int64_t M, int64_t N, int64_t nnz,
+                          void *workspace, size_t workspace_bytes, const som_bmu_config *config, void *stream);
+
+som_status som_bmu2_finalize(const double *norms, int64_t V, int64_t M, const int32_t *row_ptr, int64_t N,
+                             int64_t nnz, int32_t *bmu, double *dist, int32_t *bmu2, double *dist2, void *workspace,
+                             size_t workspace_bytes, const som_bmu_config *config, void *stream);
 
 /*
  * Input flags (SOM_FLAG_*) the last plan on this workspace recorded. Waits

@@ -7,6 +7,10 @@ same names. PyTorch supplies device memory and streams only.
 from .som import (  # noqa: F401
     SomError,
     alloc_workspace,
+    alloc_workspace2,
+    bmu2_finalize,
+    bmu2_search,
+    bmu2_sweep,
     bmu_finalize,
     bmu_plan,
     bmu_search,
@@ -17,5 +21,6 @@ from .som import (  # noqa: F401
     library_path,
     load,
     validate_csr_host,
+    workspace2_bytes,
     workspace_bytes,
 )

@@ -74,15 +74,18 @@ struct Carved {
     int2 *tiles;
     unsigned long long *keys;
     float *dots;
+    unsigned long long *keys2;  // two-best search only
+    float *dots2;
     uint32_t *flags;
     som::OrderBuffers ob;
 };
 
-som_status carve(void *ws, size_t bytes, int64_t N, int64_t M, int64_t V, int64_t nnz, const Opts &o, Carved *c)
+som_status carve(void *ws, size_t bytes, int64_t N, int64_t M, int64_t V, int64_t nnz, const Opts &o, Carved *c,
+                 bool top2 = false)
 {
     if (!ws) return fail(SOM_ERR_WORKSPACE, "workspace is NULL");
     if (reinterpret_cast<uintptr_t>(ws) & 255) return fail(SOM_ERR_WORKSPACE, "workspace must be 256-byte aligned");
-    const som::Layout L = som::layout_for(N, M, V, nnz, o.ta, o.order);
+    const som::Layout L = som::layout_for(N, M, V, nnz, o.ta, o.order, top2);
     if (bytes < L.total)
         return fail(SOM_ERR_WORKSPACE, "workspace holds %zu bytes, the search needs %zu", bytes, L.total);
     char *b = static_cast<char *>(ws);
@@ -90,6 +93,8 @@ som_status carve(void *ws, size_t bytes, int64_t N, int64_t M, int64_t V, int64_
     c->tiles = reinterpret_cast<int2 *>(b + L.tiles);
     c->keys = reinterpret_cast<unsigned long long *>(b + L.keys);
     c->dots = reinterpret_cast<float *>(b + L.dots);
+    c->keys2 = reinterpret_cast<unsigned long long *>(b + L.keys2);
+    c->dots2 = reinterpret_cast<float *>(b + L.dots2);
     c->flags = reinterpret_cast<uint32_t *>(b + L.flags);
     c->ob.freq = reinterpret_cast<uint32_t *>(b + L.freq);
     c->ob.bucket = reinterpret_cast<unsigned long long *>(b + L.bucket);
@@ -102,13 +107,19 @@ som_status carve(void *ws, size_t bytes, int64_t N, int64_t M, int64_t V, int64_
 
 // Common prologue of the phases: options, N == 0 (a no-op), workspace.
 som_status setup(int64_t N, int64_t M, int64_t V, int64_t nnz, const som_bmu_config *config, void *workspace,
-                 size_t workspace_bytes, Opts *o, Carved *c, bool *noop)
+                 size_t workspace_bytes, Opts *o, Carved *c, bool *noop, bool top2 = false)
 {
     som_status st = parse(config, o);
     if (st != SOM_OK) return st;
     *noop = N == 0;
     if (*noop) return SOM_OK;
-    return carve(workspace, workspace_bytes, N, M, V, nnz, *o, c);
+    return carve(workspace, workspace_bytes, N, M, V, nnz, *o, c, top2);
+}
+
+bool dims_ok(int64_t N, int64_t M, int64_t V, int64_t nnz)
+{
+    return !(N < 0 || N >= INT32_MAX || M < 1 || M > SOM_MAX_NEURONS || V < 1 || V >= INT32_MAX || nnz < 0 ||
+             nnz > INT32_MAX);
 }
 
 }  // namespace
@@ -117,12 +128,18 @@ extern "C" {
 
 size_t som_bmu_workspace_bytes(int64_t N, int64_t M, int64_t V, int64_t nnz, const som_bmu_config *config)
 {
-    if (N < 0 || N >= INT32_MAX || M < 1 || M > SOM_MAX_NEURONS || V < 1 || V >= INT32_MAX || nnz < 0 ||
-        nnz > INT32_MAX)
-        return 0;
+    if (!dims_ok(N, M, V, nnz)) return 0;
     Opts o;
     if (parse(config, &o) != SOM_OK) return 0;
     return som::layout_for(N, M, V, nnz, o.ta, o.order).total;
+}
+
+size_t som_bmu2_workspace_bytes(int64_t N, int64_t M, int64_t V, int64_t nnz, const som_bmu_config *config)
+{
+    if (!dims_ok(N, M, V, nnz)) return 0;
+    Opts o;
+    if (parse(config, &o) != SOM_OK) return 0;
+    return som::layout_for(N, M, V, nnz, o.ta, o.order, true).total;
 }
 
 som_status som_codebook_norms(const float *W, int64_t V, int64_t M, double *norms, void *stream)
@@ -220,6 +237,68 @@ som_status som_bmu_search(const float *W, const double *norms, int64_t V, int64_
     if ((st = som_bmu_sweep(W, norms, V, M, N, nnz, workspace, workspace_bytes, config, stream)) != SOM_OK)
         return st;
     return som_bmu_finalize(norms, V, M, row_ptr, N, nnz, bmu, dist, workspace, workspace_bytes, config, stream);
+}
+
+som_status som_bmu2_sweep(const float *W, const double *norms, int64_t V, int64_t M, int64_t N, int64_t nnz,
+                          void *workspace, size_t workspace_bytes, const som_bmu_config *config, void *stream)
+{
+    Opts o;
+    Carved c;
+    bool noop;
+    som_status st = check_dims(N, M, V, nnz);
+    if (st != SOM_OK) return st;
+    if (N > 0 && (!W || !norms)) return fail(SOM_ERR_INVALID_ARG, "som_bmu2_sweep: null pointer");
+    if (reinterpret_cast<uintptr_t>(W) & 3) return fail(SOM_ERR_INVALID_ARG, "W must be 4-byte aligned");
+    if ((st = setup(N, M, V, nnz, config, workspace, workspace_bytes, &o, &c, &noop, true)) != SOM_OK) return st;
+    if (noop) return ok();
+    hipError_t e = som::launch_sweep2(o.ta, W, norms, M, N, V, nnz, c.plan, c.tiles, c.keys, c.dots, c.keys2,
+                                      c.dots2, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "som_bmu2_sweep launch");
+    return ok();
+}
+
+som_status som_bmu2_finalize(const double *norms, int64_t V, int64_t M, const int32_t *row_ptr, int64_t N,
+                             int64_t nnz, int32_t *bmu, double *dist, int32_t *bmu2, double *dist2, void *workspace,
+                             size_t workspace_bytes, const som_bmu_config *config, void *stream)
+{
+    Opts o;
+    Carved c;
+    bool noop;
+    som_status st = check_dims(N, M, V, nnz);
+    if (st != SOM_OK) return st;
+    if (N > 0 && (!norms || !row_ptr || !bmu || !dist || !bmu2 || !dist2))
+        return fail(SOM_ERR_INVALID_ARG, "som_bmu2_finalize: null pointer");
+    if ((st = setup(N, M, V, nnz, config, workspace, workspace_bytes, &o, &c, &noop, true)) != SOM_OK) return st;
+    if (noop) return ok();
+    const int32_t *rp = o.order ? c.ob.prp : row_ptr;
+    const int32_t *perm = o.order ? c.ob.perm : nullptr;
+    hipError_t e = som::launch_finalize2(o.ta, norms, M, rp, N, nnz, perm, c.keys, c.dots, c.keys2, c.dots2, bmu,
+                                         dist, bmu2, dist2, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "som_bmu2_finalize launch");
+    return ok();
+}
+
+som_status som_bmu2_search(const float *W, const double *norms, int64_t V, int64_t M, const int32_t *row_ptr,
+                           const int32_t *col_idx, int64_t N, int64_t nnz, int32_t *bmu, double *dist, int32_t *bmu2,
+                           double *dist2, void *workspace, size_t workspace_bytes, const som_bmu_config *config,
+                           void *stream)
+{
+    Opts o;
+    Carved c;
+    bool noop;
+    som_status st = check_dims(N, M, V, nnz);
+    if (st != SOM_OK) return st;
+    if (N > 0 && (!W || !norms || !row_ptr || (nnz > 0 && !col_idx) || !bmu || !dist || !bmu2 || !dist2))
+        return fail(SOM_ERR_INVALID_ARG, "som_bmu2_search: null pointer");
+    if (reinterpret_cast<uintptr_t>(W) & 3) return fail(SOM_ERR_INVALID_ARG, "W must be 4-byte aligned");
+    if ((st = setup(N, M, V, nnz, config, workspace, workspace_bytes, &o, &c, &noop, true)) != SOM_OK) return st;
+    if (noop) return ok();
+    // the plan phase is the single-best one (the layouts share their prefix)
+    if ((st = som_bmu_plan(row_ptr, col_idx, N, nnz, V, M, workspace, workspace_bytes, config, stream)) != SOM_OK)
+        return st;
+    if ((st = som_bmu2_sweep(W, norms, V, M, N, nnz, workspace, workspace_bytes, config, stream)) != SOM_OK) return st;
+    return som_bmu2_finalize(norms, V, M, row_ptr, N, nnz, bmu, dist, bmu2, dist2, workspace, workspace_bytes, config,
+                             stream);
 }
 
 som_status som_bmu_input_flags(const void *workspace, size_t workspace_bytes, int64_t N, int64_t M, int64_t V,

@@ -35,12 +35,15 @@ struct Layout {
     size_t perm;    // int32 [N]: sample at each position of the ordered batch
     size_t prp;     // int32 [N+1]: row pointers of the ordered batch
     size_t pci;     // int32 [nnz]: feature ids of the ordered batch
+    size_t keys2;   // uint64 [n_strips * N]: per-strip second-smallest keys (two-best search only)
+    size_t dots2;   // float [n_strips * N]: their dot products (two-best search only)
     size_t total;
 };
 
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-inline Layout layout_for(int64_t N, int64_t M, int64_t V, int64_t nnz, int ta, bool order)
+// The two-best sections come last, so a single-best layout is a prefix of the two-best one.
+inline Layout layout_for(int64_t N, int64_t M, int64_t V, int64_t nnz, int ta, bool order, bool top2 = false)
 {
     Layout L;
     size_t off = 0;
@@ -61,6 +64,9 @@ inline Layout layout_for(int64_t N, int64_t M, int64_t V, int64_t nnz, int ta, b
     L.perm = take(o * (size_t)N * 4);
     L.prp = take(o * (size_t)(N + 1) * 4);
     L.pci = take(o * (size_t)nnz * 4);
+    const size_t t2 = top2 ? 1 : 0;
+    L.keys2 = take(t2 * (size_t)n_strips(M, ta) * (size_t)N * 8);
+    L.dots2 = take(t2 * (size_t)n_strips(M, ta) * (size_t)N * 4);
     L.total = off;
     return L;
 }
@@ -81,6 +87,13 @@ hipError_t launch_sweep(int ta, const float *W, const double *norms, int64_t M, 
 hipError_t launch_finalize(int ta, const double *norms, int64_t M, const int32_t *row_ptr, int64_t N, int64_t nnz,
                            const int32_t *perm, const unsigned long long *keys, const float *dots, int32_t *bmu,
                            double *dist, hipStream_t st);
+hipError_t launch_sweep2(int ta, const float *W, const double *norms, int64_t M, int64_t N, int64_t V, int64_t nnz,
+                         const uint2 *plan, const int2 *tiles, unsigned long long *keys, float *dots,
+                         unsigned long long *keys2, float *dots2, hipStream_t st);
+hipError_t launch_finalize2(int ta, const double *norms, int64_t M, const int32_t *row_ptr, int64_t N, int64_t nnz,
+                            const int32_t *perm, const unsigned long long *keys, const float *dots,
+                            const unsigned long long *keys2, const float *dots2, int32_t *bmu, double *dist,
+                            int32_t *bmu2, double *dist2, hipStream_t st);
 hipError_t launch_order(const int32_t *row_ptr, const int32_t *col_idx, int64_t N, int64_t nnz, int64_t V,
                         const OrderBuffers &ob, uint32_t *flags, hipStream_t st);
 

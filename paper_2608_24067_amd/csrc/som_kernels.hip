@@ -104,6 +104,71 @@ __device__ __forceinline__ u64 wave_min_u64(u64 x)
     return r;
 }
 
+// Minimum / maximum of a float over the whole wave, as a scalar (NaN lanes are
+// ignored unless every lane is NaN).
+__device__ __forceinline__ float wave_min_f32(float x)
+{
+    x = fminf(x, __int_as_float(dpp<0xB1>(__float_as_int(x))));
+    x = fminf(x, __int_as_float(dpp<0x4E>(__float_as_int(x))));
+    x = fminf(x, __int_as_float(dpp<0x141>(__float_as_int(x))));
+    x = fminf(x, __int_as_float(dpp<0x140>(__float_as_int(x))));
+    float r = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 0));
+#pragma unroll
+    for (int row = 1; row < 4; ++row) r = fminf(r, __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), row * 16)));
+    return r;
+}
+
+__device__ __forceinline__ float wave_max_f32(float x)
+{
+    x = fmaxf(x, __int_as_float(dpp<0xB1>(__float_as_int(x))));
+    x = fmaxf(x, __int_as_float(dpp<0x4E>(__float_as_int(x))));
+    x = fmaxf(x, __int_as_float(dpp<0x141>(__float_as_int(x))));
+    x = fmaxf(x, __int_as_float(dpp<0x140>(__float_as_int(x))));
+    float r = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 0));
+#pragma unroll
+    for (int row = 1; row < 4; ++row) r = fmaxf(r, __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), row * 16)));
+    return r;
+}
+
+__device__ __forceinline__ u64 readlane_u64(u64 x, int l)
+{
+    const unsigned lo = (unsigned)__builtin_amdgcn_readlane((int)(unsigned)x, l);
+    const unsigned hi = (unsigned)__builtin_amdgcn_readlane((int)(unsigned)(x >> 32), l);
+    return ((u64)hi << 32) | lo;
+}
+
+// The two smallest of the wave's values, each lane contributing the pair
+// (a1 <= a2): merging (a1, a2) with (b1, b2) keeps min(a1, b1) and
+// min(max(a1, b1), min(a2, b2)). Results are scalars.
+__device__ __forceinline__ void min2_merge(float &a1, float &a2, float b1, float b2)
+{
+    const float lo = fminf(a1, b1);
+    a2 = fminf(fmaxf(a1, b1), fminf(a2, b2));
+    a1 = lo;
+}
+
+template <int CTRL>
+__device__ __forceinline__ void min2_step(float &a1, float &a2)
+{
+    const float b1 = __int_as_float(dpp<CTRL>(__float_as_int(a1)));
+    const float b2 = __int_as_float(dpp<CTRL>(__float_as_int(a2)));
+    min2_merge(a1, a2, b1, b2);
+}
+
+__device__ __forceinline__ void wave_min2_f32(float a1, float a2, float &r1, float &r2)
+{
+    min2_step<0xB1>(a1, a2);
+    min2_step<0x4E>(a1, a2);
+    min2_step<0x141>(a1, a2);
+    min2_step<0x140>(a1, a2);
+    r1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(a1), 0));
+    r2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(a2), 0));
+#pragma unroll
+    for (int row = 1; row < 4; ++row)
+        min2_merge(r1, r2, __int_as_float(__builtin_amdgcn_readlane(__float_as_int(a1), row * 16)),
+                   __int_as_float(__builtin_amdgcn_readlane(__float_as_int(a2), row * 16)));
+}
+
 // ----------------------------------------------------------------- norms
 
 // n_i = sum_v W[v*M+i]^2: one thread per neuron, v ascending, fp64. The square of
@@ -412,33 +477,44 @@ __global__ __launch_bounds__(256) void k_plan(const int32_t *__restrict__ row_pt
 // ----------------------------------------------------------------- sweep
 
 // Workgroup = 4 waves = 4 consecutive tiles x one strip (blockIdx.y) of 64*NPL
-// neurons; each lane owns NPL of them, in groups of four (see nid below). VEC: M is
-// a multiple of 4 and W 16-byte aligned, so each group is one aligned 16-byte load;
-// groups past M load a valid address and are never ranked. The plan is read
-// defensively (offsets, counts and ids clamped to the workspace and the codebook),
-// so even a workspace the plan never wrote cannot drive an access out of bounds.
-template <int TA, int NPL, int U, bool VEC>
+// neurons; each lane owns NPL of them, in groups of four (see loc below). VEC: M is
+// a multiple of 4 and W 16-byte aligned, so each group is one aligned 16-byte load.
+// The plan is read defensively (offsets, counts and ids clamped to the workspace
+// and the codebook), so even a workspace the plan never wrote cannot drive an
+// access out of bounds.
+//
+// TOP2: each (sample, strip) also gets its second-smallest key and that neuron's dot
+// product (keys2, dots2), for the two best units of the fused sweep.
+template <int TA, int NPL, int U, bool VEC, bool TOP2>
 __global__ __launch_bounds__(256) void k_sweep(const float *__restrict__ W, const double *__restrict__ norms,
                                                int64_t M, int64_t N, int64_t V, int64_t nnz,
                                                const uint2 *__restrict__ plan, const int2 *__restrict__ tiles,
-                                               int64_t n_tiles, u64 *__restrict__ keys, float *__restrict__ dots)
+                                               int64_t n_tiles, u64 *__restrict__ keys, float *__restrict__ dots,
+                                               u64 *__restrict__ keys2, float *__restrict__ dots2)
 {
     const int lane = threadIdx.x & 63;
     const int wv = wave_id();
     const int64_t strip = blockIdx.y;
-    // Element j of lane l is neuron strip*64*NPL + (j/4)*256 + 4l + j%4: each group of
-    // four is one 16-byte load, and the 64 lanes' loads of a group cover one
+    // M <= 2^20: neuron indices and byte offsets within a row fit in 32 bits.
+    const int Mi = (int)M;
+    const int base = (int)strip * (64 * NPL);  // first neuron of the strip
+    // Element j of lane l is neuron base + loc(j), loc(j) = (j/4)*256 + 4l + j%4: each
+    // group of four is one 16-byte load, and the 64 lanes' loads of a group cover one
     // contiguous KiB of the row.
-    int64_t nid[NPL], col[NPL];
+    const int l4 = lane * 4;
+    auto loc = [&](int j) { return (j / 4) * 256 + l4 + (j % 4); };
+
+    // fp64 norms, +inf past M (those neurons then never pass the candidate test
+    // below); nmax = the largest fp32 norm of the strip.
+    double nrm[NPL];
+    float nmax_l = 0.0f;
 #pragma unroll
     for (int j = 0; j < NPL; ++j) {
-        nid[j] = strip * (64 * NPL) + (int64_t)(j / 4) * 256 + (int64_t)lane * 4 + (j % 4);
-        const int64_t g = nid[j] - (j % 4);  // first neuron of the 16-byte group
-        col[j] = VEC ? (g < M ? g : M - 4) + (j % 4) : (nid[j] < M ? nid[j] : M - 1);
+        const int i = base + loc(j);
+        nrm[j] = i < Mi ? norms[i] : __builtin_inf();
+        if (i < Mi) nmax_l = fmaxf(nmax_l, (float)nrm[j]);
     }
-    double nrm[NPL];
-#pragma unroll
-    for (int j = 0; j < NPL; ++j) nrm[j] = norms[col[j]];
+    const float nmax = wave_max_f32(nmax_l);
     const unsigned vmax = (unsigned)(V - 1);
 
     for (int64_t tg = blockIdx.x; tg * 4 < n_tiles; tg += gridDim.x) {
@@ -457,12 +533,15 @@ __global__ __launch_bounds__(256) void k_sweep(const float *__restrict__ W, cons
 #pragma unroll
             for (int j = 0; j < NPL; ++j) acc[s][j] = 0.0f;
 
+        // Lanes whose group lies past M (last strip only) re-read the row's last group;
+        // those neurons are never ranked.
         auto row_load = [&](unsigned id, float w[NPL]) {
             const float *r = W + (size_t)(id < vmax ? id : vmax) * (size_t)M;
             if (VEC) {
 #pragma unroll
                 for (int j = 0; j < NPL; j += 4) {
-                    const v4f q = *reinterpret_cast<const v4f *>(r + col[j]);
+                    const int g = base + loc(j);
+                    const v4f q = *reinterpret_cast<const v4f *>(r + (g < Mi ? g : Mi - 4));
                     w[j] = q.x;
                     w[j + 1] = q.y;
                     w[j + 2] = q.z;
@@ -470,7 +549,10 @@ __global__ __launch_bounds__(256) void k_sweep(const float *__restrict__ W, cons
                 }
             } else {
 #pragma unroll
-                for (int j = 0; j < NPL; ++j) w[j] = r[col[j]];
+                for (int j = 0; j < NPL; ++j) {
+                    const int g = base + loc(j);
+                    w[j] = r[g < Mi ? g : Mi - 1];
+                }
             }
         };
         // The mask is wave-uniform: each bit is a scalar branch. The empty volatile
@@ -505,37 +587,163 @@ __global__ __launch_bounds__(256) void k_sweep(const float *__restrict__ W, cons
             row_add(en.y, w);
         }
 
-        // fused argmin: d = ||w||^2 - 2*dot (fp64, one rounding), keyed. Each lane keeps
-        // its best key and that neuron's dot product; lane s then holds sample s's
-        // smallest key over the strip and the dot product of the lane that owns it
-        // (neuron index mod 256 = 4 * lane + j % 4).
-        u64 mine = kKeyNone;
-        float mine_dot = 0.0f;
+        // Fused argmin, exact, in two stages. Stage 1 ranks the strip in fp32:
+        // da = fl32(fl32(n_i) - 2*dot) differs from the fp64 distance d = fl64(n_i - 2*dot)
+        // by at most 2^-24 (n_i + |da|) + 2^-53 |d|. So the neuron with the smallest key
+        // (smallest d to the key's 44 bits, then lowest index) has
+        // da <= min(da) + 2^-20 (nmax + |min(da)| + 1), which leaves room for both
+        // errors and for the key's 2^-32 relative truncation. Stage 2 forms the fp64
+        // distance and key of those candidates only -- usually one neuron in the strip
+        // -- so the smallest key is the one a full fp64 pass would find. A non-finite
+        // threshold (overflowing norms or sums) sends every neuron to stage 2.
+        float nf[NPL];  // converted once per tile (the asm keeps it out of the main loop's registers)
+#pragma unroll
+        for (int j = 0; j < NPL; ++j) {
+            double x = nrm[j];
+            asm volatile("" : "+v"(x));
+            nf[j] = (float)x;
+        }
+        u64 mine = kKeyNone, mine2 = kKeyNone;
+        float mine_dot = 0.0f, mine_dot2 = 0.0f;
 #pragma unroll
         for (int s = 0; s < TA; ++s) {
-            u64 best = kKeyNone;
-            float bdot = 0.0f;
+            float da[NPL];
+            if constexpr (!TOP2) {
+                float lmin = __builtin_inff();
 #pragma unroll
-            for (int j = 0; j < NPL; ++j) {
-                const double d = fma(-2.0, (double)acc[s][j], nrm[j]);
-                const u64 key = (nid[j] < M) ? rank_key(d, (unsigned)nid[j]) : kKeyNone;
-                if (key < best) {
-                    best = key;
-                    bdot = acc[s][j];
+                for (int j = 0; j < NPL; ++j) {
+                    da[j] = fmaf(-2.0f, acc[s][j], nf[j]);
+                    lmin = fminf(lmin, da[j]);
                 }
-            }
-            best = wave_min_u64(best);
-            const int owner = (int)((best & 255) >> 2);
-            const float dot = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(bdot), owner));
-            if (lane == s) {
-                mine = best;
-                mine_dot = dot;
+                const float wmin = wave_min_f32(lmin);
+                const float thr = wmin + 0x1p-20f * (nmax + fabsf(wmin) + 1.0f);
+                const bool every = !(fabsf(thr) <= __FLT_MAX__);
+                // Keys carry the neuron's index within the strip; the strip's first
+                // neuron is added once the strip's smallest key is known.
+                u64 best = kKeyNone;
+                float bdot = 0.0f;
+#pragma unroll
+                for (int j = 0; j < NPL; ++j) {
+                    const bool cand = every || da[j] <= thr;
+                    if (__builtin_amdgcn_ballot_w64(cand)) {
+                        const double d = fma(-2.0, (double)acc[s][j], nrm[j]);
+                        const bool take = cand && base + loc(j) < Mi;
+                        const u64 key = take ? rank_key(d, (unsigned)loc(j)) : kKeyNone;
+                        if (key < best) {
+                            best = key;
+                            bdot = acc[s][j];
+                        }
+                    }
+                }
+                // Lane s keeps sample s's smallest key over the strip and the dot
+                // product of the lane that owns it (index within the strip mod 256 =
+                // 4 * lane + j % 4).
+                const u64 holders = __builtin_amdgcn_ballot_w64(best != kKeyNone);
+                int owner;
+                if (__popcll(holders) == 1) {
+                    owner = __builtin_ctzll(holders);
+                    best = readlane_u64(best, owner);
+                } else {
+                    best = wave_min_u64(best);
+                    owner = (int)((best & 255) >> 2);
+                }
+                const float dot = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(bdot), owner));
+                if (best != kKeyNone) best += (u64)base;
+                if (lane == s) {
+                    mine = best;
+                    mine_dot = dot;
+                }
+            } else {
+                // Stage 1 with the two smallest approximate distances: the neurons of
+                // the two smallest keys have da <= (second smallest da) + eps.
+                float m1 = __builtin_inff(), m2 = __builtin_inff();
+#pragma unroll
+                for (int j = 0; j < NPL; ++j) {
+                    da[j] = fmaf(-2.0f, acc[s][j], nf[j]);
+                    m2 = fminf(m2, fmaxf(m1, da[j]));
+                    m1 = fminf(m1, da[j]);
+                }
+                float w1, w2;
+                wave_min2_f32(m1, m2, w1, w2);
+                const float thr = w2 + 0x1p-20f * (nmax + fabsf(w1) + fabsf(w2) + 1.0f);
+                const bool every = !(fabsf(thr) <= __FLT_MAX__);
+                u64 k1 = kKeyNone, k2 = kKeyNone;
+                float q1 = 0.0f, q2 = 0.0f;
+#pragma unroll
+                for (int j = 0; j < NPL; ++j) {
+                    const bool cand = every || da[j] <= thr;
+                    if (__builtin_amdgcn_ballot_w64(cand)) {
+                        const double d = fma(-2.0, (double)acc[s][j], nrm[j]);
+                        const bool take = cand && base + loc(j) < Mi;
+                        const u64 key = take ? rank_key(d, (unsigned)loc(j)) : kKeyNone;
+                        if (key < k1) {
+                            k2 = k1;
+                            q2 = q1;
+                            k1 = key;
+                            q1 = acc[s][j];
+                        } else if (key < k2) {
+                            k2 = key;
+                            q2 = acc[s][j];
+                        }
+                    }
+                }
+                // The two smallest keys of the wave (keys are distinct: each holds its
+                // neuron index), with the dot products of their neurons.
+                u64 K1, K2;
+                float D1, D2;
+                const u64 h1 = __builtin_amdgcn_ballot_w64(k1 != kKeyNone);
+                const u64 h2 = __builtin_amdgcn_ballot_w64(k2 != kKeyNone);
+                const int n1 = __popcll(h1), n2 = __popcll(h2);
+                if (n1 + n2 <= 2) {
+                    // at most two keys in the wave: read them directly
+                    const int la = n1 ? __builtin_ctzll(h1) : 0;
+                    u64 A = n1 ? readlane_u64(k1, la) : kKeyNone;
+                    float DA = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(q1), la));
+                    u64 B = kKeyNone;
+                    float DB = 0.0f;
+                    if (n1 == 2) {
+                        const int lb = __builtin_ctzll(h1 & (h1 - 1));
+                        B = readlane_u64(k1, lb);
+                        DB = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(q1), lb));
+                    } else if (n2 == 1) {
+                        B = readlane_u64(k2, la);
+                        DB = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(q2), la));
+                    }
+                    const bool swap = B < A;
+                    K1 = swap ? B : A;
+                    D1 = swap ? DB : DA;
+                    K2 = swap ? A : B;
+                    D2 = swap ? DA : DB;
+                } else {
+                    K1 = wave_min_u64(k1);
+                    const int o1 = __builtin_ctzll(__builtin_amdgcn_ballot_w64(k1 == K1));
+                    D1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(q1), o1));
+                    // the owner of K1 offers its second key, every other lane its first
+                    const u64 nxt = lane == o1 ? k2 : k1;
+                    const float nq = lane == o1 ? q2 : q1;
+                    K2 = wave_min_u64(nxt);
+                    const u64 h = __builtin_amdgcn_ballot_w64(nxt == K2 && K2 != kKeyNone);
+                    const int o2 = h ? __builtin_ctzll(h) : 0;
+                    D2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(nq), o2));
+                }
+                if (K1 != kKeyNone) K1 += (u64)base;
+                if (K2 != kKeyNone) K2 += (u64)base;
+                if (lane == s) {
+                    mine = K1;
+                    mine_dot = D1;
+                    mine2 = K2;
+                    mine_dot2 = D2;
+                }
             }
         }
         const int64_t row = t * TA + lane;
         if (lane < TA && row < N) {
             keys[strip * N + row] = mine;
             dots[strip * N + row] = mine_dot;
+            if constexpr (TOP2) {
+                keys2[strip * N + row] = mine2;
+                dots2[strip * N + row] = mine_dot2;
+            }
         }
     }
 }
@@ -574,6 +782,57 @@ __global__ __launch_bounds__(256) void k_finalize(const double *__restrict__ nor
     }
 }
 
+// Two best units: the two smallest of the 2 * n_strips keys of each sample (each
+// strip's two smallest), with their dot products from the sweep. Without a second
+// unit (M == 1) bmu2 = -1 and dist2 = +inf.
+__global__ __launch_bounds__(256) void k_finalize2(const double *__restrict__ norms, int64_t M,
+                                                   const int32_t *__restrict__ row_ptr, int64_t N, int64_t nnz,
+                                                   const int32_t *__restrict__ perm, const u64 *__restrict__ keys,
+                                                   const float *__restrict__ dots, const u64 *__restrict__ keys2,
+                                                   const float *__restrict__ dots2, int64_t n_strips,
+                                                   int32_t *__restrict__ bmu, double *__restrict__ dist,
+                                                   int32_t *__restrict__ bmu2, double *__restrict__ dist2)
+{
+    const int64_t base = row_ptr[0];
+    for (int64_t k = (int64_t)blockIdx.x * 256 + threadIdx.x; k < N; k += (int64_t)gridDim.x * 256) {
+        const int64_t s = perm ? (int64_t)perm[k] : k;
+        if (s < 0 || s >= N) continue;
+        u64 b1 = kKeyNone, b2 = kKeyNone;
+        float q1 = 0.0f, q2 = 0.0f;
+        auto offer = [&](u64 key, float q) {
+            if (key < b1) {
+                b2 = b1;
+                q2 = q1;
+                b1 = key;
+                q1 = q;
+            } else if (key < b2) {
+                b2 = key;
+                q2 = q;
+            }
+        };
+        for (int64_t g = 0; g < n_strips; ++g) {
+            offer(keys[g * N + k], dots[g * N + k]);
+            offer(keys2[g * N + k], dots2[g * N + k]);
+        }
+        const int64_t rb = clamp64((int64_t)row_ptr[k] - base, 0, nnz);
+        const int64_t re = clamp64((int64_t)row_ptr[k + 1] - base, rb, nnz);
+        const double len = (double)(re - rb);
+        int64_t i1 = (int64_t)(b1 & kIndexMask);
+        if (i1 >= M) i1 = M - 1;
+        bmu[s] = (int32_t)i1;
+        dist[s] = fma(-2.0, (double)q1, norms[i1]) + len;
+        if (b2 == kKeyNone) {
+            bmu2[s] = -1;
+            dist2[s] = __builtin_inf();
+        } else {
+            int64_t i2 = (int64_t)(b2 & kIndexMask);
+            if (i2 >= M) i2 = M - 1;
+            bmu2[s] = (int32_t)i2;
+            dist2[s] = fma(-2.0, (double)q2, norms[i2]) + len;
+        }
+    }
+}
+
 }  // namespace
 
 // --------------------------------------------------------------- launchers
@@ -608,20 +867,23 @@ hipError_t launch_plan(int ta, const int32_t *row_ptr, const int32_t *col_idx, i
     return hipGetLastError();
 }
 
-template <int TA, int NPL>
+template <int TA, int NPL, bool TOP2>
 static void sweep_ta(bool vec, dim3 grid, hipStream_t st, const float *W, const double *norms, int64_t M, int64_t N,
-                     int64_t V, int64_t nnz, const uint2 *plan, const int2 *tiles, int64_t nt, u64 *keys, float *dots)
+                     int64_t V, int64_t nnz, const uint2 *plan, const int2 *tiles, int64_t nt, u64 *keys, float *dots,
+                     u64 *keys2, float *dots2)
 {
     if (vec)
-        hipLaunchKernelGGL((k_sweep<TA, NPL, 4, true>), grid, dim3(256), 0, st, W, norms, M, N, V, nnz, plan, tiles, nt,
-                           keys, dots);
+        hipLaunchKernelGGL((k_sweep<TA, NPL, 4, true, TOP2>), grid, dim3(256), 0, st, W, norms, M, N, V, nnz, plan,
+                           tiles, nt, keys, dots, keys2, dots2);
     else
-        hipLaunchKernelGGL((k_sweep<TA, NPL, 4, false>), grid, dim3(256), 0, st, W, norms, M, N, V, nnz, plan, tiles, nt,
-                           keys, dots);
+        hipLaunchKernelGGL((k_sweep<TA, NPL, 4, false, TOP2>), grid, dim3(256), 0, st, W, norms, M, N, V, nnz, plan,
+                           tiles, nt, keys, dots, keys2, dots2);
 }
 
-hipError_t launch_sweep(int ta, const float *W, const double *norms, int64_t M, int64_t N, int64_t V, int64_t nnz,
-                        const uint2 *plan, const int2 *tiles, unsigned long long *keys, float *dots, hipStream_t st)
+template <bool TOP2>
+static hipError_t sweep_any(int ta, const float *W, const double *norms, int64_t M, int64_t N, int64_t V,
+                            int64_t nnz, const uint2 *plan, const int2 *tiles, u64 *keys, float *dots, u64 *keys2,
+                            float *dots2, hipStream_t st)
 {
     const int64_t nt = n_tiles(N, ta);
     int64_t gx = (nt + 3) / 4;
@@ -629,12 +891,25 @@ hipError_t launch_sweep(int ta, const float *W, const double *norms, int64_t M, 
     const dim3 grid((unsigned)gx, (unsigned)n_strips(M, ta));
     const bool vec = (M % 4 == 0) && ((reinterpret_cast<uintptr_t>(W) & 15) == 0);
     switch (ta) {
-    case 8: sweep_ta<8, 8>(vec, grid, st, W, norms, M, N, V, nnz, plan, tiles, nt, keys, dots); break;
-    case 16: sweep_ta<16, 4>(vec, grid, st, W, norms, M, N, V, nnz, plan, tiles, nt, keys, dots); break;
-    case 32: sweep_ta<32, 4>(vec, grid, st, W, norms, M, N, V, nnz, plan, tiles, nt, keys, dots); break;
+    case 8: sweep_ta<8, 8, TOP2>(vec, grid, st, W, norms, M, N, V, nnz, plan, tiles, nt, keys, dots, keys2, dots2); break;
+    case 16: sweep_ta<16, 4, TOP2>(vec, grid, st, W, norms, M, N, V, nnz, plan, tiles, nt, keys, dots, keys2, dots2); break;
+    case 32: sweep_ta<32, 4, TOP2>(vec, grid, st, W, norms, M, N, V, nnz, plan, tiles, nt, keys, dots, keys2, dots2); break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
+}
+
+hipError_t launch_sweep(int ta, const float *W, const double *norms, int64_t M, int64_t N, int64_t V, int64_t nnz,
+                        const uint2 *plan, const int2 *tiles, unsigned long long *keys, float *dots, hipStream_t st)
+{
+    return sweep_any<false>(ta, W, norms, M, N, V, nnz, plan, tiles, keys, dots, nullptr, nullptr, st);
+}
+
+hipError_t launch_sweep2(int ta, const float *W, const double *norms, int64_t M, int64_t N, int64_t V, int64_t nnz,
+                         const uint2 *plan, const int2 *tiles, unsigned long long *keys, float *dots,
+                         unsigned long long *keys2, float *dots2, hipStream_t st)
+{
+    return sweep_any<true>(ta, W, norms, M, N, V, nnz, plan, tiles, keys, dots, keys2, dots2, st);
 }
 
 hipError_t launch_finalize(int ta, const double *norms, int64_t M, const int32_t *row_ptr, int64_t N, int64_t nnz,
@@ -645,6 +920,18 @@ hipError_t launch_finalize(int ta, const double *norms, int64_t M, const int32_t
     if (blocks > (1 << 22)) blocks = 1 << 22;
     hipLaunchKernelGGL(k_finalize, dim3((unsigned)blocks), dim3(256), 0, st, norms, M, row_ptr, N, nnz, perm, keys, dots,
                        n_strips(M, ta), bmu, dist);
+    return hipGetLastError();
+}
+
+hipError_t launch_finalize2(int ta, const double *norms, int64_t M, const int32_t *row_ptr, int64_t N, int64_t nnz,
+                            const int32_t *perm, const unsigned long long *keys, const float *dots,
+                            const unsigned long long *keys2, const float *dots2, int32_t *bmu, double *dist,
+                            int32_t *bmu2, double *dist2, hipStream_t st)
+{
+    int64_t blocks = (N + 255) / 256;
+    if (blocks > (1 << 22)) blocks = 1 << 22;
+    hipLaunchKernelGGL(k_finalize2, dim3((unsigned)blocks), dim3(256), 0, st, norms, M, row_ptr, N, nnz, perm, keys,
+                       dots, keys2, dots2, n_strips(M, ta), bmu, dist, bmu2, dist2);
     return hipGetLastError();
 }
 

@@ -24,7 +24,9 @@ FLAG_ID_RANGE, FLAG_UNSORTED, FLAG_ROW_PTR = 0x1, 0x2, 0x4
 
 EXPORTS = (
     "som_bmu_workspace_bytes", "som_codebook_norms", "som_bmu_search", "som_bmu_plan", "som_bmu_sweep",
-    "som_bmu_finalize", "som_bmu_input_flags", "som_validate_csr_host", "som_last_error",
+    "som_bmu_finalize", "som_bmu2_workspace_bytes", "som_bmu2_search", "som_bmu2_sweep", "som_bmu2_finalize",
+    "som_bmu_input_flags",
+    "som_validate_csr_host", "som_last_error",
 )
 
 
@@ -62,10 +64,16 @@ def load():
     lib.som_bmu_plan.argtypes = [vp, vp, i64, i64, i64, i64, vp, sz, cfgp, vp]
     lib.som_bmu_sweep.argtypes = [vp, vp, i64, i64, i64, i64, vp, sz, cfgp, vp]
     lib.som_bmu_finalize.argtypes = [vp, i64, i64, vp, i64, i64, vp, vp, vp, sz, cfgp, vp]
+    lib.som_bmu2_workspace_bytes.argtypes = [i64, i64, i64, i64, cfgp]
+    lib.som_bmu2_workspace_bytes.restype = sz
+    lib.som_bmu2_search.argtypes = [vp, vp, i64, i64, vp, vp, i64, i64, vp, vp, vp, vp, vp, sz, cfgp, vp]
+    lib.som_bmu2_sweep.argtypes = [vp, vp, i64, i64, i64, i64, vp, sz, cfgp, vp]
+    lib.som_bmu2_finalize.argtypes = [vp, i64, i64, vp, i64, i64, vp, vp, vp, vp, vp, sz, cfgp, vp]
     lib.som_bmu_input_flags.argtypes = [vp, sz, i64, i64, i64, i64, cfgp, ctypes.POINTER(ctypes.c_uint32), vp]
     lib.som_validate_csr_host.argtypes = [vp, vp, i64, i64]
     for name in ("som_codebook_norms", "som_bmu_search", "som_bmu_plan", "som_bmu_sweep", "som_bmu_finalize",
-                 "som_bmu_input_flags", "som_validate_csr_host"):
+                 "som_bmu2_search", "som_bmu2_sweep", "som_bmu2_finalize", "som_bmu_input_flags",
+                 "som_validate_csr_host"):
         getattr(lib, name).restype = ctypes.c_int
     lib.som_last_error.argtypes = []
     lib.som_last_error.restype = ctypes.c_char_p
@@ -119,6 +127,18 @@ def alloc_workspace(N: int, M: int, V: int, nnz: int, device, tile_samples: int 
     return torch.empty(workspace_bytes(N, M, V, nnz, tile_samples, keep_order), dtype=torch.uint8, device=device)
 
 
+def workspace2_bytes(N: int, M: int, V: int, nnz: int, tile_samples: int = 0, keep_order: bool = False) -> int:
+    n = load().som_bmu2_workspace_bytes(N, M, V, nnz, _cfg(tile_samples, keep_order))
+    if n == 0:
+        raise ValueError("som_bmu2_workspace_bytes: invalid sizes or config")
+    return n
+
+
+def alloc_workspace2(N: int, M: int, V: int, nnz: int, device, tile_samples: int = 0,
+                     keep_order: bool = False) -> torch.Tensor:
+    return torch.empty(workspace2_bytes(N, M, V, nnz, tile_samples, keep_order), dtype=torch.uint8, device=device)
+
+
 def codebook_norms(W: torch.Tensor, V: int, M: int, out: torch.Tensor | None = None) -> torch.Tensor:
     """fp64 per-neuron squared norms of the feature-major V x M codebook W."""
     if W.numel() != V * M:
@@ -168,6 +188,34 @@ def bmu_search(W, norms, row_ptr, col_idx, V: int, M: int, nnz: int | None = Non
     return bmu, dist
 
 
+def bmu2_search(W, norms, row_ptr, col_idx, V: int, M: int, nnz: int | None = None, out=None, workspace=None,
+                tile_samples: int = 0, keep_order: bool = False):
+    """The two best units of every CSR row, ranked by (distance, index).
+
+    Returns (bmu, dist, bmu2, dist2); bmu2 = -1 and dist2 = +inf when M == 1.
+    ``out`` may pass the four output tensors.
+    """
+    N = row_ptr.numel() - 1
+    nnz = _nnz(row_ptr, N, nnz)
+    dev = W.device
+    if out is None:
+        out = (torch.empty(N, dtype=torch.int32, device=dev), torch.empty(N, dtype=torch.float64, device=dev),
+               torch.empty(N, dtype=torch.int32, device=dev), torch.empty(N, dtype=torch.float64, device=dev))
+    bmu, dist, bmu2, dist2 = out
+    if workspace is None:
+        workspace = alloc_workspace2(N, M, V, nnz, dev, tile_samples, keep_order)
+    if W.numel() != V * M:
+        raise ValueError("W must hold V*M elements")
+    rp, ci = _csr(row_ptr, col_idx, N, nnz)
+    st = load().som_bmu2_search(
+        _dev(W, "W", torch.float32), _dev(norms, "norms", torch.float64, M), V, M, rp, ci, N, nnz,
+        _dev(bmu, "bmu", torch.int32, N), _dev(dist, "dist", torch.float64, N),
+        _dev(bmu2, "bmu2", torch.int32, N), _dev(dist2, "dist2", torch.float64, N),
+        _dev(workspace, "workspace", torch.uint8), workspace.numel(), _cfg(tile_samples, keep_order), _stream(W))
+    _check(st, "som_bmu2_search")
+    return bmu, dist, bmu2, dist2
+
+
 def bmu_plan(row_ptr, col_idx, V: int, M: int, nnz: int, workspace, tile_samples: int = 0, keep_order: bool = False):
     N = row_ptr.numel() - 1
     rp, ci = _csr(row_ptr, col_idx, N, nnz)
@@ -194,6 +242,28 @@ def bmu_finalize(norms, row_ptr, V: int, M: int, nnz: int, bmu, dist, workspace,
         _dev(workspace, "workspace", torch.uint8), workspace.numel(), _cfg(tile_samples, keep_order), _stream(norms))
     _check(st, "som_bmu_finalize")
 
+
+
+def bmu2_sweep(W, norms, V: int, M: int, N: int, nnz: int, workspace, tile_samples: int = 0, keep_order: bool = False):
+    if W.numel() != V * M:
+        raise ValueError("W must hold V*M elements")
+    st = load().som_bmu2_sweep(_dev(W, "W", torch.float32), _dev(norms, "norms", torch.float64, M), V, M, N, nnz,
+                               _dev(workspace, "workspace", torch.uint8), workspace.numel(),
+                               _cfg(tile_samples, keep_order), _stream(W))
+    _check(st, "som_bmu2_sweep")
+
+
+def bmu2_finalize(norms, row_ptr, V: int, M: int, nnz: int, out, workspace, tile_samples: int = 0,
+                  keep_order: bool = False):
+    """out = (bmu, dist, bmu2, dist2) tensors, written."""
+    N = row_ptr.numel() - 1
+    bmu, dist, bmu2, dist2 = out
+    st = load().som_bmu2_finalize(
+        _dev(norms, "norms", torch.float64, M), V, M, _dev(row_ptr, "row_ptr", torch.int32, N + 1), N, nnz,
+        _dev(bmu, "bmu", torch.int32, N), _dev(dist, "dist", torch.float64, N),
+        _dev(bmu2, "bmu2", torch.int32, N), _dev(dist2, "dist2", torch.float64, N),
+        _dev(workspace, "workspace", torch.uint8), workspace.numel(), _cfg(tile_samples, keep_order), _stream(norms))
+    _check(st, "som_bmu2_finalize")
 
 def input_flags(workspace, N: int, M: int, V: int, nnz: int, tile_samples: int = 0, keep_order: bool = False) -> int:
     """SOM_FLAG_* bits the last plan recorded (waits for the current stream)."""

@@ -57,6 +57,29 @@ def test_workspace_bytes():
                                                                                                     120_000)
 
 
+
+def test_two_best_workspace_and_checks():
+    lib = som.load()
+    for tile, keep in ((0, False), (16, False), (32, True)):
+        n1 = som.workspace_bytes(10_000, 4096, 2000, 120_000, tile, keep)
+        n2 = som.workspace2_bytes(10_000, 4096, 2000, 120_000, tile, keep)
+        # a second 8-byte key and 4-byte dot product per sample and strip, appended
+        strips = -(-4096 // (512 if tile in (0, 8) else 256))
+        assert n2 >= n1 + 12 * 10_000 * strips and n2 % 256 == 0
+    assert lib.som_bmu2_workspace_bytes(-1, 256, 2000, 0, None) == 0
+    assert lib.som_bmu2_workspace_bytes(10, 256, 2000, 0, _cfg(12)) == 0
+    n1 = som.workspace_bytes(10, 64, 100, 50)
+    # null outputs, then a workspace that only fits the single-best search
+    assert lib.som_bmu2_search(FAKE, FAKE, 100, 64, FAKE, FAKE, 10, 50, FAKE, FAKE, None, FAKE, FAKE, 1 << 30, None,
+                               None) == som.SOM_ERR_INVALID_ARG
+    assert lib.som_bmu2_search(FAKE, FAKE, 100, 64, FAKE, FAKE, 10, 50, FAKE, FAKE, FAKE, FAKE, FAKE, n1, None,
+                               None) == som.SOM_ERR_WORKSPACE
+    assert lib.som_bmu2_search(FAKE, FAKE, 100, 0, FAKE, FAKE, 10, 50, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 30, None,
+                               None) == som.SOM_ERR_INVALID_ARG
+    # N == 0 is a no-op that touches nothing
+    assert lib.som_bmu2_search(None, None, 100, 64, None, None, 0, 0, None, None, None, None, None, 0, None,
+                               None) == som.SOM_OK
+
 def _status(rp, ci, V):
     lib = som.load()
     rp = np.ascontiguousarray(rp, dtype=np.int32)
