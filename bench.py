@@ -113,6 +113,8 @@ def main():
     ap.add_argument("--tile", type=int, default=0, help="tile_samples passed to the library (0 = default)")
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--dtype", choices=("f32", "f16"), default="f32",
+                    help="codebook storage: fp32 (the workloads' own) or fp16 (rounded from it; fp32 accumulation)")
     ap.add_argument("--top2", action="store_true",
                     help="time the two-best search (som_bmu2_*) instead of the single-best one")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -138,17 +140,24 @@ def main():
     row_ptr, col_idx = synth.make_csr(cfg.seed, N, V, cfg.lam, cfg.zipf_s)
     nnz = int(row_ptr[-1])
     alg_rows = int(synth.tile_distinct(row_ptr, col_idx, ALG_TILE).astype(np.int64).sum())
-    alg_bytes = 4.0 * M * alg_rows
+    elem = 2 if args.dtype == "f16" else 4
+    alg_bytes = float(elem) * M * alg_rows
     log(f"csr: N={N} nnz={nnz} distinct rows per 16-row tile total={alg_rows} ({time.perf_counter() - t0:.1f} s)")
 
     t0 = time.perf_counter()
     keep_host = 4 * V * M <= (2 << 30)
     if keep_host:
         W_host = synth.codebook(cfg.seed, cfg.kind, V, M)
-        W = torch.from_numpy(W_host).to(dev)
+        if args.dtype == "f16":
+            W_host = W_host.astype(np.float16)
+            W = torch.from_numpy(W_host).to(dev)
+            W_host = W_host.astype(np.float32)  # the values the oracle sees: exact widening
+        else:
+            W = torch.from_numpy(W_host).to(dev)
     else:
         W_host = None
-        W = synth.codebook_to_device(cfg.seed, cfg.kind, V, M, dev)
+        W = synth.codebook_to_device(cfg.seed, cfg.kind, V, M, dev,
+                                     dtype=torch.float16 if args.dtype == "f16" else torch.float32)
     rp = torch.from_numpy(row_ptr).to(dev)
     ci = torch.from_numpy(col_idx).to(dev)
     norms = torch.empty(M, dtype=torch.float64, device=dev)
@@ -159,7 +168,7 @@ def main():
     if args.top2:
         out2 = (bmu, dist, torch.empty(N, dtype=torch.int32, device=dev), torch.empty(N, dtype=torch.float64, device=dev))
     torch.cuda.synchronize()
-    log(f"inputs resident: codebook {4 * V * M / 1e9:.2f} GB, workspace {ws.numel() / 1e9:.2f} GB "
+    log(f"inputs resident: codebook {elem * V * M / 1e9:.2f} GB, workspace {ws.numel() / 1e9:.2f} GB "
         f"({time.perf_counter() - t0:.1f} s)")
 
     if args.calibrate_copy:
@@ -218,7 +227,7 @@ def main():
     sweep_s = phase_ms["sweep"] / 1e3
     achieved = alg_bytes / sweep_s / 1e9
     workload = cfg.describe()
-    traffic = None if args.top2 else measured_traffic(args.config)
+    traffic = None if (args.top2 or args.dtype != "f32") else measured_traffic(args.config)
 
     out = {
         "metric": METRIC,
@@ -231,12 +240,12 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32 sums, f64 norms and distances",
+        "dtype": ("f16 codebook, " if args.dtype == "f16" else "") + "f32 sums, f64 norms and distances",
         "data": "synthetic (seeded stand-in for the MEDLINE/MeSH corpus)",
         "config": {"workload": workload, "map": f"{cfg.edge}x{cfg.edge}", "M": M, "V": V, "N": N, "nnz": nnz,
                    "tile_samples": args.tile or som.DEFAULT_TILE_SAMPLES,
                    "keep_order": False, "alg_tile_samples": ALG_TILE, "parallelism": "single GPU",
-                   "search": "two best units" if args.top2 else "best unit"},
+                   "search": "two best units" if args.top2 else "best unit", "codebook": args.dtype},
         "effective_codebook_GBps": eff_gbps,
         "effective_pct_of_hbm_peak": 100.0 * eff_gbps / HBM_PEAK_GBPS,
         "effective_codebook_bytes_per_step": alg_bytes,

@@ -214,6 +214,34 @@ som_status som_bmu2_finalize(const double *norms, int64_t V, int64_t M, const in
                              size_t workspace_bytes, const som_bmu_config *config, void *stream);
 
 /*
+ * FP16 codebook storage (feature-major codebook section: the codebook is held
+ * in IEEE half precision and widened to fp32 only for the accumulation, which
+ * halves the bytes each codebook row costs). W holds
+ * V*M IEEE binary16 bit patterns, feature-major as above, 2-byte aligned
+ * (16-byte alignment and M a multiple of 8 select the vector loads). Every
+ * other argument, the workspace and the results are those of the fp32 entry
+ * point of the same name: the search on an fp16 codebook returns exactly what
+ * the fp32 search returns on the same values widened to fp32 (the widening
+ * and the squares are exact), so the oracle and the bars are unchanged.
+ */
+som_status som_codebook_norms_f16(const uint16_t *W, int64_t V, int64_t M, double *norms, void *stream);
+
+som_status som_bmu_search_f16(const uint16_t *W, const double *norms, int64_t V, int64_t M, const int32_t *row_ptr,
+                              const int32_t *col_idx, int64_t N, int64_t nnz, int32_t *bmu, double *dist,
+                              void *workspace, size_t workspace_bytes, const som_bmu_config *config, void *stream);
+
+som_status som_bmu_sweep_f16(const uint16_t *W, const double *norms, int64_t V, int64_t M, int64_t N, int64_t nnz,
+                             void *workspace, size_t workspace_bytes, const som_bmu_config *config, void *stream);
+
+som_status som_bmu2_search_f16(const uint16_t *W, const double *norms, int64_t V, int64_t M, const int32_t *row_ptr,
+                               const int32_t *col_idx, int64_t N, int64_t nnz, int32_t *bmu, double *dist,
+                               int32_t *bmu2, double *dist2, void *workspace, size_t workspace_bytes,
+                               const som_bmu_config *config, void *stream);
+
+som_status som_bmu2_sweep_f16(const uint16_t *W, const double *norms, int64_t V, int64_t M, int64_t N, int64_t nnz,
+                              void *workspace, size_t workspace_bytes, const som_bmu_config *config, void *stream);
+
+/*
  * Input flags (SOM_FLAG_*) the last plan on this workspace recorded. Waits
  * for `stream`, then copies one word to *flags (host). 0 means the device
  * saw a valid CSR.

@@ -122,6 +122,90 @@ bool dims_ok(int64_t N, int64_t M, int64_t V, int64_t nnz)
              nnz > INT32_MAX);
 }
 
+// A codebook: fp32, or IEEE binary16 bit patterns.
+struct Book {
+    const void *p;
+    bool f16;
+};
+
+som_status check_book(const Book &b, const char *who)
+{
+    if (reinterpret_cast<uintptr_t>(b.p) & (b.f16 ? 1 : 3))
+        return fail(SOM_ERR_INVALID_ARG, "%s: W must be %d-byte aligned", who, b.f16 ? 2 : 4);
+    return SOM_OK;
+}
+
+som_status norms_impl(const Book &b, int64_t V, int64_t M, double *norms, void *stream, const char *who)
+{
+    if (!b.p || !norms) return fail(SOM_ERR_INVALID_ARG, "%s: null pointer", who);
+    if (M < 1 || M > SOM_MAX_NEURONS || V < 1 || V >= INT32_MAX)
+        return fail(SOM_ERR_INVALID_ARG, "%s: need 1 <= M <= %d and 1 <= V < 2^31-1", who, SOM_MAX_NEURONS);
+    som_status st = check_book(b, who);
+    if (st != SOM_OK) return st;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipError_t e = b.f16 ? som::launch_norms_f16(static_cast<const uint16_t *>(b.p), V, M, norms, s)
+                         : som::launch_norms(static_cast<const float *>(b.p), V, M, norms, s);
+    if (e != hipSuccess) return hip_fail(e, who);
+    return ok();
+}
+
+som_status sweep_impl(const Book &b, bool top2, const double *norms, int64_t V, int64_t M, int64_t N, int64_t nnz,
+                      void *workspace, size_t workspace_bytes, const som_bmu_config *config, void *stream,
+                      const char *who)
+{
+    Opts o;
+    Carved c;
+    bool noop;
+    som_status st = check_dims(N, M, V, nnz);
+    if (st != SOM_OK) return st;
+    if (N > 0 && (!b.p || !norms)) return fail(SOM_ERR_INVALID_ARG, "%s: null pointer", who);
+    if ((st = check_book(b, who)) != SOM_OK) return st;
+    if ((st = setup(N, M, V, nnz, config, workspace, workspace_bytes, &o, &c, &noop, top2)) != SOM_OK) return st;
+    if (noop) return ok();
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipError_t e;
+    if (b.f16) {
+        const uint16_t *W = static_cast<const uint16_t *>(b.p);
+        e = top2 ? som::launch_sweep2_f16(o.ta, W, norms, M, N, V, nnz, c.plan, c.tiles, c.keys, c.dots, c.keys2,
+                                          c.dots2, s)
+                 : som::launch_sweep_f16(o.ta, W, norms, M, N, V, nnz, c.plan, c.tiles, c.keys, c.dots, s);
+    } else {
+        const float *W = static_cast<const float *>(b.p);
+        e = top2 ? som::launch_sweep2(o.ta, W, norms, M, N, V, nnz, c.plan, c.tiles, c.keys, c.dots, c.keys2, c.dots2,
+                                      s)
+                 : som::launch_sweep(o.ta, W, norms, M, N, V, nnz, c.plan, c.tiles, c.keys, c.dots, s);
+    }
+    if (e != hipSuccess) return hip_fail(e, who);
+    return ok();
+}
+
+som_status search_impl(const Book &b, const double *norms, int64_t V, int64_t M, const int32_t *row_ptr,
+                       const int32_t *col_idx, int64_t N, int64_t nnz, int32_t *bmu, double *dist, int32_t *bmu2,
+                       double *dist2, void *workspace, size_t workspace_bytes, const som_bmu_config *config,
+                       void *stream, const char *who)
+{
+    const bool top2 = bmu2 != nullptr || dist2 != nullptr;
+    Opts o;
+    Carved c;
+    bool noop;
+    som_status st = check_dims(N, M, V, nnz);
+    if (st != SOM_OK) return st;
+    if (N > 0 && (!b.p || !norms || !row_ptr || (nnz > 0 && !col_idx) || !bmu || !dist || (top2 && (!bmu2 || !dist2))))
+        return fail(SOM_ERR_INVALID_ARG, "%s: null pointer", who);
+    if ((st = check_book(b, who)) != SOM_OK) return st;
+    if ((st = setup(N, M, V, nnz, config, workspace, workspace_bytes, &o, &c, &noop, top2)) != SOM_OK) return st;
+    if (noop) return ok();
+    // the plan phase is shared (a single-best layout is a prefix of the two-best one)
+    if ((st = som_bmu_plan(row_ptr, col_idx, N, nnz, V, M, workspace, workspace_bytes, config, stream)) != SOM_OK)
+        return st;
+    if ((st = sweep_impl(b, top2, norms, V, M, N, nnz, workspace, workspace_bytes, config, stream, who)) != SOM_OK)
+        return st;
+    if (top2)
+        return som_bmu2_finalize(norms, V, M, row_ptr, N, nnz, bmu, dist, bmu2, dist2, workspace, workspace_bytes,
+                                 config, stream);
+    return som_bmu_finalize(norms, V, M, row_ptr, N, nnz, bmu, dist, workspace, workspace_bytes, config, stream);
+}
+
 }  // namespace
 
 extern "C" {
@@ -144,13 +228,12 @@ size_t som_bmu2_workspace_bytes(int64_t N, int64_t M, int64_t V, int64_t nnz, co
 
 som_status som_codebook_norms(const float *W, int64_t V, int64_t M, double *norms, void *stream)
 {
-    if (!W || !norms) return fail(SOM_ERR_INVALID_ARG, "som_codebook_norms: null pointer");
-    if (M < 1 || M > SOM_MAX_NEURONS || V < 1 || V >= INT32_MAX)
-        return fail(SOM_ERR_INVALID_ARG, "som_codebook_norms: need 1 <= M <= %d and 1 <= V < 2^31-1", SOM_MAX_NEURONS);
-    if (reinterpret_cast<uintptr_t>(W) & 3) return fail(SOM_ERR_INVALID_ARG, "W must be 4-byte aligned");
-    hipError_t e = som::launch_norms(W, V, M, norms, static_cast<hipStream_t>(stream));
-    if (e != hipSuccess) return hip_fail(e, "som_codebook_norms launch");
-    return ok();
+    return norms_impl(Book{W, false}, V, M, norms, stream, "som_codebook_norms");
+}
+
+som_status som_codebook_norms_f16(const uint16_t *W, int64_t V, int64_t M, double *norms, void *stream)
+{
+    return norms_impl(Book{W, true}, V, M, norms, stream, "som_codebook_norms_f16");
 }
 
 som_status som_bmu_plan(const int32_t *row_ptr, const int32_t *col_idx, int64_t N, int64_t nnz, int64_t V, int64_t M,
@@ -182,20 +265,15 @@ som_status som_bmu_plan(const int32_t *row_ptr, const int32_t *col_idx, int64_t 
 som_status som_bmu_sweep(const float *W, const double *norms, int64_t V, int64_t M, int64_t N, int64_t nnz,
                          void *workspace, size_t workspace_bytes, const som_bmu_config *config, void *stream)
 {
-    Opts o;
-    Carved c;
-    bool noop;
-    som_status st = check_dims(N, M, V, nnz);
-    if (st != SOM_OK) return st;
-    if (N > 0 && (!W || !norms)) return fail(SOM_ERR_INVALID_ARG, "som_bmu_sweep: null pointer");
-    if (reinterpret_cast<uintptr_t>(W) & 3) return fail(SOM_ERR_INVALID_ARG, "W must be 4-byte aligned");
-    if ((st = setup(N, M, V, nnz, config, workspace, workspace_bytes, &o, &c, &noop)) != SOM_OK) return st;
-    if (noop) return ok();
-    hipError_t e =
-        som::launch_sweep(o.ta, W, norms, M, N, V, nnz, c.plan, c.tiles, c.keys, c.dots,
-                         static_cast<hipStream_t>(stream));
-    if (e != hipSuccess) return hip_fail(e, "som_bmu_sweep launch");
-    return ok();
+    return sweep_impl(Book{W, false}, false, norms, V, M, N, nnz, workspace, workspace_bytes, config, stream,
+                      "som_bmu_sweep");
+}
+
+som_status som_bmu_sweep_f16(const uint16_t *W, const double *norms, int64_t V, int64_t M, int64_t N, int64_t nnz,
+                             void *workspace, size_t workspace_bytes, const som_bmu_config *config, void *stream)
+{
+    return sweep_impl(Book{W, true}, false, norms, V, M, N, nnz, workspace, workspace_bytes, config, stream,
+                      "som_bmu_sweep_f16");
 }
 
 som_status som_bmu_finalize(const double *norms, int64_t V, int64_t M, const int32_t *row_ptr, int64_t N, int64_t nnz,
@@ -222,39 +300,30 @@ som_status som_bmu_search(const float *W, const double *norms, int64_t V, int64_
                           const int32_t *col_idx, int64_t N, int64_t nnz, int32_t *bmu, double *dist,
                           void *workspace, size_t workspace_bytes, const som_bmu_config *config, void *stream)
 {
-    Opts o;
-    Carved c;
-    bool noop;
-    som_status st = check_dims(N, M, V, nnz);
-    if (st != SOM_OK) return st;
-    if (N > 0 && (!W || !norms || !row_ptr || (nnz > 0 && !col_idx) || !bmu || !dist))
-        return fail(SOM_ERR_INVALID_ARG, "som_bmu_search: null pointer");
-    if (reinterpret_cast<uintptr_t>(W) & 3) return fail(SOM_ERR_INVALID_ARG, "W must be 4-byte aligned");
-    if ((st = setup(N, M, V, nnz, config, workspace, workspace_bytes, &o, &c, &noop)) != SOM_OK) return st;
-    if (noop) return ok();
-    if ((st = som_bmu_plan(row_ptr, col_idx, N, nnz, V, M, workspace, workspace_bytes, config, stream)) != SOM_OK)
-        return st;
-    if ((st = som_bmu_sweep(W, norms, V, M, N, nnz, workspace, workspace_bytes, config, stream)) != SOM_OK)
-        return st;
-    return som_bmu_finalize(norms, V, M, row_ptr, N, nnz, bmu, dist, workspace, workspace_bytes, config, stream);
+    return search_impl(Book{W, false}, norms, V, M, row_ptr, col_idx, N, nnz, bmu, dist, nullptr, nullptr, workspace,
+                       workspace_bytes, config, stream, "som_bmu_search");
+}
+
+som_status som_bmu_search_f16(const uint16_t *W, const double *norms, int64_t V, int64_t M, const int32_t *row_ptr,
+                              const int32_t *col_idx, int64_t N, int64_t nnz, int32_t *bmu, double *dist,
+                              void *workspace, size_t workspace_bytes, const som_bmu_config *config, void *stream)
+{
+    return search_impl(Book{W, true}, norms, V, M, row_ptr, col_idx, N, nnz, bmu, dist, nullptr, nullptr, workspace,
+                       workspace_bytes, config, stream, "som_bmu_search_f16");
 }
 
 som_status som_bmu2_sweep(const float *W, const double *norms, int64_t V, int64_t M, int64_t N, int64_t nnz,
                           void *workspace, size_t workspace_bytes, const som_bmu_config *config, void *stream)
 {
-    Opts o;
-    Carved c;
-    bool noop;
-    som_status st = check_dims(N, M, V, nnz);
-    if (st != SOM_OK) return st;
-    if (N > 0 && (!W || !norms)) return fail(SOM_ERR_INVALID_ARG, "som_bmu2_sweep: null pointer");
-    if (reinterpret_cast<uintptr_t>(W) & 3) return fail(SOM_ERR_INVALID_ARG, "W must be 4-byte aligned");
-    if ((st = setup(N, M, V, nnz, config, workspace, workspace_bytes, &o, &c, &noop, true)) != SOM_OK) return st;
-    if (noop) return ok();
-    hipError_t e = som::launch_sweep2(o.ta, W, norms, M, N, V, nnz, c.plan, c.tiles, c.keys, c.dots, c.keys2,
-                                      c.dots2, static_cast<hipStream_t>(stream));
-    if (e != hipSuccess) return hip_fail(e, "som_bmu2_sweep launch");
-    return ok();
+    return sweep_impl(Book{W, false}, true, norms, V, M, N, nnz, workspace, workspace_bytes, config, stream,
+                      "som_bmu2_sweep");
+}
+
+som_status som_bmu2_sweep_f16(const uint16_t *W, const double *norms, int64_t V, int64_t M, int64_t N, int64_t nnz,
+                              void *workspace, size_t workspace_bytes, const som_bmu_config *config, void *stream)
+{
+    return sweep_impl(Book{W, true}, true, norms, V, M, N, nnz, workspace, workspace_bytes, config, stream,
+                      "som_bmu2_sweep_f16");
 }
 
 som_status som_bmu2_finalize(const double *norms, int64_t V, int64_t M, const int32_t *row_ptr, int64_t N,
@@ -283,22 +352,19 @@ som_status som_bmu2_search(const float *W, const double *norms, int64_t V, int64
                            double *dist2, void *workspace, size_t workspace_bytes, const som_bmu_config *config,
                            void *stream)
 {
-    Opts o;
-    Carved c;
-    bool noop;
-    som_status st = check_dims(N, M, V, nnz);
-    if (st != SOM_OK) return st;
-    if (N > 0 && (!W || !norms || !row_ptr || (nnz > 0 && !col_idx) || !bmu || !dist || !bmu2 || !dist2))
-        return fail(SOM_ERR_INVALID_ARG, "som_bmu2_search: null pointer");
-    if (reinterpret_cast<uintptr_t>(W) & 3) return fail(SOM_ERR_INVALID_ARG, "W must be 4-byte aligned");
-    if ((st = setup(N, M, V, nnz, config, workspace, workspace_bytes, &o, &c, &noop, true)) != SOM_OK) return st;
-    if (noop) return ok();
-    // the plan phase is the single-best one (the layouts share their prefix)
-    if ((st = som_bmu_plan(row_ptr, col_idx, N, nnz, V, M, workspace, workspace_bytes, config, stream)) != SOM_OK)
-        return st;
-    if ((st = som_bmu2_sweep(W, norms, V, M, N, nnz, workspace, workspace_bytes, config, stream)) != SOM_OK) return st;
-    return som_bmu2_finalize(norms, V, M, row_ptr, N, nnz, bmu, dist, bmu2, dist2, workspace, workspace_bytes, config,
-                             stream);
+    if (N > 0 && (!bmu2 || !dist2)) return fail(SOM_ERR_INVALID_ARG, "som_bmu2_search: null pointer");
+    return search_impl(Book{W, false}, norms, V, M, row_ptr, col_idx, N, nnz, bmu, dist, bmu2, dist2, workspace,
+                       workspace_bytes, config, stream, "som_bmu2_search");
+}
+
+som_status som_bmu2_search_f16(const uint16_t *W, const double *norms, int64_t V, int64_t M, const int32_t *row_ptr,
+                               const int32_t *col_idx, int64_t N, int64_t nnz, int32_t *bmu, double *dist,
+                               int32_t *bmu2, double *dist2, void *workspace, size_t workspace_bytes,
+                               const som_bmu_config *config, void *stream)
+{
+    if (N > 0 && (!bmu2 || !dist2)) return fail(SOM_ERR_INVALID_ARG, "som_bmu2_search_f16: null pointer");
+    return search_impl(Book{W, true}, norms, V, M, row_ptr, col_idx, N, nnz, bmu, dist, bmu2, dist2, workspace,
+                       workspace_bytes, config, stream, "som_bmu2_search_f16");
 }
 
 som_status som_bmu_input_flags(const void *workspace, size_t workspace_bytes, int64_t N, int64_t M, int64_t V,

@@ -79,6 +79,14 @@ struct OrderBuffers {
 
 // Kernel launchers (som_kernels.hip). Each returns the launch's hipError_t.
 hipError_t launch_norms(const float *W, int64_t V, int64_t M, double *norms, hipStream_t st);
+// fp16 codebooks: W holds IEEE binary16 bit patterns.
+hipError_t launch_norms_f16(const uint16_t *W, int64_t V, int64_t M, double *norms, hipStream_t st);
+hipError_t launch_sweep_f16(int ta, const uint16_t *W, const double *norms, int64_t M, int64_t N, int64_t V,
+                            int64_t nnz, const uint2 *plan, const int2 *tiles, unsigned long long *keys, float *dots,
+                            hipStream_t st);
+hipError_t launch_sweep2_f16(int ta, const uint16_t *W, const double *norms, int64_t M, int64_t N, int64_t V,
+                             int64_t nnz, const uint2 *plan, const int2 *tiles, unsigned long long *keys, float *dots,
+                             unsigned long long *keys2, float *dots2, hipStream_t st);
 hipError_t launch_clear_flags(uint32_t *flags, hipStream_t st);
 hipError_t launch_plan(int ta, const int32_t *row_ptr, const int32_t *col_idx, int64_t N, int64_t nnz, int64_t V,
                        uint2 *plan, int2 *tiles, uint32_t *flags, hipStream_t st);

@@ -35,6 +35,43 @@ namespace {
 
 typedef unsigned long long u64;
 typedef float v4f __attribute__((ext_vector_type(4)));
+typedef _Float16 h8 __attribute__((ext_vector_type(8)));
+typedef _Float16 h4 __attribute__((ext_vector_type(4)));
+
+// Codebook element types: fp32, or IEEE binary16 storage (the paper's FP16 codebook,
+// feature-major codebook section) widened to fp32 for the accumulation. Both
+// conversions to fp32 and fp64 are exact.
+//
+// Elements per vector load in the sweep: 16 bytes, but no more than a lane's
+// neurons (fp32: 4; fp16: 8, or 4 when a lane owns 4 neurons).
+template <typename E, int NPL>
+__host__ __device__ constexpr int group_elems()
+{
+    return (int)(16 / sizeof(E)) < NPL ? (int)(16 / sizeof(E)) : NPL;
+}
+
+// GRP consecutive elements at p (aligned to GRP * sizeof(E) bytes) as floats.
+template <typename E, int GRP>
+__device__ __forceinline__ void load_group(const E *p, float *w)
+{
+    if constexpr (sizeof(E) == 4) {
+        static_assert(GRP == 4, "fp32 groups are 16 bytes");
+        const v4f q = *reinterpret_cast<const v4f *>(p);
+        w[0] = q.x;
+        w[1] = q.y;
+        w[2] = q.z;
+        w[3] = q.w;
+    } else if constexpr (GRP == 8) {
+        const h8 q = *reinterpret_cast<const h8 *>(p);
+#pragma unroll
+        for (int k = 0; k < 8; ++k) w[k] = (float)q[k];
+    } else {
+        static_assert(GRP == 4, "fp16 groups are 8 or 16 bytes");
+        const h4 q = *reinterpret_cast<const h4 *>(p);
+#pragma unroll
+        for (int k = 0; k < 4; ++k) w[k] = (float)q[k];
+    }
+}
 
 constexpr u64 kKeyNone = ~0ull;
 constexpr u64 kIndexMask = (1ull << 20) - 1;
@@ -172,19 +209,20 @@ __device__ __forceinline__ void wave_min2_f32(float a1, float a2, float &r1, flo
 // ----------------------------------------------------------------- norms
 
 // n_i = sum_v W[v*M+i]^2: one thread per neuron, v ascending, fp64. The square of
-// an fp32 value is exact in fp64, so fma(w, w, acc) equals acc + w*w.
-__global__ __launch_bounds__(256) void k_norms(const float *__restrict__ W, int64_t V, int64_t M,
+// an fp32 (or fp16) value is exact in fp64, so fma(w, w, acc) equals acc + w*w.
+template <typename E>
+__global__ __launch_bounds__(256) void k_norms(const E *__restrict__ W, int64_t V, int64_t M,
                                                double *__restrict__ norms)
 {
     const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (i >= M) return;
-    const float *p = W + i;
+    const E *p = W + i;
     double acc = 0.0;
     int64_t v = 0;
     for (; v + 8 <= V; v += 8) {
         float w[8];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) w[u] = __builtin_nontemporal_load(p + (v + u) * M);
+        for (int u = 0; u < 8; ++u) w[u] = (float)__builtin_nontemporal_load(p + (v + u) * M);
 #pragma unroll
         for (int u = 0; u < 8; ++u) {
             const double x = (double)w[u];
@@ -192,7 +230,7 @@ __global__ __launch_bounds__(256) void k_norms(const float *__restrict__ W, int6
         }
     }
     for (; v < V; ++v) {
-        const double x = (double)p[v * M];
+        const double x = (double)(float)p[v * M];
         acc = fma(x, x, acc);
     }
     norms[i] = acc;
@@ -205,8 +243,8 @@ __global__ void k_clear_flags(uint32_t *flags) { flags[threadIdx.x] = 0u; }
 // Sample order. The post-submission section's tuning groups samples so that a
 // tile's rows share features. Here the samples of a batch are bucketed by their
 // least frequent feature in that batch: rows that share a rare feature land in
-// the same or neighbouring tiles, so unions shrink and the rare codebook rows
-// are re-read while still in L2. A sample's result does not depend on where it
+// the same or neighbouring tiles, which run close together in time, so a rare
+// codebook row is re-read while still in L2. A sample's result does not depend on where it
 // sits (its sum order is fixed by its own features), so the permutation never
 // shows in the output. The permuted batch is written to the workspace as a CSR
 // of its own (prp, pci); k_finalize maps positions back to samples.
@@ -485,8 +523,8 @@ __global__ __launch_bounds__(256) void k_plan(const int32_t *__restrict__ row_pt
 //
 // TOP2: each (sample, strip) also gets its second-smallest key and that neuron's dot
 // product (keys2, dots2), for the two best units of the fused sweep.
-template <int TA, int NPL, int U, bool VEC, bool TOP2>
-__global__ __launch_bounds__(256) void k_sweep(const float *__restrict__ W, const double *__restrict__ norms,
+template <typename E, int TA, int NPL, int U, bool VEC, bool TOP2>
+__global__ __launch_bounds__(256) void k_sweep(const E *__restrict__ W, const double *__restrict__ norms,
                                                int64_t M, int64_t N, int64_t V, int64_t nnz,
                                                const uint2 *__restrict__ plan, const int2 *__restrict__ tiles,
                                                int64_t n_tiles, u64 *__restrict__ keys, float *__restrict__ dots,
@@ -498,11 +536,21 @@ __global__ __launch_bounds__(256) void k_sweep(const float *__restrict__ W, cons
     // M <= 2^20: neuron indices and byte offsets within a row fit in 32 bits.
     const int Mi = (int)M;
     const int base = (int)strip * (64 * NPL);  // first neuron of the strip
-    // Element j of lane l is neuron base + loc(j), loc(j) = (j/4)*256 + 4l + j%4: each
-    // group of four is one 16-byte load, and the 64 lanes' loads of a group cover one
-    // contiguous KiB of the row.
-    const int l4 = lane * 4;
-    auto loc = [&](int j) { return (j / 4) * 256 + l4 + (j % 4); };
+    // Element j of lane l is neuron base + loc(j), loc(j) = (j/G)*64G + G*l + j%G with
+    // G = group_elems (4 for fp32): each group of G is one vector load, and the 64
+    // lanes' loads of a group cover one contiguous stretch of the row (1 KiB for fp32
+    // and for fp16 at 8 neurons per lane).
+    constexpr int G = group_elems<E, NPL>();
+    const int lg = lane * G;
+    // a lane's part of one codebook row, as stored
+    struct Seg {
+        typedef E vec __attribute__((ext_vector_type(G)));
+        union {
+            vec v[NPL / G];
+            E e[NPL];
+        };
+    };
+    auto loc = [&](int j) { return (j / G) * (64 * G) + lg + (j % G); };
 
     // fp64 norms, +inf past M (those neurons then never pass the candidate test
     // below); nmax = the largest fp32 norm of the strip.
@@ -517,15 +565,31 @@ __global__ __launch_bounds__(256) void k_sweep(const float *__restrict__ W, cons
     const float nmax = wave_max_f32(nmax_l);
     const unsigned vmax = (unsigned)(V - 1);
 
-    for (int64_t tg = blockIdx.x; tg * 4 < n_tiles; tg += gridDim.x) {
-        const int64_t t = tg * 4 + wv;
-        if (t >= n_tiles) break;  // wave-uniform; this kernel has no barriers
-        const int2 te = tiles[t];
-        const int64_t off = clamp64(te.x, 0, nnz);
+    // Tiles t, t + 4*gridDim.x, ... of this wave. The next tile's header (its plan
+    // offset and union size, and the next tile's offset that bounds it) and its first
+    // U plan entries are fetched while the current tile is still being worked on, so
+    // no scalar-load latency sits between two tiles.
+    const int64_t tstep = 4 * (int64_t)gridDim.x;
+    int64_t t = (int64_t)blockIdx.x * 4 + wv;
+    if (t >= n_tiles) return;  // wave-uniform; this kernel has no barriers
+    // header of tile tt from its table entry and the next tile's offset (nnz past the
+    // last tile): a tile's union never reaches the next tile's span
+    auto header = [&](int2 te, int next_off, int64_t &off_o, int &cnt_o) {
+        off_o = clamp64(te.x, 0, nnz);
+        cnt_o = (int)clamp64(te.y, 0, clamp64(next_off, off_o, nnz) - off_o);
+    };
+    auto next_offset = [&](int64_t tt) { return tt + 1 < n_tiles ? tiles[tt + 1].x : (int)nnz; };
+    int64_t off;
+    int cnt;
+    header(tiles[t], next_offset(t), off, cnt);
+    uint2 nx[U];
+    if (cnt >= U) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) nx[u] = plan[off + u];
+    }
+    for (;;) {
         const uint2 *ent = plan + off;
-        // a tile's union never reaches the next tile's span
-        const int64_t nxt = t + 1 < n_tiles ? clamp64(tiles[t + 1].x, off, nnz) : nnz;
-        const int cnt = (int)clamp64(te.y, 0, nxt - off);
+        const int64_t tn = t + tstep;
 
         float acc[TA][NPL];
 #pragma unroll
@@ -533,32 +597,37 @@ __global__ __launch_bounds__(256) void k_sweep(const float *__restrict__ W, cons
 #pragma unroll
             for (int j = 0; j < NPL; ++j) acc[s][j] = 0.0f;
 
-        // Lanes whose group lies past M (last strip only) re-read the row's last group;
-        // those neurons are never ranked.
-        auto row_load = [&](unsigned id, float w[NPL]) {
-            const float *r = W + (size_t)(id < vmax ? id : vmax) * (size_t)M;
-            if (VEC) {
+        // A row segment is held as loaded (fp16 stays packed, half the registers) and
+        // widened when it is added. Lanes whose group lies past M (last strip only)
+        // re-read the row's last group; those neurons are never ranked.
+        auto row_load = [&](unsigned id, Seg &seg) {
+            const E *r = W + (size_t)(id < vmax ? id : vmax) * (size_t)M;
+            if constexpr (VEC) {
 #pragma unroll
-                for (int j = 0; j < NPL; j += 4) {
-                    const int g = base + loc(j);
-                    const v4f q = *reinterpret_cast<const v4f *>(r + (g < Mi ? g : Mi - 4));
-                    w[j] = q.x;
-                    w[j + 1] = q.y;
-                    w[j + 2] = q.z;
-                    w[j + 3] = q.w;
+                for (int q = 0; q < NPL / G; ++q) {
+                    const int g = base + loc(q * G);
+                    seg.v[q] = *reinterpret_cast<const typename Seg::vec *>(r + (g < Mi ? g : Mi - G));
                 }
             } else {
 #pragma unroll
                 for (int j = 0; j < NPL; ++j) {
                     const int g = base + loc(j);
-                    w[j] = r[g < Mi ? g : Mi - 1];
+                    seg.e[j] = r[g < Mi ? g : Mi - 1];
                 }
             }
         };
         // The mask is wave-uniform: each bit is a scalar branch. The empty volatile
         // asm keeps the compiler from turning the branch into unconditional adds
         // and selects.
-        auto row_add = [&](unsigned mask, const float w[NPL]) {
+        auto row_add = [&](unsigned mask, const Seg &seg) {
+            float w[NPL];
+#pragma unroll
+            for (int j = 0; j < NPL; ++j) {
+                if constexpr (VEC)
+                    w[j] = (float)seg.v[j / G][j % G];
+                else
+                    w[j] = (float)seg.e[j];
+            }
 #pragma unroll
             for (int s = 0; s < TA; ++s) {
                 if (mask & (1u << s)) {
@@ -569,23 +638,39 @@ __global__ __launch_bounds__(256) void k_sweep(const float *__restrict__ W, cons
             }
         };
 
+        // U rows in flight; the next U plan entries are fetched (scalar loads) while
+        // the current rows are loaded and added.
         int k = 0;
         for (; k + U <= cnt; k += U) {
             uint2 en[U];
-            float w[U][NPL];
 #pragma unroll
-            for (int u = 0; u < U; ++u) en[u] = ent[k + u];
+            for (int u = 0; u < U; ++u) en[u] = nx[u];
+            if (k + 2 * U <= cnt) {
 #pragma unroll
-            for (int u = 0; u < U; ++u) row_load(en[u].x, w[u]);
+                for (int u = 0; u < U; ++u) nx[u] = ent[k + U + u];
+            }
+            Seg seg[U];
 #pragma unroll
-            for (int u = 0; u < U; ++u) row_add(en[u].y, w[u]);
+            for (int u = 0; u < U; ++u) row_load(en[u].x, seg[u]);
+#pragma unroll
+            for (int u = 0; u < U; ++u) row_add(en[u].y, seg[u]);
         }
         for (; k < cnt; ++k) {
             const uint2 en = ent[k];
-            float w[NPL];
-            row_load(en.x, w);
-            row_add(en.y, w);
+            Seg seg;
+            row_load(en.x, seg);
+            row_add(en.y, seg);
         }
+        // The next tile's table entries are read now, its first plan entries halfway
+        // through this tile's epilogue; both are in flight while the epilogue runs.
+        int2 te_n = make_int2(0, 0);
+        int next_n = 0;
+        if (tn < n_tiles) {
+            te_n = tiles[tn];
+            next_n = next_offset(tn);
+        }
+        int64_t off_n = 0;
+        int cnt_n = 0;
 
         // Fused argmin, exact, in two stages. Stage 1 ranks the strip in fp32:
         // da = fl32(fl32(n_i) - 2*dot) differs from the fp64 distance d = fl64(n_i - 2*dot)
@@ -607,6 +692,13 @@ __global__ __launch_bounds__(256) void k_sweep(const float *__restrict__ W, cons
         float mine_dot = 0.0f, mine_dot2 = 0.0f;
 #pragma unroll
         for (int s = 0; s < TA; ++s) {
+            if (s == TA / 2 && tn < n_tiles) {
+                header(te_n, next_n, off_n, cnt_n);
+                if (cnt_n >= U) {
+#pragma unroll
+                    for (int u = 0; u < U; ++u) nx[u] = plan[off_n + u];
+                }
+            }
             float da[NPL];
             if constexpr (!TOP2) {
                 float lmin = __builtin_inff();
@@ -636,8 +728,8 @@ __global__ __launch_bounds__(256) void k_sweep(const float *__restrict__ W, cons
                     }
                 }
                 // Lane s keeps sample s's smallest key over the strip and the dot
-                // product of the lane that owns it (index within the strip mod 256 =
-                // 4 * lane + j % 4).
+                // product of the lane that owns it (index within the strip mod 64G =
+                // G * lane + j % G).
                 const u64 holders = __builtin_amdgcn_ballot_w64(best != kKeyNone);
                 int owner;
                 if (__popcll(holders) == 1) {
@@ -645,7 +737,7 @@ __global__ __launch_bounds__(256) void k_sweep(const float *__restrict__ W, cons
                     best = readlane_u64(best, owner);
                 } else {
                     best = wave_min_u64(best);
-                    owner = (int)((best & 255) >> 2);
+                    owner = (int)((best & (64 * G - 1)) / G);
                 }
                 const float dot = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(bdot), owner));
                 if (best != kKeyNone) best += (u64)base;
@@ -745,6 +837,10 @@ __global__ __launch_bounds__(256) void k_sweep(const float *__restrict__ W, cons
                 dots2[strip * N + row] = mine_dot2;
             }
         }
+        if (tn >= n_tiles) break;
+        t = tn;
+        off = off_n;
+        cnt = cnt_n;
     }
 }
 
@@ -840,7 +936,15 @@ __global__ __launch_bounds__(256) void k_finalize2(const double *__restrict__ no
 hipError_t launch_norms(const float *W, int64_t V, int64_t M, double *norms, hipStream_t st)
 {
     const int64_t blocks = (M + 255) / 256;
-    hipLaunchKernelGGL(k_norms, dim3((unsigned)blocks), dim3(256), 0, st, W, V, M, norms);
+    hipLaunchKernelGGL(k_norms<float>, dim3((unsigned)blocks), dim3(256), 0, st, W, V, M, norms);
+    return hipGetLastError();
+}
+
+hipError_t launch_norms_f16(const uint16_t *W, int64_t V, int64_t M, double *norms, hipStream_t st)
+{
+    const int64_t blocks = (M + 255) / 256;
+    hipLaunchKernelGGL(k_norms<_Float16>, dim3((unsigned)blocks), dim3(256), 0, st,
+                       reinterpret_cast<const _Float16 *>(W), V, M, norms);
     return hipGetLastError();
 }
 
@@ -867,33 +971,49 @@ hipError_t launch_plan(int ta, const int32_t *row_ptr, const int32_t *col_idx, i
     return hipGetLastError();
 }
 
-template <int TA, int NPL, bool TOP2>
-static void sweep_ta(bool vec, dim3 grid, hipStream_t st, const float *W, const double *norms, int64_t M, int64_t N,
+template <typename E, int TA, int NPL, bool TOP2>
+static void sweep_ta(bool vec, dim3 grid, hipStream_t st, const E *W, const double *norms, int64_t M, int64_t N,
                      int64_t V, int64_t nnz, const uint2 *plan, const int2 *tiles, int64_t nt, u64 *keys, float *dots,
                      u64 *keys2, float *dots2)
 {
     if (vec)
-        hipLaunchKernelGGL((k_sweep<TA, NPL, 4, true, TOP2>), grid, dim3(256), 0, st, W, norms, M, N, V, nnz, plan,
+        hipLaunchKernelGGL((k_sweep<E, TA, NPL, 4, true, TOP2>), grid, dim3(256), 0, st, W, norms, M, N, V, nnz, plan,
                            tiles, nt, keys, dots, keys2, dots2);
     else
-        hipLaunchKernelGGL((k_sweep<TA, NPL, 4, false, TOP2>), grid, dim3(256), 0, st, W, norms, M, N, V, nnz, plan,
+        hipLaunchKernelGGL((k_sweep<E, TA, NPL, 4, false, TOP2>), grid, dim3(256), 0, st, W, norms, M, N, V, nnz, plan,
                            tiles, nt, keys, dots, keys2, dots2);
 }
 
-template <bool TOP2>
-static hipError_t sweep_any(int ta, const float *W, const double *norms, int64_t M, int64_t N, int64_t V,
-                            int64_t nnz, const uint2 *plan, const int2 *tiles, u64 *keys, float *dots, u64 *keys2,
-                            float *dots2, hipStream_t st)
+// Vector loads need M to be a multiple of the group and W aligned to the group's bytes.
+template <typename E, int NPL>
+static bool vector_loads(const E *W, int64_t M)
+{
+    constexpr int G = group_elems<E, NPL>();
+    return M % G == 0 && (reinterpret_cast<uintptr_t>(W) % (G * sizeof(E))) == 0;
+}
+
+template <typename E, bool TOP2>
+static hipError_t sweep_any(int ta, const E *W, const double *norms, int64_t M, int64_t N, int64_t V, int64_t nnz,
+                            const uint2 *plan, const int2 *tiles, u64 *keys, float *dots, u64 *keys2, float *dots2,
+                            hipStream_t st)
 {
     const int64_t nt = n_tiles(N, ta);
     int64_t gx = (nt + 3) / 4;
     if (gx > (1 << 22)) gx = 1 << 22;
     const dim3 grid((unsigned)gx, (unsigned)n_strips(M, ta));
-    const bool vec = (M % 4 == 0) && ((reinterpret_cast<uintptr_t>(W) & 15) == 0);
     switch (ta) {
-    case 8: sweep_ta<8, 8, TOP2>(vec, grid, st, W, norms, M, N, V, nnz, plan, tiles, nt, keys, dots, keys2, dots2); break;
-    case 16: sweep_ta<16, 4, TOP2>(vec, grid, st, W, norms, M, N, V, nnz, plan, tiles, nt, keys, dots, keys2, dots2); break;
-    case 32: sweep_ta<32, 4, TOP2>(vec, grid, st, W, norms, M, N, V, nnz, plan, tiles, nt, keys, dots, keys2, dots2); break;
+    case 8:
+        sweep_ta<E, 8, 8, TOP2>(vector_loads<E, 8>(W, M), grid, st, W, norms, M, N, V, nnz, plan, tiles, nt, keys, dots,
+                                keys2, dots2);
+        break;
+    case 16:
+        sweep_ta<E, 16, 4, TOP2>(vector_loads<E, 4>(W, M), grid, st, W, norms, M, N, V, nnz, plan, tiles, nt, keys,
+                                 dots, keys2, dots2);
+        break;
+    case 32:
+        sweep_ta<E, 32, 4, TOP2>(vector_loads<E, 4>(W, M), grid, st, W, norms, M, N, V, nnz, plan, tiles, nt, keys,
+                                 dots, keys2, dots2);
+        break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
@@ -902,14 +1022,30 @@ static hipError_t sweep_any(int ta, const float *W, const double *norms, int64_t
 hipError_t launch_sweep(int ta, const float *W, const double *norms, int64_t M, int64_t N, int64_t V, int64_t nnz,
                         const uint2 *plan, const int2 *tiles, unsigned long long *keys, float *dots, hipStream_t st)
 {
-    return sweep_any<false>(ta, W, norms, M, N, V, nnz, plan, tiles, keys, dots, nullptr, nullptr, st);
+    return sweep_any<float, false>(ta, W, norms, M, N, V, nnz, plan, tiles, keys, dots, nullptr, nullptr, st);
 }
 
 hipError_t launch_sweep2(int ta, const float *W, const double *norms, int64_t M, int64_t N, int64_t V, int64_t nnz,
                          const uint2 *plan, const int2 *tiles, unsigned long long *keys, float *dots,
                          unsigned long long *keys2, float *dots2, hipStream_t st)
 {
-    return sweep_any<true>(ta, W, norms, M, N, V, nnz, plan, tiles, keys, dots, keys2, dots2, st);
+    return sweep_any<float, true>(ta, W, norms, M, N, V, nnz, plan, tiles, keys, dots, keys2, dots2, st);
+}
+
+hipError_t launch_sweep_f16(int ta, const uint16_t *W, const double *norms, int64_t M, int64_t N, int64_t V,
+                            int64_t nnz, const uint2 *plan, const int2 *tiles, unsigned long long *keys, float *dots,
+                            hipStream_t st)
+{
+    return sweep_any<_Float16, false>(ta, reinterpret_cast<const _Float16 *>(W), norms, M, N, V, nnz, plan, tiles,
+                                      keys, dots, nullptr, nullptr, st);
+}
+
+hipError_t launch_sweep2_f16(int ta, const uint16_t *W, const double *norms, int64_t M, int64_t N, int64_t V,
+                             int64_t nnz, const uint2 *plan, const int2 *tiles, unsigned long long *keys, float *dots,
+                             unsigned long long *keys2, float *dots2, hipStream_t st)
+{
+    return sweep_any<_Float16, true>(ta, reinterpret_cast<const _Float16 *>(W), norms, M, N, V, nnz, plan, tiles,
+                                     keys, dots, keys2, dots2, st);
 }
 
 hipError_t launch_finalize(int ta, const double *norms, int64_t M, const int32_t *row_ptr, int64_t N, int64_t nnz,

@@ -25,6 +25,7 @@ FLAG_ID_RANGE, FLAG_UNSORTED, FLAG_ROW_PTR = 0x1, 0x2, 0x4
 EXPORTS = (
     "som_bmu_workspace_bytes", "som_codebook_norms", "som_bmu_search", "som_bmu_plan", "som_bmu_sweep",
     "som_bmu_finalize", "som_bmu2_workspace_bytes", "som_bmu2_search", "som_bmu2_sweep", "som_bmu2_finalize",
+    "som_codebook_norms_f16", "som_bmu_search_f16", "som_bmu_sweep_f16", "som_bmu2_search_f16", "som_bmu2_sweep_f16",
     "som_bmu_input_flags",
     "som_validate_csr_host", "som_last_error",
 )
@@ -69,6 +70,10 @@ def load():
     lib.som_bmu2_search.argtypes = [vp, vp, i64, i64, vp, vp, i64, i64, vp, vp, vp, vp, vp, sz, cfgp, vp]
     lib.som_bmu2_sweep.argtypes = [vp, vp, i64, i64, i64, i64, vp, sz, cfgp, vp]
     lib.som_bmu2_finalize.argtypes = [vp, i64, i64, vp, i64, i64, vp, vp, vp, vp, vp, sz, cfgp, vp]
+    # fp16 codebooks: the same arguments with W holding binary16 values
+    for name in ("som_codebook_norms", "som_bmu_search", "som_bmu_sweep", "som_bmu2_search", "som_bmu2_sweep"):
+        getattr(lib, name + "_f16").argtypes = getattr(lib, name).argtypes
+        getattr(lib, name + "_f16").restype = ctypes.c_int
     lib.som_bmu_input_flags.argtypes = [vp, sz, i64, i64, i64, i64, cfgp, ctypes.POINTER(ctypes.c_uint32), vp]
     lib.som_validate_csr_host.argtypes = [vp, vp, i64, i64]
     for name in ("som_codebook_norms", "som_bmu_search", "som_bmu_plan", "som_bmu_sweep", "som_bmu_finalize",
@@ -139,15 +144,24 @@ def alloc_workspace2(N: int, M: int, V: int, nnz: int, device, tile_samples: int
     return torch.empty(workspace2_bytes(N, M, V, nnz, tile_samples, keep_order), dtype=torch.uint8, device=device)
 
 
-def codebook_norms(W: torch.Tensor, V: int, M: int, out: torch.Tensor | None = None) -> torch.Tensor:
-    """fp64 per-neuron squared norms of the feature-major V x M codebook W."""
+def _book(W: torch.Tensor, V: int, M: int, entry: str):
+    """The entry point for W's element type (fp32, or fp16 storage: the name + "_f16") and W's pointer."""
+    if not isinstance(W, torch.Tensor):
+        raise TypeError("W must be a torch.Tensor")
     if W.numel() != V * M:
         raise ValueError("W must hold V*M elements")
-    wp = _dev(W, "W", torch.float32)
+    if W.dtype == torch.float16:
+        return getattr(load(), entry + "_f16"), _dev(W, "W", torch.float16), entry + "_f16"
+    return getattr(load(), entry), _dev(W, "W", torch.float32), entry
+
+
+def codebook_norms(W: torch.Tensor, V: int, M: int, out: torch.Tensor | None = None) -> torch.Tensor:
+    """fp64 per-neuron squared norms of the feature-major V x M codebook W (float32 or float16)."""
+    fn, wp, name = _book(W, V, M, "som_codebook_norms")
     if out is None:
         out = torch.empty(M, dtype=torch.float64, device=W.device)
     op = _dev(out, "norms", torch.float64, M)
-    _check(load().som_codebook_norms(wp, V, M, op, _stream(W)), "som_codebook_norms")
+    _check(fn(wp, V, M, op, _stream(W)), name)
     return out
 
 
@@ -177,14 +191,12 @@ def bmu_search(W, norms, row_ptr, col_idx, V: int, M: int, nnz: int | None = Non
         dist = torch.empty(N, dtype=torch.float64, device=dev)
     if workspace is None:
         workspace = alloc_workspace(N, M, V, nnz, dev, tile_samples, keep_order)
-    if W.numel() != V * M:
-        raise ValueError("W must hold V*M elements")
+    fn, wp, name = _book(W, V, M, "som_bmu_search")
     rp, ci = _csr(row_ptr, col_idx, N, nnz)
-    st = load().som_bmu_search(
-        _dev(W, "W", torch.float32), _dev(norms, "norms", torch.float64, M), V, M, rp, ci, N, nnz,
-        _dev(bmu, "bmu", torch.int32, N), _dev(dist, "dist", torch.float64, N),
-        _dev(workspace, "workspace", torch.uint8), workspace.numel(), _cfg(tile_samples, keep_order), _stream(W))
-    _check(st, "som_bmu_search")
+    st = fn(wp, _dev(norms, "norms", torch.float64, M), V, M, rp, ci, N, nnz,
+            _dev(bmu, "bmu", torch.int32, N), _dev(dist, "dist", torch.float64, N),
+            _dev(workspace, "workspace", torch.uint8), workspace.numel(), _cfg(tile_samples, keep_order), _stream(W))
+    _check(st, name)
     return bmu, dist
 
 
@@ -204,15 +216,13 @@ def bmu2_search(W, norms, row_ptr, col_idx, V: int, M: int, nnz: int | None = No
     bmu, dist, bmu2, dist2 = out
     if workspace is None:
         workspace = alloc_workspace2(N, M, V, nnz, dev, tile_samples, keep_order)
-    if W.numel() != V * M:
-        raise ValueError("W must hold V*M elements")
+    fn, wp, name = _book(W, V, M, "som_bmu2_search")
     rp, ci = _csr(row_ptr, col_idx, N, nnz)
-    st = load().som_bmu2_search(
-        _dev(W, "W", torch.float32), _dev(norms, "norms", torch.float64, M), V, M, rp, ci, N, nnz,
-        _dev(bmu, "bmu", torch.int32, N), _dev(dist, "dist", torch.float64, N),
-        _dev(bmu2, "bmu2", torch.int32, N), _dev(dist2, "dist2", torch.float64, N),
-        _dev(workspace, "workspace", torch.uint8), workspace.numel(), _cfg(tile_samples, keep_order), _stream(W))
-    _check(st, "som_bmu2_search")
+    st = fn(wp, _dev(norms, "norms", torch.float64, M), V, M, rp, ci, N, nnz,
+            _dev(bmu, "bmu", torch.int32, N), _dev(dist, "dist", torch.float64, N),
+            _dev(bmu2, "bmu2", torch.int32, N), _dev(dist2, "dist2", torch.float64, N),
+            _dev(workspace, "workspace", torch.uint8), workspace.numel(), _cfg(tile_samples, keep_order), _stream(W))
+    _check(st, name)
     return bmu, dist, bmu2, dist2
 
 
@@ -225,12 +235,10 @@ def bmu_plan(row_ptr, col_idx, V: int, M: int, nnz: int, workspace, tile_samples
 
 
 def bmu_sweep(W, norms, V: int, M: int, N: int, nnz: int, workspace, tile_samples: int = 0, keep_order: bool = False):
-    if W.numel() != V * M:
-        raise ValueError("W must hold V*M elements")
-    st = load().som_bmu_sweep(_dev(W, "W", torch.float32), _dev(norms, "norms", torch.float64, M), V, M, N, nnz,
-                              _dev(workspace, "workspace", torch.uint8), workspace.numel(),
-                              _cfg(tile_samples, keep_order), _stream(W))
-    _check(st, "som_bmu_sweep")
+    fn, wp, name = _book(W, V, M, "som_bmu_sweep")
+    st = fn(wp, _dev(norms, "norms", torch.float64, M), V, M, N, nnz, _dev(workspace, "workspace", torch.uint8),
+            workspace.numel(), _cfg(tile_samples, keep_order), _stream(W))
+    _check(st, name)
 
 
 def bmu_finalize(norms, row_ptr, V: int, M: int, nnz: int, bmu, dist, workspace, tile_samples: int = 0,
@@ -245,12 +253,10 @@ def bmu_finalize(norms, row_ptr, V: int, M: int, nnz: int, bmu, dist, workspace,
 
 
 def bmu2_sweep(W, norms, V: int, M: int, N: int, nnz: int, workspace, tile_samples: int = 0, keep_order: bool = False):
-    if W.numel() != V * M:
-        raise ValueError("W must hold V*M elements")
-    st = load().som_bmu2_sweep(_dev(W, "W", torch.float32), _dev(norms, "norms", torch.float64, M), V, M, N, nnz,
-                               _dev(workspace, "workspace", torch.uint8), workspace.numel(),
-                               _cfg(tile_samples, keep_order), _stream(W))
-    _check(st, "som_bmu2_sweep")
+    fn, wp, name = _book(W, V, M, "som_bmu2_sweep")
+    st = fn(wp, _dev(norms, "norms", torch.float64, M), V, M, N, nnz, _dev(workspace, "workspace", torch.uint8),
+            workspace.numel(), _cfg(tile_samples, keep_order), _stream(W))
+    _check(st, name)
 
 
 def bmu2_finalize(norms, row_ptr, V: int, M: int, nnz: int, out, workspace, tile_samples: int = 0,

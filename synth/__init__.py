@@ -151,15 +151,18 @@ def tile_distinct(row_ptr: np.ndarray, col_idx: np.ndarray, TA: int = 16, nthrea
 
 
 def codebook_to_device(seed: int, kind: int, V: int, M: int, device, chunk_bytes: int = 1 << 28,
-                       nthreads: int | None = None):
-    """The whole V x M codebook as a float32 device tensor, drawn on the host in row chunks.
+                       nthreads: int | None = None, dtype=None):
+    """The whole V x M codebook as a device tensor, drawn on the host in row chunks.
 
     Two pinned staging buffers alternate, so drawing the next chunk overlaps
-    the copy of the previous one; host memory stays at two chunks.
+    the copy of the previous one; host memory stays at two chunks. With
+    dtype=torch.float16 each chunk is rounded to binary16 on the device
+    (round to nearest even, as numpy's astype(np.float16)).
     """
     import torch
 
-    W = torch.empty((V, M), dtype=torch.float32, device=device)
+    dtype = dtype or torch.float32
+    W = torch.empty((V, M), dtype=dtype, device=device)
     rows = max(1, min(V, chunk_bytes // (4 * M)))
     bufs = [torch.empty((rows, M), dtype=torch.float32, pin_memory=True) for _ in range(2)]
     events = [None, None]
@@ -171,7 +174,10 @@ def codebook_to_device(seed: int, kind: int, V: int, M: int, device, chunk_bytes
             events[k].synchronize()
         host = bufs[k][: v1 - v0]
         codebook(seed, kind, V, M, v0, v1, 0, M, out=host.numpy(), nthreads=nthreads)
-        W[v0:v1].copy_(host, non_blocking=True)
+        if dtype == torch.float32:
+            W[v0:v1].copy_(host, non_blocking=True)
+        else:
+            W[v0:v1].copy_(host.to(device, non_blocking=True))
         ev = torch.cuda.Event()
         ev.record(stream)
         events[k] = ev

@@ -58,6 +58,23 @@ def test_workspace_bytes():
 
 
 
+def test_f16_entry_points_check_alignment():
+    lib = som.load()
+    odd = ctypes.c_void_p((1 << 20) + 1)
+    assert lib.som_codebook_norms_f16(None, 10, 10, FAKE, None) == som.SOM_ERR_INVALID_ARG
+    assert lib.som_codebook_norms_f16(odd, 10, 10, FAKE, None) == som.SOM_ERR_INVALID_ARG
+    assert lib.som_bmu_search_f16(odd, FAKE, 100, 64, FAKE, FAKE, 10, 50, FAKE, FAKE, FAKE, 1 << 30, None,
+                                  None) == som.SOM_ERR_INVALID_ARG
+    assert lib.som_bmu_sweep_f16(odd, FAKE, 100, 64, 10, 50, FAKE, 1 << 30, None, None) == som.SOM_ERR_INVALID_ARG
+    assert lib.som_bmu2_sweep_f16(FAKE, FAKE, 100, 64, 10, 50, FAKE, 100, None, None) == som.SOM_ERR_WORKSPACE
+    assert lib.som_bmu2_search_f16(FAKE, FAKE, 100, 64, FAKE, FAKE, 10, 50, FAKE, FAKE, None, FAKE, FAKE, 1 << 30,
+                                   None, None) == som.SOM_ERR_INVALID_ARG
+    # a 2-byte aligned fp16 codebook is fine where fp32 needs 4 bytes
+    two = ctypes.c_void_p((1 << 20) + 2)
+    assert lib.som_bmu_sweep_f16(two, FAKE, 100, 64, 10, 50, FAKE, 100, None, None) == som.SOM_ERR_WORKSPACE
+    assert lib.som_bmu_sweep(two, FAKE, 100, 64, 10, 50, FAKE, 100, None, None) == som.SOM_ERR_INVALID_ARG
+
+
 def test_two_best_workspace_and_checks():
     lib = som.load()
     for tile, keep in ((0, False), (16, False), (32, True)):
