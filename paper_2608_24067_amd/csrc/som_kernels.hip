@@ -620,20 +620,40 @@ __global__ __launch_bounds__(256) void k_sweep(const E *__restrict__ W, const do
         // asm keeps the compiler from turning the branch into unconditional adds
         // and selects.
         auto row_add = [&](unsigned mask, const Seg &seg) {
-            float w[NPL];
+            if constexpr (sizeof(E) == 2 && VEC) {
+                // Packed fp16: each add is one mixed-precision FMA, acc + h * 1.0 with h
+                // read as a half straight from the loaded dword (exact widening, one
+                // rounding: the same result as widening first and adding).
+                const unsigned *dw = reinterpret_cast<const unsigned *>(&seg.v[0]);
 #pragma unroll
-            for (int j = 0; j < NPL; ++j) {
-                if constexpr (VEC)
-                    w[j] = (float)seg.v[j / G][j % G];
-                else
-                    w[j] = (float)seg.e[j];
-            }
+                for (int s = 0; s < TA; ++s) {
+                    if (mask & (1u << s)) {
 #pragma unroll
-            for (int s = 0; s < TA; ++s) {
-                if (mask & (1u << s)) {
+                        for (int d = 0; d < NPL / 2; ++d) {
+                            asm("v_fma_mix_f32 %0, %1, 1.0, %0 op_sel_hi:[1,0,0]" : "+v"(acc[s][2 * d]) : "v"(dw[d]));
+                            asm("v_fma_mix_f32 %0, %1, 1.0, %0 op_sel:[1,0,0] op_sel_hi:[1,0,0]"
+                                : "+v"(acc[s][2 * d + 1])
+                                : "v"(dw[d]));
+                        }
+                        asm volatile("");
+                    }
+                }
+            } else {
+                float w[NPL];
 #pragma unroll
-                    for (int j = 0; j < NPL; ++j) acc[s][j] += w[j];
-                    asm volatile("");
+                for (int j = 0; j < NPL; ++j) {
+                    if constexpr (VEC)
+                        w[j] = (float)seg.v[j / G][j % G];
+                    else
+                        w[j] = (float)seg.e[j];
+                }
+#pragma unroll
+                for (int s = 0; s < TA; ++s) {
+                    if (mask & (1u << s)) {
+#pragma unroll
+                        for (int j = 0; j < NPL; ++j) acc[s][j] += w[j];
+                        asm volatile("");
+                    }
                 }
             }
         };
