@@ -13,13 +13,17 @@ contiguous blocks, each block is evaluated by the single-threaded oracle
 merged with the same rule (smallest distance, then lowest index), so the
 merged answer equals one oracle call over the whole map.
 
+``bmu_sf`` ranks the same way for sparse real-valued rows (a value with each
+feature id; the Discussion's gather-multiply variant).
+
 ``bmu2`` returns the two best units per sample in the order (distance,
 index) -- the pair the paper's fused sweep produces (Figure 2 caption), which
 defines the topographic error -- plus the third distance, for margin checks.
 
 Parity status: pinned (see tests/test_oracle_pins.py) by exact integer
 arithmetic on quantised codebooks (ranks 1-3 by a pure-Python sort for the
-two-best oracle), scipy's cdist on both layouts, the expanded form of Eq. (1),
+two-best oracle, and the same for real-valued rows), all-ones values
+reducing to the binary oracle, exact scaling, scipy's cdist on both layouts, the expanded form of Eq. (1),
 planted, tied and constant codebooks, and a mutation check that each
 plausible slip in oracle.c fails a pin.
 """
@@ -60,6 +64,8 @@ def load(path: str | None = None):
     lib.som_bmu_oracle_host.restype = ctypes.c_int
     lib.som_bmu2_oracle_host.argtypes = [vp, i64, i64, i64, i64, vp, vp, i64, vp, vp, vp, vp, vp]
     lib.som_bmu2_oracle_host.restype = ctypes.c_int
+    lib.som_bmu_sf_oracle_host.argtypes = [vp, i64, i64, i64, i64, vp, vp, vp, i64, vp, vp, vp, vp, vp]
+    lib.som_bmu_sf_oracle_host.restype = ctypes.c_int
     lib.som_norms_oracle_host.argtypes = [vp, i64, i64, i64, i64, vp]
     lib.som_norms_oracle_host.restype = ctypes.c_int
     return lib
@@ -126,6 +132,57 @@ def bmu2(W: np.ndarray, row_ptr: np.ndarray, col_idx: np.ndarray, i0: int = 0, l
     if rc != OK:
         raise ValueError(f"som_bmu2_oracle_host returned {rc}")
     return b1, d1, b2, d2, d3
+
+
+def bmu_sf(W: np.ndarray, row_ptr: np.ndarray, col_idx: np.ndarray, values: np.ndarray, i0: int = 0, lib=None):
+    """bmu2() for sparse real-valued rows: values[p] is the value of feature col_idx[p].
+
+    Returns (bmu, dist, bmu2, dist2, dist3) as bmu2().
+    """
+    ldw = _block_view(W)
+    V, B = W.shape
+    row_ptr = np.ascontiguousarray(row_ptr, dtype=np.int32)
+    col_idx = np.ascontiguousarray(col_idx, dtype=np.int32)
+    values = np.ascontiguousarray(values, dtype=np.float32)
+    if values.shape != col_idx.shape:
+        raise ValueError("values must match col_idx")
+    N = row_ptr.shape[0] - 1
+    b1 = np.empty(N, dtype=np.int32)
+    d1 = np.empty(N, dtype=np.float64)
+    b2 = np.empty(N, dtype=np.int32)
+    d2 = np.empty(N, dtype=np.float64)
+    d3 = np.empty(N, dtype=np.float64)
+    rc = _lib(lib).som_bmu_sf_oracle_host(W.ctypes.data, ldw, V, i0, i0 + B, row_ptr.ctypes.data,
+                                          col_idx.ctypes.data if col_idx.size else None,
+                                          values.ctypes.data if values.size else None, N, b1.ctypes.data,
+                                          d1.ctypes.data, b2.ctypes.data, d2.ctypes.data, d3.ctypes.data)
+    if rc != OK:
+        raise ValueError(f"som_bmu_sf_oracle_host returned {rc}")
+    return b1, d1, b2, d2, d3
+
+
+def bmu_sf_streamed(block_fn: Callable[[int, int], np.ndarray], M: int, row_ptr: np.ndarray, col_idx: np.ndarray,
+                    values: np.ndarray, block: int = 4096, nthreads: int = 1, lib=None):
+    """bmu_sf() over a whole map whose codebook is produced block by block (see bmu_streamed)."""
+    starts = list(range(0, M, block))
+
+    def run(i0):
+        i1 = min(M, i0 + block)
+        return bmu_sf(block_fn(i0, i1), row_ptr, col_idx, values, i0=i0, lib=lib)
+
+    if nthreads <= 1:
+        parts = [run(i0) for i0 in starts]
+    else:
+        with ThreadPoolExecutor(max_workers=nthreads) as ex:
+            parts = list(ex.map(run, starts))
+    return merge_blocks2(parts)
+
+
+def distance_sf_at(column: np.ndarray, ids: np.ndarray, vals: np.ndarray) -> float:
+    """D for one neuron and one real-valued row."""
+    col = np.ascontiguousarray(column, dtype=np.float32).reshape(-1, 1)
+    rp = np.array([0, len(ids)], dtype=np.int32)
+    return float(bmu_sf(col, rp, np.asarray(ids, dtype=np.int32), np.asarray(vals, dtype=np.float32))[1][0])
 
 
 def norms(W: np.ndarray, lib=None) -> np.ndarray:

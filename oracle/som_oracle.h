@@ -64,6 +64,17 @@ int som_bmu2_oracle_host(const float *W, int64_t ldw, int64_t V, int64_t i0, int
                          double *dist3);
 
 /*
+ * Sparse real-valued inputs (Discussion: the gather-multiply variant, a values
+ * array beside the feature ids): x_v = values[p] for the id col_idx[p] of the
+ * row, 0 elsewhere, and D_i = sum_v (x_v - w_{v,i})^2 in fp64, v ascending.
+ * Ranks and outputs as som_bmu2_oracle_host. values: host float[nnz], indexed
+ * like col_idx.
+ */
+int som_bmu_sf_oracle_host(const float *W, int64_t ldw, int64_t V, int64_t i0, int64_t i1, const int32_t *row_ptr,
+                           const int32_t *col_idx, const float *values, int64_t N, int32_t *bmu, double *dist,
+                           int32_t *bmu2, double *dist2, double *dist3);
+
+/*
  * Per-neuron squared norms n_i = sum_v w_{v,i}^2 in fp64, v ascending, for
  * i in [i0, i1): norms[i - i0]. Same W layout as above.
  */

@@ -55,6 +55,8 @@ def _load():
         lib.synth_csr_row_ptr.restype = ctypes.c_int64
         lib.synth_csr_col_idx.argtypes = [u64, i64, i64, ctypes.c_double, ctypes.c_double, i32p, i32p, ctypes.c_int]
         lib.synth_csr_col_idx.restype = ctypes.c_int
+        lib.synth_values.argtypes = [u64, ctypes.c_int, i64, f32p, ctypes.c_int]
+        lib.synth_values.restype = ctypes.c_int
         lib.synth_tile_distinct.argtypes = [i32p, i32p, i64, i64, i32p, ctypes.c_int]
         lib.synth_tile_distinct.restype = ctypes.c_int
         _lib = lib
@@ -131,6 +133,19 @@ def codebook(seed: int, kind: int, V: int, M: int, v0: int = 0, v1: int | None =
     rc = lib.synth_codebook(seed, kind, V, M, v0, v1, i0, i1, _ptr(out), ld, nthreads or default_threads())
     if rc != 0:
         raise ValueError(f"synth_codebook failed ({rc})")
+    return out
+
+
+VAL_UNIFORM = 0    # (h+1) * 2^-24, in (0, 1]
+VAL_QUANTISED = 1  # (k+1) / 256, in [1/256, 1]
+
+
+def values(seed: int, n: int, kind: int = VAL_UNIFORM, nthreads: int | None = None) -> np.ndarray:
+    """Values for the first n CSR positions of a sparse real-valued batch (float32, all positive)."""
+    out = np.empty(max(n, 1), dtype=np.float32)[:n]
+    rc = _load().synth_values(seed, kind, n, _ptr(out) if n else None, nthreads or default_threads())
+    if rc != 0:
+        raise ValueError("synth_values failed")
     return out
 
 

@@ -39,6 +39,7 @@ static inline uint64_t mix64(uint64_t z)
  * from the same seed are unrelated. */
 static inline uint64_t csr_base(uint64_t seed) { return mix64(seed ^ 0xA0761D6478BD642FULL); }
 static inline uint64_t cb_base(uint64_t seed) { return mix64(seed ^ 0xE7037ED1A0B428DBULL); }
+static inline uint64_t val_base(uint64_t seed) { return mix64(seed ^ 0x8EBC6AF09C88C6E3ULL); }
 
 /* ------------------------------------------------------------------ threads */
 
@@ -395,5 +396,31 @@ int synth_tile_distinct(const int32_t *row_ptr, const int32_t *col_idx, int64_t 
     if (!row_ptr || !out || N < 0 || TA < 1) return -1;
     tile_ctx c = {row_ptr, col_idx, N, TA, out};
     parallel_for((N + TA - 1) / TA, 1024, nthreads, tile_rows, &c);
+    return 0;
+}
+
+/* ------------------------------------------------------------------ values */
+
+typedef struct {
+    uint64_t base;
+    int kind;
+    float *out;
+} val_ctx;
+
+static void val_range(int64_t b, int64_t e, void *p)
+{
+    const val_ctx *c = (const val_ctx *)p;
+    for (int64_t q = b; q < e; ++q) {
+        const uint64_t h = mix64(c->base + ((uint64_t)q + 1) * GOLDEN);
+        c->out[q] = c->kind == SYNTH_VAL_QUANTISED ? (float)((h >> 56) + 1) * (1.0f / 256.0f)
+                                                   : (float)((h >> 40) + 1) * 0x1p-24f;
+    }
+}
+
+int synth_values(uint64_t seed, int kind, int64_t n, float *out, int nthreads)
+{
+    if (n < 0 || (n > 0 && !out) || (kind != SYNTH_VAL_UNIFORM && kind != SYNTH_VAL_QUANTISED)) return -1;
+    val_ctx c = {val_base(seed), kind, out};
+    parallel_for(n, 4096, nthreads, val_range, &c);
     return 0;
 }

@@ -37,6 +37,14 @@ int64_t synth_csr_row_ptr(uint64_t seed, int64_t N, int64_t V, double lam, int32
 int synth_csr_col_idx(uint64_t seed, int64_t N, int64_t V, double lam, double zipf_s, const int32_t *row_ptr,
                       int32_t *col_idx, int nthreads);
 
+/* Values of a sparse real-valued batch: out[q] for the ids at CSR positions
+ * q = 0 .. n-1, each a pure function of (seed, q).
+ *   SYNTH_VAL_UNIFORM    (h+1) * 2^-24 with 24 random bits h: in (0, 1]
+ *   SYNTH_VAL_QUANTISED  (k+1) / 256 with k uniform on {0..255}: in [1/256, 1]
+ * Returns 0, or -1 on bad arguments. */
+enum { SYNTH_VAL_UNIFORM = 0, SYNTH_VAL_QUANTISED = 1 };
+int synth_values(uint64_t seed, int kind, int64_t n, float *out, int nthreads);
+
 /* Number of distinct feature ids in each group of TA consecutive rows
  * (the last group may be short): out has ceil(N/TA) entries. */
 int synth_tile_distinct(const int32_t *row_ptr, const int32_t *col_idx, int64_t N, int64_t TA, int32_t *out,

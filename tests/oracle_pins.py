@@ -300,6 +300,78 @@ def check_top2_blocks(lib):
         assert np.array_equal(a, b)
 
 
+# ----------------------------------------------- sparse real-valued inputs
+
+def sf_case(seed, N, V, M, kind=synth.QUANTISED, vkind=synth.VAL_QUANTISED):
+    rp, ci = synth.make_csr(seed, N, V)
+    W = synth.codebook(seed, kind, V, M)
+    vals = synth.values(seed, len(ci), vkind)
+    return rp, ci, vals, W
+
+
+def dense_values(row_ptr, col_idx, vals, V):
+    N = row_ptr.shape[0] - 1
+    X = np.zeros((N, V), dtype=np.float64)
+    for s in range(N):
+        X[s, col_idx[row_ptr[s]:row_ptr[s + 1]]] = vals[row_ptr[s]:row_ptr[s + 1]]
+    return X
+
+
+def check_sf_exact_integer(lib):
+    """k/256 codebook and (j+1)/256 values: 65536*D_i = sum_v (256 x_v - k_{v,i})^2 in int64; ranks by a Python sort."""
+    rp, ci, vals, W = sf_case(26, 50, 220, 31)
+    K = np.rint(W * 256).astype(np.int64)
+    X256 = np.rint(dense_values(rp, ci, vals, W.shape[0]) * 256).astype(np.int64)
+    Dint = ((X256[:, :, None] - K[None, :, :]) ** 2).sum(axis=1)
+    b1, d1, b2, d2, d3 = oracle.bmu_sf(W, rp, ci, vals, lib=lib)
+    for s in range(len(b1)):
+        r = exact_ranks(Dint[s])
+        assert (int(b1[s]), int(b2[s])) == (r[0], r[1]), f"sample {s}: ranks differ"
+        assert (d1[s] * 65536.0, d2[s] * 65536.0, d3[s] * 65536.0) == tuple(float(Dint[s, i]) for i in r[:3])
+
+
+def check_sf_binary_values_reduce(lib):
+    """All values 1: the real-valued oracle returns exactly the binary two-best oracle's answer."""
+    rp, ci, _, W = sf_case(27, 40, 300, 45, kind=synth.UNIFORM)
+    ones = np.ones(len(ci), dtype=np.float32)
+    for a, b in zip(oracle.bmu_sf(W, rp, ci, ones, lib=lib), oracle.bmu2(W, rp, ci, lib=lib)):
+        assert np.array_equal(a, b)
+
+
+def check_sf_cdist_and_planted(lib):
+    """Continuous values: scipy cdist sorted agrees; a prototype equal to the input has distance 0, one
+    whose value for the first feature is halved has distance (x/2)^2 exactly; three tied copies rank by
+    index; doubling x and W scales every distance by exactly 4."""
+    rp, ci, vals, W = sf_case(28, 36, 240, 40, kind=synth.UNIFORM, vkind=synth.VAL_UNIFORM)
+    X = dense_values(rp, ci, vals, W.shape[0])
+    D = cdist(X, np.ascontiguousarray(W.T).astype(np.float64), "sqeuclidean")
+    b1, d1, b2, d2, d3 = oracle.bmu_sf(W, rp, ci, vals, lib=lib)
+    order = np.argsort(D, axis=1, kind="stable")
+    assert np.array_equal(b1, order[:, 0]) and np.array_equal(b2, order[:, 1])
+    srt = np.sort(D, axis=1)
+    for got, k in ((d1, 0), (d2, 1), (d3, 2)):
+        assert np.allclose(got, srt[:, k], rtol=1e-12, atol=0)
+    s = 7
+    ids, xv = ci[rp[s]:rp[s + 1]], vals[rp[s]:rp[s + 1]]
+    Wp = W.copy()
+    Wp[:, 13] = 0.0
+    Wp[ids, 13] = xv
+    Wp[:, 2] = Wp[:, 13]
+    Wp[ids[0], 2] = xv[0] / 2
+    r = oracle.bmu_sf(Wp, rp[s:s + 2], ci, vals, lib=lib)
+    assert (int(r[0][0]), float(r[1][0]), int(r[2][0])) == (13, 0.0, 2)
+    assert float(r[3][0]) == (float(xv[0]) / 2) ** 2
+    Wt = W.copy()
+    for j in (9, 2, 5):  # three exact copies of the input: ranks 2 then 5, all at distance 0
+        Wt[:, j] = 0.0
+        Wt[ids, j] = xv
+    r = oracle.bmu_sf(Wt, rp[s:s + 2], ci, vals, lib=lib)
+    assert (int(r[0][0]), int(r[2][0]), float(r[1][0]), float(r[3][0]), float(r[4][0])) == (2, 5, 0.0, 0.0, 0.0)
+    r2 = oracle.bmu_sf(np.ascontiguousarray(2 * W), rp, ci, 2 * vals, lib=lib)
+    assert np.array_equal(r2[0], b1) and np.array_equal(r2[2], b2)
+    assert np.array_equal(r2[1], 4 * d1) and np.array_equal(r2[3], 4 * d2)
+
+
 ALL_CHECKS = [
     check_exact_integer_direct,
     check_cdist_node_major,
@@ -317,4 +389,7 @@ ALL_CHECKS = [
     check_top2_ties_and_small_maps,
     check_top2_cdist_and_top1,
     check_top2_blocks,
+    check_sf_exact_integer,
+    check_sf_binary_values_reduce,
+    check_sf_cdist_and_planted,
 ]

@@ -27,23 +27,27 @@ def test_exact_integer_full_tiny_workload():
 
 
 MUTANTS = [
-    ("sign", "const double diff = xv - (double)wrow[k];", "const double diff = xv + (double)wrow[k];"),
+    ("sign", "const double diff = x[v] - (double)wrow[k];", "const double diff = x[v] + (double)wrow[k];"),
     ("dropped_square", "D[k] += diff * diff;", "D[k] += diff;"),
-    ("input_ignored", "        x[v] = 1;\n", "        (void)v;\n"),
+    ("input_ignored", "        x[v] = 1.0;\n", "        (void)v;\n"),
     ("transposed_stride", "const float *wrow = W + v * ldw;\n        for (int64_t k = 0; k < B; ++k) {\n            const double diff",
      "const float *wrow = W + v;\n        for (int64_t k = 0; k < B; ++k) {\n            const double diff"),
     ("tie_highest_index", "if (D[k] < D[best]) best = k;", "if (D[k] <= D[best]) best = k;"),
     ("block_offset_lost", "bmu[s] = (int32_t)(i0 + best);", "bmu[s] = (int32_t)best;"),
     ("second_best_includes_best", "if (k != best && D[k] < second)", "if (D[k] < second)"),
-    ("last_feature_dropped", "for (int64_t v = 0; v < V; ++v) {\n        const double xv",
-     "for (int64_t v = 0; v < V - 1; ++v) {\n        const double xv"),
+    ("last_feature_dropped",
+     "for (int64_t v = 0; v < V; ++v) {\n        const float *wrow = W + v * ldw;\n        for (int64_t k = 0; k < B; ++k) {\n            const double diff",
+     "for (int64_t v = 0; v < V - 1; ++v) {\n        const float *wrow = W + v * ldw;\n        for (int64_t k = 0; k < B; ++k) {\n            const double diff"),
     ("norm_not_squared", "norms[k] += w * w;", "norms[k] += w;"),
-    ("x_off_by_one", "x[v] = 1;", "x[v < V - 1 ? v + 1 : v] = 1;"),
+    ("x_off_by_one", "x[v] = 1.0;", "x[v < V - 1 ? v + 1 : v] = 1.0;"),
     ("rank2_tie_highest_index", "} else if (r2 < 0 || D[k] < D[r2]) {", "} else if (r2 < 0 || D[k] <= D[r2]) {"),
     ("rank2_not_demoted", "                r3 = r2;\n                r2 = r1;\n                r1 = k;",
      "                r3 = r2;\n                r1 = k;"),
     ("rank2_block_offset_lost", "bmu2[s] = r2 < 0 ? -1 : (int32_t)(i0 + r2);", "bmu2[s] = r2 < 0 ? -1 : (int32_t)r2;"),
     ("rank3_ignored", "} else if (r3 < 0 || D[k] < D[r3]) {", "} else if (r3 < 0) {"),
+    ("sf_value_ignored", "x[v] = (double)values[p];", "x[v] = 1.0;"),
+    ("sf_value_squared", "x[v] = (double)values[p];", "x[v] = (double)values[p] * (double)values[p];"),
+    ("sf_rank2_tie_highest_index", "} else if (q2 < 0 || D[k] < D[q2]) {", "} else if (q2 < 0 || D[k] <= D[q2]) {"),
 ]
 
 
