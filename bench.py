@@ -115,6 +115,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--dtype", choices=("f32", "f16"), default="f32",
                     help="codebook storage: fp32 (the workloads' own) or fp16 (rounded from it; fp32 accumulation)")
+    ap.add_argument("--values", action="store_true",
+                    help="sparse real-valued rows: a U(0,1] value with every id (the gather-multiply variant)")
     ap.add_argument("--top2", action="store_true",
                     help="time the two-best search (som_bmu2_*) instead of the single-best one")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -163,7 +165,11 @@ def main():
     norms = torch.empty(M, dtype=torch.float64, device=dev)
     bmu = torch.empty(N, dtype=torch.int32, device=dev)
     dist = torch.empty(N, dtype=torch.float64, device=dev)
-    alloc = som.alloc_workspace2 if args.top2 else som.alloc_workspace
+    if args.values:
+        vals_d = torch.from_numpy(synth.values(cfg.seed, nnz)).to(dev)
+        alloc = som.alloc_workspace_sf
+    else:
+        alloc = som.alloc_workspace2 if args.top2 else som.alloc_workspace
     ws = alloc(N, M, V, nnz, dev, tile_samples=args.tile)
     if args.top2:
         out2 = (bmu, dist, torch.empty(N, dtype=torch.int32, device=dev), torch.empty(N, dtype=torch.float64, device=dev))
@@ -188,16 +194,23 @@ def main():
         som.codebook_norms(W, V, M, out=norms)
         if ev is not None:
             ev[1].record()
-        som.bmu_plan(rp, ci, V, M, nnz, ws, tile_samples=args.tile)
+        if args.values:
+            som.bmu_sf_plan(rp, ci, vals_d, V, M, nnz, ws, tile_samples=args.tile)
+        else:
+            som.bmu_plan(rp, ci, V, M, nnz, ws, tile_samples=args.tile)
         if ev is not None:
             ev[2].record()
-        if args.top2:
+        if args.values:
+            som.bmu_sf_sweep(W, norms, V, M, N, nnz, ws, two_best=args.top2, tile_samples=args.tile)
+        elif args.top2:
             som.bmu2_sweep(W, norms, V, M, N, nnz, ws, tile_samples=args.tile)
         else:
             som.bmu_sweep(W, norms, V, M, N, nnz, ws, tile_samples=args.tile)
         if ev is not None:
             ev[3].record()
-        if args.top2:
+        if args.values:
+            som.bmu_sf_finalize(norms, rp, V, M, nnz, out2 if args.top2 else (bmu, dist), ws, tile_samples=args.tile)
+        elif args.top2:
             som.bmu2_finalize(norms, rp, V, M, nnz, out2, ws, tile_samples=args.tile)
         else:
             som.bmu_finalize(norms, rp, V, M, nnz, bmu, dist, ws, tile_samples=args.tile)
@@ -227,7 +240,7 @@ def main():
     sweep_s = phase_ms["sweep"] / 1e3
     achieved = alg_bytes / sweep_s / 1e9
     workload = cfg.describe()
-    traffic = None if (args.top2 or args.dtype != "f32") else measured_traffic(args.config)
+    traffic = None if (args.top2 or args.values or args.dtype != "f32") else measured_traffic(args.config)
 
     out = {
         "metric": METRIC,
@@ -245,13 +258,14 @@ def main():
         "config": {"workload": workload, "map": f"{cfg.edge}x{cfg.edge}", "M": M, "V": V, "N": N, "nnz": nnz,
                    "tile_samples": args.tile or som.DEFAULT_TILE_SAMPLES,
                    "keep_order": False, "alg_tile_samples": ALG_TILE, "parallelism": "single GPU",
-                   "search": "two best units" if args.top2 else "best unit", "codebook": args.dtype},
+                   "search": "two best units" if args.top2 else "best unit", "codebook": args.dtype,
+                   "rows": "real-valued" if args.values else "binary"},
         "effective_codebook_GBps": eff_gbps,
         "effective_pct_of_hbm_peak": 100.0 * eff_gbps / HBM_PEAK_GBPS,
         "effective_codebook_bytes_per_step": alg_bytes,
         "event_ms_per_step": step_ms,
         "phase_ms": phase_ms,
-        "roofline": {"bound": "hbm", "kernel": "k_sweep (two-best)" if args.top2 else "k_sweep", "achieved": achieved, "peak": HBM_PEAK_GBPS,
+        "roofline": {"bound": "hbm", "kernel": "k_sweep" + (" (real values)" if args.values else "") + (" (two-best)" if args.top2 else ""), "achieved": achieved, "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBPS,
                      "traffic": traffic},
     }

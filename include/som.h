@@ -242,6 +242,55 @@ som_status som_bmu2_sweep_f16(const uint16_t *W, const double *norms, int64_t V,
                               void *workspace, size_t workspace_bytes, const som_bmu_config *config, void *stream);
 
 /*
+ * Sparse real-valued rows (the Discussion's gather-multiply variant: a values
+ * array beside the feature ids, and ||x||^2). values: device float [nnz],
+ * indexed like col_idx (values[p] belongs to feature col_idx[p]), finite.
+ * The BMU of x is argmin_i ||x - w_i||^2 with x_v the given values; the sweep
+ * accumulates x_v * W[v*M+i] with one fp32 fused multiply-add per term in
+ * ascending feature order, and dist = (||w||^2 - 2*dot) + ||x||^2 with
+ * ||x||^2 the fp64 sum of the squared values in row order.
+ *   bmu2, dist2  both NULL: the best unit only; both non-NULL: the two best,
+ *                as som_bmu2_search.
+ * Tiles of 8 samples only (tile_samples 0 or 8; other values are rejected).
+ * The workspace (som_bmu_sf_workspace_bytes) adds 32 bytes per id for the
+ * plan's per-entry values and 8 per sample for ||x||^2 to the two-best one.
+ * With all values 1 the results equal the binary search's bit for bit.
+ */
+size_t som_bmu_sf_workspace_bytes(int64_t N, int64_t M, int64_t V, int64_t nnz, const som_bmu_config *config);
+
+som_status som_bmu_sf_search(const float *W, const double *norms, int64_t V, int64_t M, const int32_t *row_ptr,
+                             const int32_t *col_idx, const float *values, int64_t N, int64_t nnz, int32_t *bmu,
+                             double *dist, int32_t *bmu2, double *dist2, void *workspace, size_t workspace_bytes,
+                             const som_bmu_config *config, void *stream);
+
+som_status som_bmu_sf_search_f16(const uint16_t *W, const double *norms, int64_t V, int64_t M, const int32_t *row_ptr,
+                                 const int32_t *col_idx, const float *values, int64_t N, int64_t nnz, int32_t *bmu,
+                                 double *dist, int32_t *bmu2, double *dist2, void *workspace, size_t workspace_bytes,
+                                 const som_bmu_config *config, void *stream);
+
+/*
+ * Phases of som_bmu_sf_search, in this order on one stream and workspace:
+ *   som_bmu_sf_plan -- the plan with each entry's sample values and ||x||^2;
+ *   som_bmu_sf_sweep(_f16) -- the sweep; two_best != 0 keeps the two best;
+ *   som_bmu_sf_finalize -- as above (bmu2/dist2 non-NULL after a two-best sweep).
+ */
+som_status som_bmu_sf_plan(const int32_t *row_ptr, const int32_t *col_idx, const float *values, int64_t N,
+                           int64_t nnz, int64_t V, int64_t M, void *workspace, size_t workspace_bytes,
+                           const som_bmu_config *config, void *stream);
+
+som_status som_bmu_sf_sweep(const float *W, const double *norms, int64_t V, int64_t M, int64_t N, int64_t nnz,
+                            int32_t two_best, void *workspace, size_t workspace_bytes, const som_bmu_config *config,
+                            void *stream);
+
+som_status som_bmu_sf_sweep_f16(const uint16_t *W, const double *norms, int64_t V, int64_t M, int64_t N, int64_t nnz,
+                                int32_t two_best, void *workspace, size_t workspace_bytes,
+                                const som_bmu_config *config, void *stream);
+
+som_status som_bmu_sf_finalize(const double *norms, int64_t V, int64_t M, const int32_t *row_ptr, int64_t N,
+                               int64_t nnz, int32_t *bmu, double *dist, int32_t *bmu2, double *dist2, void *workspace,
+                               size_t workspace_bytes, const som_bmu_config *config, void *stream);
+
+/*
  * Input flags (SOM_FLAG_*) the last plan on this workspace recorded. Waits
  * for `stream`, then copies one word to *flags (host). 0 means the device
  * saw a valid CSR.

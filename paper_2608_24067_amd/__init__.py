@@ -8,10 +8,15 @@ from .som import (  # noqa: F401
     SomError,
     alloc_workspace,
     alloc_workspace2,
+    alloc_workspace_sf,
     bmu2_finalize,
     bmu2_search,
     bmu2_sweep,
     bmu_finalize,
+    bmu_sf_finalize,
+    bmu_sf_plan,
+    bmu_sf_search,
+    bmu_sf_sweep,
     bmu_plan,
     bmu_search,
     bmu_sweep,
@@ -22,5 +27,6 @@ from .som import (  # noqa: F401
     load,
     validate_csr_host,
     workspace2_bytes,
+    workspace_sf_bytes,
     workspace_bytes,
 )

@@ -69,32 +69,45 @@ som_status check_dims(int64_t N, int64_t M, int64_t V, int64_t nnz)
     return SOM_OK;
 }
 
+bool dims_ok(int64_t N, int64_t M, int64_t V, int64_t nnz)
+{
+    return !(N < 0 || N >= INT32_MAX || M < 1 || M > SOM_MAX_NEURONS || V < 1 || V >= INT32_MAX || nnz < 0 ||
+             nnz > INT32_MAX);
+}
+
+// Which workspace layout a call works on. Binary rows: single-best, or two-best (a
+// superset). Real-valued rows: always the two-best layout plus the value sections.
+struct Kind {
+    bool top2;  // produce the two best units
+    bool real;  // real-valued rows
+    bool layout_top2() const { return top2 || real; }
+};
+
 struct Carved {
     uint2 *plan;
     int2 *tiles;
-    unsigned long long *keys;
-    float *dots;
-    unsigned long long *keys2;  // two-best search only
-    float *dots2;
+    som::SweepOut out;
     uint32_t *flags;
     som::OrderBuffers ob;
+    float *vals;
+    double *xsq;
 };
 
-som_status carve(void *ws, size_t bytes, int64_t N, int64_t M, int64_t V, int64_t nnz, const Opts &o, Carved *c,
-                 bool top2 = false)
+som_status carve(void *ws, size_t bytes, int64_t N, int64_t M, int64_t V, int64_t nnz, const Opts &o, const Kind &k,
+                 Carved *c)
 {
     if (!ws) return fail(SOM_ERR_WORKSPACE, "workspace is NULL");
     if (reinterpret_cast<uintptr_t>(ws) & 255) return fail(SOM_ERR_WORKSPACE, "workspace must be 256-byte aligned");
-    const som::Layout L = som::layout_for(N, M, V, nnz, o.ta, o.order, top2);
+    const som::Layout L = som::layout_for(N, M, V, nnz, o.ta, o.order, k.layout_top2(), k.real);
     if (bytes < L.total)
         return fail(SOM_ERR_WORKSPACE, "workspace holds %zu bytes, the search needs %zu", bytes, L.total);
     char *b = static_cast<char *>(ws);
     c->plan = reinterpret_cast<uint2 *>(b + L.plan);
     c->tiles = reinterpret_cast<int2 *>(b + L.tiles);
-    c->keys = reinterpret_cast<unsigned long long *>(b + L.keys);
-    c->dots = reinterpret_cast<float *>(b + L.dots);
-    c->keys2 = reinterpret_cast<unsigned long long *>(b + L.keys2);
-    c->dots2 = reinterpret_cast<float *>(b + L.dots2);
+    c->out.keys = reinterpret_cast<unsigned long long *>(b + L.keys);
+    c->out.dots = reinterpret_cast<float *>(b + L.dots);
+    c->out.keys2 = k.layout_top2() ? reinterpret_cast<unsigned long long *>(b + L.keys2) : nullptr;
+    c->out.dots2 = k.layout_top2() ? reinterpret_cast<float *>(b + L.dots2) : nullptr;
     c->flags = reinterpret_cast<uint32_t *>(b + L.flags);
     c->ob.freq = reinterpret_cast<uint32_t *>(b + L.freq);
     c->ob.bucket = reinterpret_cast<unsigned long long *>(b + L.bucket);
@@ -102,24 +115,32 @@ som_status carve(void *ws, size_t bytes, int64_t N, int64_t M, int64_t V, int64_
     c->ob.perm = reinterpret_cast<int32_t *>(b + L.perm);
     c->ob.prp = reinterpret_cast<int32_t *>(b + L.prp);
     c->ob.pci = reinterpret_cast<int32_t *>(b + L.pci);
+    c->ob.pvals = k.real ? reinterpret_cast<float *>(b + L.pvals) : nullptr;
+    c->vals = k.real ? reinterpret_cast<float *>(b + L.vals) : nullptr;
+    c->xsq = k.real ? reinterpret_cast<double *>(b + L.xsq) : nullptr;
     return SOM_OK;
 }
 
 // Common prologue of the phases: options, N == 0 (a no-op), workspace.
 som_status setup(int64_t N, int64_t M, int64_t V, int64_t nnz, const som_bmu_config *config, void *workspace,
-                 size_t workspace_bytes, Opts *o, Carved *c, bool *noop, bool top2 = false)
+                 size_t workspace_bytes, const Kind &k, Opts *o, Carved *c, bool *noop)
 {
     som_status st = parse(config, o);
     if (st != SOM_OK) return st;
+    if (k.real && o->ta != 8)
+        return fail(SOM_ERR_INVALID_ARG, "real-valued rows use tiles of 8 samples (tile_samples 0 or 8)");
     *noop = N == 0;
     if (*noop) return SOM_OK;
-    return carve(workspace, workspace_bytes, N, M, V, nnz, *o, c, top2);
+    return carve(workspace, workspace_bytes, N, M, V, nnz, *o, k, c);
 }
 
-bool dims_ok(int64_t N, int64_t M, int64_t V, int64_t nnz)
+size_t workspace_for(int64_t N, int64_t M, int64_t V, int64_t nnz, const som_bmu_config *config, const Kind &k)
 {
-    return !(N < 0 || N >= INT32_MAX || M < 1 || M > SOM_MAX_NEURONS || V < 1 || V >= INT32_MAX || nnz < 0 ||
-             nnz > INT32_MAX);
+    if (!dims_ok(N, M, V, nnz)) return 0;
+    Opts o;
+    if (parse(config, &o) != SOM_OK) return 0;
+    if (k.real && o.ta != 8) return 0;
+    return som::layout_for(N, M, V, nnz, o.ta, o.order, k.layout_top2(), k.real).total;
 }
 
 // A codebook: fp32, or IEEE binary16 bit patterns.
@@ -149,7 +170,37 @@ som_status norms_impl(const Book &b, int64_t V, int64_t M, double *norms, void *
     return ok();
 }
 
-som_status sweep_impl(const Book &b, bool top2, const double *norms, int64_t V, int64_t M, int64_t N, int64_t nnz,
+som_status plan_impl(const int32_t *row_ptr, const int32_t *col_idx, const float *values, int64_t N, int64_t nnz,
+                     int64_t V, int64_t M, void *workspace, size_t workspace_bytes, const som_bmu_config *config,
+                     void *stream, const Kind &k, const char *who)
+{
+    Opts o;
+    Carved c;
+    bool noop;
+    som_status st = check_dims(N, M, V, nnz);
+    if (st != SOM_OK) return st;
+    if (N > 0 && (!row_ptr || (nnz > 0 && (!col_idx || (k.real && !values)))))
+        return fail(SOM_ERR_INVALID_ARG, "%s: null CSR pointer", who);
+    if ((st = setup(N, M, V, nnz, config, workspace, workspace_bytes, k, &o, &c, &noop)) != SOM_OK) return st;
+    if (noop) return ok();
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipError_t e = som::launch_clear_flags(c.flags, s);
+    if (e != hipSuccess) return hip_fail(e, who);
+    const int32_t *rp = row_ptr, *ci = col_idx;
+    const float *vs = k.real ? values : nullptr;
+    if (o.order) {
+        e = som::launch_order(row_ptr, col_idx, vs, N, nnz, V, c.ob, c.flags, s);
+        if (e != hipSuccess) return hip_fail(e, who);
+        rp = c.ob.prp;
+        ci = c.ob.pci;
+        if (vs) vs = c.ob.pvals;
+    }
+    e = som::launch_plan(o.ta, rp, ci, vs, N, nnz, V, c.plan, c.tiles, c.vals, c.xsq, c.flags, s);
+    if (e != hipSuccess) return hip_fail(e, who);
+    return ok();
+}
+
+som_status sweep_impl(const Book &b, const Kind &k, const double *norms, int64_t V, int64_t M, int64_t N, int64_t nnz,
                       void *workspace, size_t workspace_bytes, const som_bmu_config *config, void *stream,
                       const char *who)
 {
@@ -160,51 +211,66 @@ som_status sweep_impl(const Book &b, bool top2, const double *norms, int64_t V, 
     if (st != SOM_OK) return st;
     if (N > 0 && (!b.p || !norms)) return fail(SOM_ERR_INVALID_ARG, "%s: null pointer", who);
     if ((st = check_book(b, who)) != SOM_OK) return st;
-    if ((st = setup(N, M, V, nnz, config, workspace, workspace_bytes, &o, &c, &noop, top2)) != SOM_OK) return st;
+    if ((st = setup(N, M, V, nnz, config, workspace, workspace_bytes, k, &o, &c, &noop)) != SOM_OK) return st;
     if (noop) return ok();
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    hipError_t e;
-    if (b.f16) {
-        const uint16_t *W = static_cast<const uint16_t *>(b.p);
-        e = top2 ? som::launch_sweep2_f16(o.ta, W, norms, M, N, V, nnz, c.plan, c.tiles, c.keys, c.dots, c.keys2,
-                                          c.dots2, s)
-                 : som::launch_sweep_f16(o.ta, W, norms, M, N, V, nnz, c.plan, c.tiles, c.keys, c.dots, s);
-    } else {
-        const float *W = static_cast<const float *>(b.p);
-        e = top2 ? som::launch_sweep2(o.ta, W, norms, M, N, V, nnz, c.plan, c.tiles, c.keys, c.dots, c.keys2, c.dots2,
-                                      s)
-                 : som::launch_sweep(o.ta, W, norms, M, N, V, nnz, c.plan, c.tiles, c.keys, c.dots, s);
-    }
+    som::SweepOut out = c.out;
+    if (!k.top2) out.keys2 = nullptr, out.dots2 = nullptr;
+    hipError_t e = som::launch_sweep(o.ta, b.f16, k.top2, b.p, norms, M, N, V, nnz, c.plan, c.tiles, c.vals, out,
+                                     static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, who);
     return ok();
 }
 
-som_status search_impl(const Book &b, const double *norms, int64_t V, int64_t M, const int32_t *row_ptr,
-                       const int32_t *col_idx, int64_t N, int64_t nnz, int32_t *bmu, double *dist, int32_t *bmu2,
-                       double *dist2, void *workspace, size_t workspace_bytes, const som_bmu_config *config,
-                       void *stream, const char *who)
+som_status finalize_impl(const Kind &k, const double *norms, int64_t V, int64_t M, const int32_t *row_ptr, int64_t N,
+                         int64_t nnz, int32_t *bmu, double *dist, int32_t *bmu2, double *dist2, void *workspace,
+                         size_t workspace_bytes, const som_bmu_config *config, void *stream, const char *who)
 {
-    const bool top2 = bmu2 != nullptr || dist2 != nullptr;
     Opts o;
     Carved c;
     bool noop;
     som_status st = check_dims(N, M, V, nnz);
     if (st != SOM_OK) return st;
-    if (N > 0 && (!b.p || !norms || !row_ptr || (nnz > 0 && !col_idx) || !bmu || !dist || (top2 && (!bmu2 || !dist2))))
+    if (N > 0 && (!norms || !row_ptr || !bmu || !dist || (k.top2 && (!bmu2 || !dist2))))
+        return fail(SOM_ERR_INVALID_ARG, "%s: null pointer", who);
+    if ((st = setup(N, M, V, nnz, config, workspace, workspace_bytes, k, &o, &c, &noop)) != SOM_OK) return st;
+    if (noop) return ok();
+    const int32_t *rp = o.order ? c.ob.prp : row_ptr;
+    const int32_t *perm = o.order ? c.ob.perm : nullptr;
+    hipError_t e = som::launch_finalize(o.ta, norms, M, rp, N, nnz, perm, c.xsq, c.out, bmu, dist,
+                                        k.top2 ? bmu2 : nullptr, k.top2 ? dist2 : nullptr,
+                                        static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, who);
+    return ok();
+}
+
+som_status search_impl(const Book &b, const Kind &k, const double *norms, int64_t V, int64_t M, const int32_t *row_ptr,
+                       const int32_t *col_idx, const float *values, int64_t N, int64_t nnz, int32_t *bmu,
+                       double *dist, int32_t *bmu2, double *dist2, void *workspace, size_t workspace_bytes,
+                       const som_bmu_config *config, void *stream, const char *who)
+{
+    Opts o;
+    Carved c;
+    bool noop;
+    som_status st = check_dims(N, M, V, nnz);
+    if (st != SOM_OK) return st;
+    if (N > 0 && (!b.p || !norms || !row_ptr || (nnz > 0 && (!col_idx || (k.real && !values))) || !bmu || !dist ||
+                  (k.top2 && (!bmu2 || !dist2))))
         return fail(SOM_ERR_INVALID_ARG, "%s: null pointer", who);
     if ((st = check_book(b, who)) != SOM_OK) return st;
-    if ((st = setup(N, M, V, nnz, config, workspace, workspace_bytes, &o, &c, &noop, top2)) != SOM_OK) return st;
+    if ((st = setup(N, M, V, nnz, config, workspace, workspace_bytes, k, &o, &c, &noop)) != SOM_OK) return st;
     if (noop) return ok();
-    // the plan phase is shared (a single-best layout is a prefix of the two-best one)
-    if ((st = som_bmu_plan(row_ptr, col_idx, N, nnz, V, M, workspace, workspace_bytes, config, stream)) != SOM_OK)
+    if ((st = plan_impl(row_ptr, col_idx, values, N, nnz, V, M, workspace, workspace_bytes, config, stream, k, who)) !=
+        SOM_OK)
         return st;
-    if ((st = sweep_impl(b, top2, norms, V, M, N, nnz, workspace, workspace_bytes, config, stream, who)) != SOM_OK)
+    if ((st = sweep_impl(b, k, norms, V, M, N, nnz, workspace, workspace_bytes, config, stream, who)) != SOM_OK)
         return st;
-    if (top2)
-        return som_bmu2_finalize(norms, V, M, row_ptr, N, nnz, bmu, dist, bmu2, dist2, workspace, workspace_bytes,
-                                 config, stream);
-    return som_bmu_finalize(norms, V, M, row_ptr, N, nnz, bmu, dist, workspace, workspace_bytes, config, stream);
+    return finalize_impl(k, norms, V, M, row_ptr, N, nnz, bmu, dist, bmu2, dist2, workspace, workspace_bytes, config,
+                         stream, who);
 }
+
+constexpr Kind kOne{false, false}, kTwo{true, false};
+
+Kind real_kind(const int32_t *bmu2, const double *dist2) { return Kind{bmu2 != nullptr || dist2 != nullptr, true}; }
 
 }  // namespace
 
@@ -212,18 +278,17 @@ extern "C" {
 
 size_t som_bmu_workspace_bytes(int64_t N, int64_t M, int64_t V, int64_t nnz, const som_bmu_config *config)
 {
-    if (!dims_ok(N, M, V, nnz)) return 0;
-    Opts o;
-    if (parse(config, &o) != SOM_OK) return 0;
-    return som::layout_for(N, M, V, nnz, o.ta, o.order).total;
+    return workspace_for(N, M, V, nnz, config, kOne);
 }
 
 size_t som_bmu2_workspace_bytes(int64_t N, int64_t M, int64_t V, int64_t nnz, const som_bmu_config *config)
 {
-    if (!dims_ok(N, M, V, nnz)) return 0;
-    Opts o;
-    if (parse(config, &o) != SOM_OK) return 0;
-    return som::layout_for(N, M, V, nnz, o.ta, o.order, true).total;
+    return workspace_for(N, M, V, nnz, config, kTwo);
+}
+
+size_t som_bmu_sf_workspace_bytes(int64_t N, int64_t M, int64_t V, int64_t nnz, const som_bmu_config *config)
+{
+    return workspace_for(N, M, V, nnz, config, Kind{true, true});
 }
 
 som_status som_codebook_norms(const float *W, int64_t V, int64_t M, double *norms, void *stream)
@@ -239,40 +304,21 @@ som_status som_codebook_norms_f16(const uint16_t *W, int64_t V, int64_t M, doubl
 som_status som_bmu_plan(const int32_t *row_ptr, const int32_t *col_idx, int64_t N, int64_t nnz, int64_t V, int64_t M,
                         void *workspace, size_t workspace_bytes, const som_bmu_config *config, void *stream)
 {
-    Opts o;
-    Carved c;
-    bool noop;
-    som_status st = check_dims(N, M, V, nnz);
-    if (st != SOM_OK) return st;
-    if (N > 0 && (!row_ptr || (nnz > 0 && !col_idx))) return fail(SOM_ERR_INVALID_ARG, "som_bmu_plan: null CSR pointer");
-    if ((st = setup(N, M, V, nnz, config, workspace, workspace_bytes, &o, &c, &noop)) != SOM_OK) return st;
-    if (noop) return ok();
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    hipError_t e = som::launch_clear_flags(c.flags, s);
-    if (e != hipSuccess) return hip_fail(e, "som_bmu_plan: flag clear launch");
-    const int32_t *rp = row_ptr, *ci = col_idx;
-    if (o.order) {
-        e = som::launch_order(row_ptr, col_idx, N, nnz, V, c.ob, c.flags, s);
-        if (e != hipSuccess) return hip_fail(e, "som_bmu_plan: ordering launch");
-        rp = c.ob.prp;
-        ci = c.ob.pci;
-    }
-    e = som::launch_plan(o.ta, rp, ci, N, nnz, V, c.plan, c.tiles, c.flags, s);
-    if (e != hipSuccess) return hip_fail(e, "som_bmu_plan launch");
-    return ok();
+    return plan_impl(row_ptr, col_idx, nullptr, N, nnz, V, M, workspace, workspace_bytes, config, stream, kOne,
+                     "som_bmu_plan");
 }
 
 som_status som_bmu_sweep(const float *W, const double *norms, int64_t V, int64_t M, int64_t N, int64_t nnz,
                          void *workspace, size_t workspace_bytes, const som_bmu_config *config, void *stream)
 {
-    return sweep_impl(Book{W, false}, false, norms, V, M, N, nnz, workspace, workspace_bytes, config, stream,
+    return sweep_impl(Book{W, false}, kOne, norms, V, M, N, nnz, workspace, workspace_bytes, config, stream,
                       "som_bmu_sweep");
 }
 
 som_status som_bmu_sweep_f16(const uint16_t *W, const double *norms, int64_t V, int64_t M, int64_t N, int64_t nnz,
                              void *workspace, size_t workspace_bytes, const som_bmu_config *config, void *stream)
 {
-    return sweep_impl(Book{W, true}, false, norms, V, M, N, nnz, workspace, workspace_bytes, config, stream,
+    return sweep_impl(Book{W, true}, kOne, norms, V, M, N, nnz, workspace, workspace_bytes, config, stream,
                       "som_bmu_sweep_f16");
 }
 
@@ -280,49 +326,37 @@ som_status som_bmu_finalize(const double *norms, int64_t V, int64_t M, const int
                             int32_t *bmu, double *dist, void *workspace, size_t workspace_bytes,
                             const som_bmu_config *config, void *stream)
 {
-    Opts o;
-    Carved c;
-    bool noop;
-    som_status st = check_dims(N, M, V, nnz);
-    if (st != SOM_OK) return st;
-    if (N > 0 && (!norms || !row_ptr || !bmu || !dist)) return fail(SOM_ERR_INVALID_ARG, "som_bmu_finalize: null pointer");
-    if ((st = setup(N, M, V, nnz, config, workspace, workspace_bytes, &o, &c, &noop)) != SOM_OK) return st;
-    if (noop) return ok();
-    const int32_t *rp = o.order ? c.ob.prp : row_ptr;
-    const int32_t *perm = o.order ? c.ob.perm : nullptr;
-    hipError_t e = som::launch_finalize(o.ta, norms, M, rp, N, nnz, perm, c.keys, c.dots, bmu, dist,
-                                        static_cast<hipStream_t>(stream));
-    if (e != hipSuccess) return hip_fail(e, "som_bmu_finalize launch");
-    return ok();
+    return finalize_impl(kOne, norms, V, M, row_ptr, N, nnz, bmu, dist, nullptr, nullptr, workspace, workspace_bytes,
+                         config, stream, "som_bmu_finalize");
 }
 
 som_status som_bmu_search(const float *W, const double *norms, int64_t V, int64_t M, const int32_t *row_ptr,
                           const int32_t *col_idx, int64_t N, int64_t nnz, int32_t *bmu, double *dist,
                           void *workspace, size_t workspace_bytes, const som_bmu_config *config, void *stream)
 {
-    return search_impl(Book{W, false}, norms, V, M, row_ptr, col_idx, N, nnz, bmu, dist, nullptr, nullptr, workspace,
-                       workspace_bytes, config, stream, "som_bmu_search");
+    return search_impl(Book{W, false}, kOne, norms, V, M, row_ptr, col_idx, nullptr, N, nnz, bmu, dist, nullptr,
+                       nullptr, workspace, workspace_bytes, config, stream, "som_bmu_search");
 }
 
 som_status som_bmu_search_f16(const uint16_t *W, const double *norms, int64_t V, int64_t M, const int32_t *row_ptr,
                               const int32_t *col_idx, int64_t N, int64_t nnz, int32_t *bmu, double *dist,
                               void *workspace, size_t workspace_bytes, const som_bmu_config *config, void *stream)
 {
-    return search_impl(Book{W, true}, norms, V, M, row_ptr, col_idx, N, nnz, bmu, dist, nullptr, nullptr, workspace,
-                       workspace_bytes, config, stream, "som_bmu_search_f16");
+    return search_impl(Book{W, true}, kOne, norms, V, M, row_ptr, col_idx, nullptr, N, nnz, bmu, dist, nullptr,
+                       nullptr, workspace, workspace_bytes, config, stream, "som_bmu_search_f16");
 }
 
 som_status som_bmu2_sweep(const float *W, const double *norms, int64_t V, int64_t M, int64_t N, int64_t nnz,
                           void *workspace, size_t workspace_bytes, const som_bmu_config *config, void *stream)
 {
-    return sweep_impl(Book{W, false}, true, norms, V, M, N, nnz, workspace, workspace_bytes, config, stream,
+    return sweep_impl(Book{W, false}, kTwo, norms, V, M, N, nnz, workspace, workspace_bytes, config, stream,
                       "som_bmu2_sweep");
 }
 
 som_status som_bmu2_sweep_f16(const uint16_t *W, const double *norms, int64_t V, int64_t M, int64_t N, int64_t nnz,
                               void *workspace, size_t workspace_bytes, const som_bmu_config *config, void *stream)
 {
-    return sweep_impl(Book{W, true}, true, norms, V, M, N, nnz, workspace, workspace_bytes, config, stream,
+    return sweep_impl(Book{W, true}, kTwo, norms, V, M, N, nnz, workspace, workspace_bytes, config, stream,
                       "som_bmu2_sweep_f16");
 }
 
@@ -330,21 +364,8 @@ som_status som_bmu2_finalize(const double *norms, int64_t V, int64_t M, const in
                              int64_t nnz, int32_t *bmu, double *dist, int32_t *bmu2, double *dist2, void *workspace,
                              size_t workspace_bytes, const som_bmu_config *config, void *stream)
 {
-    Opts o;
-    Carved c;
-    bool noop;
-    som_status st = check_dims(N, M, V, nnz);
-    if (st != SOM_OK) return st;
-    if (N > 0 && (!norms || !row_ptr || !bmu || !dist || !bmu2 || !dist2))
-        return fail(SOM_ERR_INVALID_ARG, "som_bmu2_finalize: null pointer");
-    if ((st = setup(N, M, V, nnz, config, workspace, workspace_bytes, &o, &c, &noop, true)) != SOM_OK) return st;
-    if (noop) return ok();
-    const int32_t *rp = o.order ? c.ob.prp : row_ptr;
-    const int32_t *perm = o.order ? c.ob.perm : nullptr;
-    hipError_t e = som::launch_finalize2(o.ta, norms, M, rp, N, nnz, perm, c.keys, c.dots, c.keys2, c.dots2, bmu,
-                                         dist, bmu2, dist2, static_cast<hipStream_t>(stream));
-    if (e != hipSuccess) return hip_fail(e, "som_bmu2_finalize launch");
-    return ok();
+    return finalize_impl(kTwo, norms, V, M, row_ptr, N, nnz, bmu, dist, bmu2, dist2, workspace, workspace_bytes,
+                         config, stream, "som_bmu2_finalize");
 }
 
 som_status som_bmu2_search(const float *W, const double *norms, int64_t V, int64_t M, const int32_t *row_ptr,
@@ -352,9 +373,8 @@ som_status som_bmu2_search(const float *W, const double *norms, int64_t V, int64
                            double *dist2, void *workspace, size_t workspace_bytes, const som_bmu_config *config,
                            void *stream)
 {
-    if (N > 0 && (!bmu2 || !dist2)) return fail(SOM_ERR_INVALID_ARG, "som_bmu2_search: null pointer");
-    return search_impl(Book{W, false}, norms, V, M, row_ptr, col_idx, N, nnz, bmu, dist, bmu2, dist2, workspace,
-                       workspace_bytes, config, stream, "som_bmu2_search");
+    return search_impl(Book{W, false}, kTwo, norms, V, M, row_ptr, col_idx, nullptr, N, nnz, bmu, dist, bmu2, dist2,
+                       workspace, workspace_bytes, config, stream, "som_bmu2_search");
 }
 
 som_status som_bmu2_search_f16(const uint16_t *W, const double *norms, int64_t V, int64_t M, const int32_t *row_ptr,
@@ -362,9 +382,58 @@ som_status som_bmu2_search_f16(const uint16_t *W, const double *norms, int64_t V
                                int32_t *bmu2, double *dist2, void *workspace, size_t workspace_bytes,
                                const som_bmu_config *config, void *stream)
 {
-    if (N > 0 && (!bmu2 || !dist2)) return fail(SOM_ERR_INVALID_ARG, "som_bmu2_search_f16: null pointer");
-    return search_impl(Book{W, true}, norms, V, M, row_ptr, col_idx, N, nnz, bmu, dist, bmu2, dist2, workspace,
-                       workspace_bytes, config, stream, "som_bmu2_search_f16");
+    return search_impl(Book{W, true}, kTwo, norms, V, M, row_ptr, col_idx, nullptr, N, nnz, bmu, dist, bmu2, dist2,
+                       workspace, workspace_bytes, config, stream, "som_bmu2_search_f16");
+}
+
+som_status som_bmu_sf_plan(const int32_t *row_ptr, const int32_t *col_idx, const float *values, int64_t N,
+                           int64_t nnz, int64_t V, int64_t M, void *workspace, size_t workspace_bytes,
+                           const som_bmu_config *config, void *stream)
+{
+    return plan_impl(row_ptr, col_idx, values, N, nnz, V, M, workspace, workspace_bytes, config, stream,
+                     Kind{true, true}, "som_bmu_sf_plan");
+}
+
+som_status som_bmu_sf_sweep(const float *W, const double *norms, int64_t V, int64_t M, int64_t N, int64_t nnz,
+                            int32_t two_best, void *workspace, size_t workspace_bytes, const som_bmu_config *config,
+                            void *stream)
+{
+    return sweep_impl(Book{W, false}, Kind{two_best != 0, true}, norms, V, M, N, nnz, workspace, workspace_bytes,
+                      config, stream, "som_bmu_sf_sweep");
+}
+
+som_status som_bmu_sf_sweep_f16(const uint16_t *W, const double *norms, int64_t V, int64_t M, int64_t N, int64_t nnz,
+                                int32_t two_best, void *workspace, size_t workspace_bytes,
+                                const som_bmu_config *config, void *stream)
+{
+    return sweep_impl(Book{W, true}, Kind{two_best != 0, true}, norms, V, M, N, nnz, workspace, workspace_bytes,
+                      config, stream, "som_bmu_sf_sweep_f16");
+}
+
+som_status som_bmu_sf_finalize(const double *norms, int64_t V, int64_t M, const int32_t *row_ptr, int64_t N,
+                               int64_t nnz, int32_t *bmu, double *dist, int32_t *bmu2, double *dist2, void *workspace,
+                               size_t workspace_bytes, const som_bmu_config *config, void *stream)
+{
+    return finalize_impl(real_kind(bmu2, dist2), norms, V, M, row_ptr, N, nnz, bmu, dist, bmu2, dist2, workspace,
+                         workspace_bytes, config, stream, "som_bmu_sf_finalize");
+}
+
+som_status som_bmu_sf_search(const float *W, const double *norms, int64_t V, int64_t M, const int32_t *row_ptr,
+                             const int32_t *col_idx, const float *values, int64_t N, int64_t nnz, int32_t *bmu,
+                             double *dist, int32_t *bmu2, double *dist2, void *workspace, size_t workspace_bytes,
+                             const som_bmu_config *config, void *stream)
+{
+    return search_impl(Book{W, false}, real_kind(bmu2, dist2), norms, V, M, row_ptr, col_idx, values, N, nnz, bmu,
+                       dist, bmu2, dist2, workspace, workspace_bytes, config, stream, "som_bmu_sf_search");
+}
+
+som_status som_bmu_sf_search_f16(const uint16_t *W, const double *norms, int64_t V, int64_t M, const int32_t *row_ptr,
+                                 const int32_t *col_idx, const float *values, int64_t N, int64_t nnz, int32_t *bmu,
+                                 double *dist, int32_t *bmu2, double *dist2, void *workspace, size_t workspace_bytes,
+                                 const som_bmu_config *config, void *stream)
+{
+    return search_impl(Book{W, true}, real_kind(bmu2, dist2), norms, V, M, row_ptr, col_idx, values, N, nnz, bmu,
+                       dist, bmu2, dist2, workspace, workspace_bytes, config, stream, "som_bmu_sf_search_f16");
 }
 
 som_status som_bmu_input_flags(const void *workspace, size_t workspace_bytes, int64_t N, int64_t M, int64_t V,
@@ -377,7 +446,9 @@ som_status som_bmu_input_flags(const void *workspace, size_t workspace_bytes, in
     if (st != SOM_OK) return st;
     if (!flags) return fail(SOM_ERR_INVALID_ARG, "som_bmu_input_flags: flags is NULL");
     *flags = 0;
-    if ((st = setup(N, M, V, nnz, config, const_cast<void *>(workspace), workspace_bytes, &o, &c, &noop)) != SOM_OK)
+    // the flags lead every layout; the single-best one is a prefix of all others
+    if ((st = setup(N, M, V, nnz, config, const_cast<void *>(workspace), workspace_bytes, kOne, &o, &c, &noop)) !=
+        SOM_OK)
         return st;
     if (noop) return ok();
     hipStream_t s = static_cast<hipStream_t>(stream);

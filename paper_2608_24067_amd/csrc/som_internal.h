@@ -37,13 +37,18 @@ struct Layout {
     size_t pci;     // int32 [nnz]: feature ids of the ordered batch
     size_t keys2;   // uint64 [n_strips * N]: per-strip second-smallest keys (two-best search only)
     size_t dots2;   // float [n_strips * N]: their dot products (two-best search only)
+    size_t vals;    // float [nnz * TA]: sample values of every plan entry (real-valued rows only)
+    size_t xsq;     // double [N]: ||x||^2 by batch position (real-valued rows only)
+    size_t pvals;   // float [nnz]: values of the ordered batch (real-valued rows, regrouped only)
     size_t total;
 };
 
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-// The two-best sections come last, so a single-best layout is a prefix of the two-best one.
-inline Layout layout_for(int64_t N, int64_t M, int64_t V, int64_t nnz, int ta, bool order, bool top2 = false)
+// The two-best sections follow the single-best ones and the real-valued sections
+// follow those, so each smaller layout is a prefix of the larger ones.
+inline Layout layout_for(int64_t N, int64_t M, int64_t V, int64_t nnz, int ta, bool order, bool top2 = false,
+                         bool real = false)
 {
     Layout L;
     size_t off = 0;
@@ -67,6 +72,10 @@ inline Layout layout_for(int64_t N, int64_t M, int64_t V, int64_t nnz, int ta, b
     const size_t t2 = top2 ? 1 : 0;
     L.keys2 = take(t2 * (size_t)n_strips(M, ta) * (size_t)N * 8);
     L.dots2 = take(t2 * (size_t)n_strips(M, ta) * (size_t)N * 4);
+    const size_t r = real ? 1 : 0;
+    L.vals = take(r * (size_t)nnz * (size_t)ta * 4);
+    L.xsq = take(r * (size_t)N * 8);
+    L.pvals = take(r * o * (size_t)nnz * 4);
     L.total = off;
     return L;
 }
@@ -75,34 +84,35 @@ struct OrderBuffers {
     uint32_t *freq;
     unsigned long long *bucket;
     int32_t *skey, *perm, *prp, *pci;
+    float *pvals;  // real-valued rows only
+};
+
+// Where the sweep leaves its per-(sample, strip) results.
+struct SweepOut {
+    unsigned long long *keys;
+    float *dots;
+    unsigned long long *keys2;  // two-best only, else null
+    float *dots2;
 };
 
 // Kernel launchers (som_kernels.hip). Each returns the launch's hipError_t.
 hipError_t launch_norms(const float *W, int64_t V, int64_t M, double *norms, hipStream_t st);
 // fp16 codebooks: W holds IEEE binary16 bit patterns.
 hipError_t launch_norms_f16(const uint16_t *W, int64_t V, int64_t M, double *norms, hipStream_t st);
-hipError_t launch_sweep_f16(int ta, const uint16_t *W, const double *norms, int64_t M, int64_t N, int64_t V,
-                            int64_t nnz, const uint2 *plan, const int2 *tiles, unsigned long long *keys, float *dots,
-                            hipStream_t st);
-hipError_t launch_sweep2_f16(int ta, const uint16_t *W, const double *norms, int64_t M, int64_t N, int64_t V,
-                             int64_t nnz, const uint2 *plan, const int2 *tiles, unsigned long long *keys, float *dots,
-                             unsigned long long *keys2, float *dots2, hipStream_t st);
 hipError_t launch_clear_flags(uint32_t *flags, hipStream_t st);
-hipError_t launch_plan(int ta, const int32_t *row_ptr, const int32_t *col_idx, int64_t N, int64_t nnz, int64_t V,
-                       uint2 *plan, int2 *tiles, uint32_t *flags, hipStream_t st);
-hipError_t launch_sweep(int ta, const float *W, const double *norms, int64_t M, int64_t N, int64_t V, int64_t nnz,
-                        const uint2 *plan, const int2 *tiles, unsigned long long *keys, float *dots, hipStream_t st);
+// values, vals, xsq: real-valued rows only (else null).
+hipError_t launch_plan(int ta, const int32_t *row_ptr, const int32_t *col_idx, const float *values, int64_t N,
+                       int64_t nnz, int64_t V, uint2 *plan, int2 *tiles, float *vals, double *xsq, uint32_t *flags,
+                       hipStream_t st);
+// f16: W holds binary16 values; top2: fill keys2/dots2 too; vals: real-valued rows (tile 8 only).
+hipError_t launch_sweep(int ta, bool f16, bool top2, const void *W, const double *norms, int64_t M, int64_t N,
+                        int64_t V, int64_t nnz, const uint2 *plan, const int2 *tiles, const float *vals,
+                        const SweepOut &o, hipStream_t st);
+// bmu2/dist2 non-null: the two best units. xsq: real-valued rows (else ||x||^2 = nnz of the row).
 hipError_t launch_finalize(int ta, const double *norms, int64_t M, const int32_t *row_ptr, int64_t N, int64_t nnz,
-                           const int32_t *perm, const unsigned long long *keys, const float *dots, int32_t *bmu,
-                           double *dist, hipStream_t st);
-hipError_t launch_sweep2(int ta, const float *W, const double *norms, int64_t M, int64_t N, int64_t V, int64_t nnz,
-                         const uint2 *plan, const int2 *tiles, unsigned long long *keys, float *dots,
-                         unsigned long long *keys2, float *dots2, hipStream_t st);
-hipError_t launch_finalize2(int ta, const double *norms, int64_t M, const int32_t *row_ptr, int64_t N, int64_t nnz,
-                            const int32_t *perm, const unsigned long long *keys, const float *dots,
-                            const unsigned long long *keys2, const float *dots2, int32_t *bmu, double *dist,
-                            int32_t *bmu2, double *dist2, hipStream_t st);
-hipError_t launch_order(const int32_t *row_ptr, const int32_t *col_idx, int64_t N, int64_t nnz, int64_t V,
-                        const OrderBuffers &ob, uint32_t *flags, hipStream_t st);
+                           const int32_t *perm, const double *xsq, const SweepOut &o, int32_t *bmu, double *dist,
+                           int32_t *bmu2, double *dist2, hipStream_t st);
+hipError_t launch_order(const int32_t *row_ptr, const int32_t *col_idx, const float *values, int64_t N, int64_t nnz,
+                        int64_t V, const OrderBuffers &ob, uint32_t *flags, hipStream_t st);
 
 }  // namespace som

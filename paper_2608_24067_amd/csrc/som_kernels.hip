@@ -379,12 +379,14 @@ __global__ __launch_bounds__(256) void k_place(const int32_t *__restrict__ row_p
     }
 }
 
-// Position k copies the ids of sample perm[k] to pci[prp[k] ...]: consecutive threads
-// write consecutive rows. Sample indices and offsets are re-checked, so positions
-// never placed (invalid input only) cannot drive an access out of bounds.
+// Position k copies the ids of sample perm[k] to pci[prp[k] ...] (and its values to
+// pvals, for real-valued rows): consecutive threads write consecutive rows. Sample
+// indices and offsets are re-checked, so positions never placed (invalid input
+// only) cannot drive an access out of bounds.
 __global__ __launch_bounds__(256) void k_gather(const int32_t *__restrict__ row_ptr, const int32_t *__restrict__ col_idx,
                                                 int64_t N, int64_t nnz, const int32_t *__restrict__ perm,
-                                                const int32_t *__restrict__ prp, int32_t *__restrict__ pci)
+                                                const int32_t *__restrict__ prp, int32_t *__restrict__ pci,
+                                                const float *__restrict__ values, float *__restrict__ pvals)
 {
     const int64_t base = row_ptr[0];
     uint32_t bad = 0;
@@ -406,6 +408,18 @@ __global__ __launch_bounds__(256) void k_gather(const int32_t *__restrict__ row_
         for (int q = 0; q < 16; ++q)
             if (q < n) out[q] = v[q];
         for (int64_t q = 16; q < n; ++q) out[q] = src[q];
+        if (values) {
+            const float *vs = values + base + rb;
+            float *vo = pvals + dst;
+            float x[16];
+#pragma unroll
+            for (int q = 0; q < 16; ++q)
+                if (q < n) x[q] = vs[q];
+#pragma unroll
+            for (int q = 0; q < 16; ++q)
+                if (q < n) vo[q] = x[q];
+            for (int64_t q = 16; q < n; ++q) vo[q] = vs[q];
+        }
     }
 }
 
@@ -422,11 +436,17 @@ constexpr int kPlanStage = 2048;  // ids staged in LDS per wave
 // and to each tile's own range, ids outside [0, V) are skipped, and a tile never
 // writes more entries than its own CSR span, so no input can drive an access out
 // of bounds.
+//
+// Real-valued rows (values != nullptr): every union entry also gets the TA values of
+// its samples (vals[entry*TA + s], written for the samples whose mask bit is set;
+// the other slots are never read), and every row the fp64 sum of its squared
+// values in its own order (xsq, by batch position), which is ||x||^2.
 template <int TA>
 __global__ __launch_bounds__(256) void k_plan(const int32_t *__restrict__ row_ptr, const int32_t *__restrict__ col_idx,
                                               int64_t N, int64_t nnz, int32_t V, int64_t n_tiles,
                                               uint2 *__restrict__ plan, int2 *__restrict__ tiles,
-                                              uint32_t *__restrict__ flags)
+                                              uint32_t *__restrict__ flags, const float *__restrict__ values,
+                                              float *__restrict__ vals, double *__restrict__ xsq)
 {
     constexpr int G = 64 / TA;  // tiles per wave
     __shared__ int32_t stage[kPlanWaves][kPlanStage];
@@ -469,13 +489,19 @@ __global__ __launch_bounds__(256) void k_plan(const int32_t *__restrict__ row_pt
 
         int64_t p = b;
         int cur = INT_MAX;
-        // next valid id of this lane's row (INT_MAX once the row is done)
+        float curv = 0.0f;
+        double sq = 0.0;
+        // next valid id of this lane's row (INT_MAX once the row is done), with its value
         auto fetch = [&]() {
             cur = INT_MAX;
             while (p < e) {
                 const int id = staged ? stage[wv][p - wlo] : col_idx[base + p];
                 if (id >= 0 && id < V) {
                     cur = id;
+                    if (values) {
+                        curv = values[base + p];
+                        sq = fma((double)curv, (double)curv, sq);
+                    }
                     break;
                 }
                 bad |= SOM_FLAG_ID_RANGE;
@@ -498,6 +524,7 @@ __global__ __launch_bounds__(256) void k_plan(const int32_t *__restrict__ row_pt
             const unsigned mask = (unsigned)((bal >> (grp * TA)) & (TA == 32 ? 0xFFFFFFFFull : ((1ull << TA) - 1)));
             if (m != INT_MAX) {
                 if (sl == 0) plan[lo + k] = make_uint2((unsigned)m, mask);
+                if (values && cur == m) vals[(lo + k) * TA + sl] = curv;
                 ++k;
                 if (cur == m) {
                     ++p;
@@ -507,6 +534,7 @@ __global__ __launch_bounds__(256) void k_plan(const int32_t *__restrict__ row_pt
             }
         }
         if (live && sl == 0) tiles[t] = make_int2((int)lo, (int)k);
+        if (values && live && t * TA + sl < N) xsq[t * TA + sl] = sq;
         __syncthreads();
     }
     if (bad) atomicOr(flags, bad);
@@ -523,12 +551,18 @@ __global__ __launch_bounds__(256) void k_plan(const int32_t *__restrict__ row_pt
 //
 // TOP2: each (sample, strip) also gets its second-smallest key and that neuron's dot
 // product (keys2, dots2), for the two best units of the fused sweep.
-template <typename E, int TA, int NPL, int U, bool VEC, bool TOP2>
+//
+// REAL: real-valued rows (the Discussion's gather-multiply variant). The plan holds
+// each union entry's TA sample values (vals); a set mask bit adds value * weight
+// (one fused multiply-add, fp32) instead of the weight, still in ascending feature
+// order per sample.
+template <typename E, int TA, int NPL, int U, bool VEC, bool TOP2, bool REAL>
 __global__ __launch_bounds__(256) void k_sweep(const E *__restrict__ W, const double *__restrict__ norms,
                                                int64_t M, int64_t N, int64_t V, int64_t nnz,
                                                const uint2 *__restrict__ plan, const int2 *__restrict__ tiles,
                                                int64_t n_tiles, u64 *__restrict__ keys, float *__restrict__ dots,
-                                               u64 *__restrict__ keys2, float *__restrict__ dots2)
+                                               u64 *__restrict__ keys2, float *__restrict__ dots2,
+                                               const float *__restrict__ vals)
 {
     const int lane = threadIdx.x & 63;
     const int wv = wave_id();
@@ -619,21 +653,34 @@ __global__ __launch_bounds__(256) void k_sweep(const E *__restrict__ W, const do
         // The mask is wave-uniform: each bit is a scalar branch. The empty volatile
         // asm keeps the compiler from turning the branch into unconditional adds
         // and selects.
-        auto row_add = [&](unsigned mask, const Seg &seg) {
+        // xv: the entry's TA sample values (REAL only; scalar registers)
+        auto row_add = [&](unsigned mask, const Seg &seg, const float *xv) {
             if constexpr (sizeof(E) == 2 && VEC) {
-                // Packed fp16: each add is one mixed-precision FMA, acc + h * 1.0 with h
-                // read as a half straight from the loaded dword (exact widening, one
-                // rounding: the same result as widening first and adding).
+                // Packed fp16: each update is one mixed-precision FMA with h read as a
+                // half straight from the loaded dword (exact widening, one rounding):
+                // acc + h * 1.0, or acc + h * x for real values -- the same result as
+                // widening first.
                 const unsigned *dw = reinterpret_cast<const unsigned *>(&seg.v[0]);
 #pragma unroll
                 for (int s = 0; s < TA; ++s) {
                     if (mask & (1u << s)) {
 #pragma unroll
                         for (int d = 0; d < NPL / 2; ++d) {
-                            asm("v_fma_mix_f32 %0, %1, 1.0, %0 op_sel_hi:[1,0,0]" : "+v"(acc[s][2 * d]) : "v"(dw[d]));
-                            asm("v_fma_mix_f32 %0, %1, 1.0, %0 op_sel:[1,0,0] op_sel_hi:[1,0,0]"
-                                : "+v"(acc[s][2 * d + 1])
-                                : "v"(dw[d]));
+                            if constexpr (REAL) {
+                                asm("v_fma_mix_f32 %0, %1, %2, %0 op_sel_hi:[1,0,0]"
+                                    : "+v"(acc[s][2 * d])
+                                    : "v"(dw[d]), "s"(xv[s]));
+                                asm("v_fma_mix_f32 %0, %1, %2, %0 op_sel:[1,0,0] op_sel_hi:[1,0,0]"
+                                    : "+v"(acc[s][2 * d + 1])
+                                    : "v"(dw[d]), "s"(xv[s]));
+                            } else {
+                                asm("v_fma_mix_f32 %0, %1, 1.0, %0 op_sel_hi:[1,0,0]"
+                                    : "+v"(acc[s][2 * d])
+                                    : "v"(dw[d]));
+                                asm("v_fma_mix_f32 %0, %1, 1.0, %0 op_sel:[1,0,0] op_sel_hi:[1,0,0]"
+                                    : "+v"(acc[s][2 * d + 1])
+                                    : "v"(dw[d]));
+                            }
                         }
                         asm volatile("");
                     }
@@ -651,10 +698,23 @@ __global__ __launch_bounds__(256) void k_sweep(const E *__restrict__ W, const do
                 for (int s = 0; s < TA; ++s) {
                     if (mask & (1u << s)) {
 #pragma unroll
-                        for (int j = 0; j < NPL; ++j) acc[s][j] += w[j];
+                        for (int j = 0; j < NPL; ++j) {
+                            if constexpr (REAL)
+                                acc[s][j] = fmaf(xv[s], w[j], acc[s][j]);
+                            else
+                                acc[s][j] += w[j];
+                        }
                         asm volatile("");
                     }
                 }
+            }
+        };
+        // the TA sample values of plan entry q (REAL only)
+        auto entry_values = [&](int64_t q, float *xv) {
+            if constexpr (REAL) {
+                const float *src = vals + (off + q) * TA;
+#pragma unroll
+                for (int s = 0; s < TA; ++s) xv[s] = src[s];
             }
         };
 
@@ -672,14 +732,19 @@ __global__ __launch_bounds__(256) void k_sweep(const E *__restrict__ W, const do
             Seg seg[U];
 #pragma unroll
             for (int u = 0; u < U; ++u) row_load(en[u].x, seg[u]);
+            float xv[U][TA];
 #pragma unroll
-            for (int u = 0; u < U; ++u) row_add(en[u].y, seg[u]);
+            for (int u = 0; u < U; ++u) entry_values(k + u, xv[u]);
+#pragma unroll
+            for (int u = 0; u < U; ++u) row_add(en[u].y, seg[u], xv[u]);
         }
         for (; k < cnt; ++k) {
             const uint2 en = ent[k];
             Seg seg;
             row_load(en.x, seg);
-            row_add(en.y, seg);
+            float xv[TA];
+            entry_values(k, xv);
+            row_add(en.y, seg, xv);
         }
         // The next tile's table entries are read now, its first plan entries halfway
         // through this tile's epilogue; both are in flight while the epilogue runs.
@@ -869,10 +934,12 @@ __global__ __launch_bounds__(256) void k_sweep(const E *__restrict__ W, const do
 // One thread per position k of the (possibly permuted) batch: smallest key over the
 // strips; the winner's dot product comes from the sweep (the same fp32 sum of the
 // row's weights in ascending feature order), so the full squared distance is
-// (||w||^2 - 2*dot) + nnz. Results go to sample perm[k] (k without a permutation).
+// (||w||^2 - 2*dot) + ||x||^2, with ||x||^2 = nnz for binary rows and xsq[k] from the
+// plan for real-valued ones. Results go to sample perm[k] (k without a permutation).
 __global__ __launch_bounds__(256) void k_finalize(const double *__restrict__ norms, int64_t M,
                                                   const int32_t *__restrict__ row_ptr, int64_t N, int64_t nnz,
-                                                  const int32_t *__restrict__ perm, const u64 *__restrict__ keys,
+                                                  const int32_t *__restrict__ perm, const double *__restrict__ xsq,
+                                                  const u64 *__restrict__ keys,
                                                   const float *__restrict__ dots, int64_t n_strips,
                                                   int32_t *__restrict__ bmu, double *__restrict__ dist)
 {
@@ -894,7 +961,7 @@ __global__ __launch_bounds__(256) void k_finalize(const double *__restrict__ nor
         const int64_t rb = clamp64((int64_t)row_ptr[k] - base, 0, nnz);
         const int64_t re = clamp64((int64_t)row_ptr[k + 1] - base, rb, nnz);
         bmu[s] = (int32_t)b;
-        dist[s] = fma(-2.0, (double)dots[gb * N + k], norms[b]) + (double)(re - rb);
+        dist[s] = fma(-2.0, (double)dots[gb * N + k], norms[b]) + (xsq ? xsq[k] : (double)(re - rb));
     }
 }
 
@@ -903,7 +970,8 @@ __global__ __launch_bounds__(256) void k_finalize(const double *__restrict__ nor
 // unit (M == 1) bmu2 = -1 and dist2 = +inf.
 __global__ __launch_bounds__(256) void k_finalize2(const double *__restrict__ norms, int64_t M,
                                                    const int32_t *__restrict__ row_ptr, int64_t N, int64_t nnz,
-                                                   const int32_t *__restrict__ perm, const u64 *__restrict__ keys,
+                                                   const int32_t *__restrict__ perm, const double *__restrict__ xsq,
+                                                   const u64 *__restrict__ keys,
                                                    const float *__restrict__ dots, const u64 *__restrict__ keys2,
                                                    const float *__restrict__ dots2, int64_t n_strips,
                                                    int32_t *__restrict__ bmu, double *__restrict__ dist,
@@ -932,7 +1000,7 @@ __global__ __launch_bounds__(256) void k_finalize2(const double *__restrict__ no
         }
         const int64_t rb = clamp64((int64_t)row_ptr[k] - base, 0, nnz);
         const int64_t re = clamp64((int64_t)row_ptr[k + 1] - base, rb, nnz);
-        const double len = (double)(re - rb);
+        const double len = xsq ? xsq[k] : (double)(re - rb);
         int64_t i1 = (int64_t)(b1 & kIndexMask);
         if (i1 >= M) i1 = M - 1;
         bmu[s] = (int32_t)i1;
@@ -974,34 +1042,45 @@ hipError_t launch_clear_flags(uint32_t *flags, hipStream_t st)
     return hipGetLastError();
 }
 
-hipError_t launch_plan(int ta, const int32_t *row_ptr, const int32_t *col_idx, int64_t N, int64_t nnz, int64_t V,
-                       uint2 *plan, int2 *tiles, uint32_t *flags, hipStream_t st)
+hipError_t launch_plan(int ta, const int32_t *row_ptr, const int32_t *col_idx, const float *values, int64_t N,
+                       int64_t nnz, int64_t V, uint2 *plan, int2 *tiles, float *vals, double *xsq, uint32_t *flags,
+                       hipStream_t st)
 {
     const int64_t nt = n_tiles(N, ta);
     const int64_t per_block = (int64_t)kPlanWaves * (64 / ta);
     int64_t blocks = (nt + per_block - 1) / per_block;
     if (blocks > (1 << 22)) blocks = 1 << 22;
     const dim3 grid((unsigned)blocks), block(256);
+    const int32_t v = (int32_t)V;
     switch (ta) {
-    case 8: hipLaunchKernelGGL(k_plan<8>, grid, block, 0, st, row_ptr, col_idx, N, nnz, (int32_t)V, nt, plan, tiles, flags); break;
-    case 16: hipLaunchKernelGGL(k_plan<16>, grid, block, 0, st, row_ptr, col_idx, N, nnz, (int32_t)V, nt, plan, tiles, flags); break;
-    case 32: hipLaunchKernelGGL(k_plan<32>, grid, block, 0, st, row_ptr, col_idx, N, nnz, (int32_t)V, nt, plan, tiles, flags); break;
+    case 8:
+        hipLaunchKernelGGL(k_plan<8>, grid, block, 0, st, row_ptr, col_idx, N, nnz, v, nt, plan, tiles, flags, values,
+                           vals, xsq);
+        break;
+    case 16:
+        hipLaunchKernelGGL(k_plan<16>, grid, block, 0, st, row_ptr, col_idx, N, nnz, v, nt, plan, tiles, flags, values,
+                           vals, xsq);
+        break;
+    case 32:
+        hipLaunchKernelGGL(k_plan<32>, grid, block, 0, st, row_ptr, col_idx, N, nnz, v, nt, plan, tiles, flags, values,
+                           vals, xsq);
+        break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
 }
 
-template <typename E, int TA, int NPL, bool TOP2>
+template <typename E, int TA, int NPL, bool TOP2, bool REAL>
 static void sweep_ta(bool vec, dim3 grid, hipStream_t st, const E *W, const double *norms, int64_t M, int64_t N,
-                     int64_t V, int64_t nnz, const uint2 *plan, const int2 *tiles, int64_t nt, u64 *keys, float *dots,
-                     u64 *keys2, float *dots2)
+                     int64_t V, int64_t nnz, const uint2 *plan, const int2 *tiles, int64_t nt, const SweepOut &o,
+                     const float *vals)
 {
     if (vec)
-        hipLaunchKernelGGL((k_sweep<E, TA, NPL, 4, true, TOP2>), grid, dim3(256), 0, st, W, norms, M, N, V, nnz, plan,
-                           tiles, nt, keys, dots, keys2, dots2);
+        hipLaunchKernelGGL((k_sweep<E, TA, NPL, 4, true, TOP2, REAL>), grid, dim3(256), 0, st, W, norms, M, N, V, nnz,
+                           plan, tiles, nt, o.keys, o.dots, o.keys2, o.dots2, vals);
     else
-        hipLaunchKernelGGL((k_sweep<E, TA, NPL, 4, false, TOP2>), grid, dim3(256), 0, st, W, norms, M, N, V, nnz, plan,
-                           tiles, nt, keys, dots, keys2, dots2);
+        hipLaunchKernelGGL((k_sweep<E, TA, NPL, 4, false, TOP2, REAL>), grid, dim3(256), 0, st, W, norms, M, N, V, nnz,
+                           plan, tiles, nt, o.keys, o.dots, o.keys2, o.dots2, vals);
 }
 
 // Vector loads need M to be a multiple of the group and W aligned to the group's bytes.
@@ -1014,85 +1093,68 @@ static bool vector_loads(const E *W, int64_t M)
 
 template <typename E, bool TOP2>
 static hipError_t sweep_any(int ta, const E *W, const double *norms, int64_t M, int64_t N, int64_t V, int64_t nnz,
-                            const uint2 *plan, const int2 *tiles, u64 *keys, float *dots, u64 *keys2, float *dots2,
+                            const uint2 *plan, const int2 *tiles, const float *vals, const SweepOut &o,
                             hipStream_t st)
 {
     const int64_t nt = n_tiles(N, ta);
     int64_t gx = (nt + 3) / 4;
     if (gx > (1 << 22)) gx = 1 << 22;
     const dim3 grid((unsigned)gx, (unsigned)n_strips(M, ta));
+    if (vals) {  // real-valued rows: tiles of 8 only (8 values per plan entry in scalar registers)
+        if (ta != 8) return hipErrorInvalidValue;
+        sweep_ta<E, 8, 8, TOP2, true>(vector_loads<E, 8>(W, M), grid, st, W, norms, M, N, V, nnz, plan, tiles, nt, o,
+                                      vals);
+        return hipGetLastError();
+    }
     switch (ta) {
     case 8:
-        sweep_ta<E, 8, 8, TOP2>(vector_loads<E, 8>(W, M), grid, st, W, norms, M, N, V, nnz, plan, tiles, nt, keys, dots,
-                                keys2, dots2);
+        sweep_ta<E, 8, 8, TOP2, false>(vector_loads<E, 8>(W, M), grid, st, W, norms, M, N, V, nnz, plan, tiles, nt, o,
+                                       nullptr);
         break;
     case 16:
-        sweep_ta<E, 16, 4, TOP2>(vector_loads<E, 4>(W, M), grid, st, W, norms, M, N, V, nnz, plan, tiles, nt, keys,
-                                 dots, keys2, dots2);
+        sweep_ta<E, 16, 4, TOP2, false>(vector_loads<E, 4>(W, M), grid, st, W, norms, M, N, V, nnz, plan, tiles, nt, o,
+                                        nullptr);
         break;
     case 32:
-        sweep_ta<E, 32, 4, TOP2>(vector_loads<E, 4>(W, M), grid, st, W, norms, M, N, V, nnz, plan, tiles, nt, keys,
-                                 dots, keys2, dots2);
+        sweep_ta<E, 32, 4, TOP2, false>(vector_loads<E, 4>(W, M), grid, st, W, norms, M, N, V, nnz, plan, tiles, nt, o,
+                                        nullptr);
         break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
 }
 
-hipError_t launch_sweep(int ta, const float *W, const double *norms, int64_t M, int64_t N, int64_t V, int64_t nnz,
-                        const uint2 *plan, const int2 *tiles, unsigned long long *keys, float *dots, hipStream_t st)
+hipError_t launch_sweep(int ta, bool f16, bool top2, const void *W, const double *norms, int64_t M, int64_t N,
+                        int64_t V, int64_t nnz, const uint2 *plan, const int2 *tiles, const float *vals,
+                        const SweepOut &o, hipStream_t st)
 {
-    return sweep_any<float, false>(ta, W, norms, M, N, V, nnz, plan, tiles, keys, dots, nullptr, nullptr, st);
-}
-
-hipError_t launch_sweep2(int ta, const float *W, const double *norms, int64_t M, int64_t N, int64_t V, int64_t nnz,
-                         const uint2 *plan, const int2 *tiles, unsigned long long *keys, float *dots,
-                         unsigned long long *keys2, float *dots2, hipStream_t st)
-{
-    return sweep_any<float, true>(ta, W, norms, M, N, V, nnz, plan, tiles, keys, dots, keys2, dots2, st);
-}
-
-hipError_t launch_sweep_f16(int ta, const uint16_t *W, const double *norms, int64_t M, int64_t N, int64_t V,
-                            int64_t nnz, const uint2 *plan, const int2 *tiles, unsigned long long *keys, float *dots,
-                            hipStream_t st)
-{
-    return sweep_any<_Float16, false>(ta, reinterpret_cast<const _Float16 *>(W), norms, M, N, V, nnz, plan, tiles,
-                                      keys, dots, nullptr, nullptr, st);
-}
-
-hipError_t launch_sweep2_f16(int ta, const uint16_t *W, const double *norms, int64_t M, int64_t N, int64_t V,
-                             int64_t nnz, const uint2 *plan, const int2 *tiles, unsigned long long *keys, float *dots,
-                             unsigned long long *keys2, float *dots2, hipStream_t st)
-{
-    return sweep_any<_Float16, true>(ta, reinterpret_cast<const _Float16 *>(W), norms, M, N, V, nnz, plan, tiles,
-                                     keys, dots, keys2, dots2, st);
+    if (f16) {
+        const _Float16 *w = static_cast<const _Float16 *>(W);
+        return top2 ? sweep_any<_Float16, true>(ta, w, norms, M, N, V, nnz, plan, tiles, vals, o, st)
+                    : sweep_any<_Float16, false>(ta, w, norms, M, N, V, nnz, plan, tiles, vals, o, st);
+    }
+    const float *w = static_cast<const float *>(W);
+    return top2 ? sweep_any<float, true>(ta, w, norms, M, N, V, nnz, plan, tiles, vals, o, st)
+                : sweep_any<float, false>(ta, w, norms, M, N, V, nnz, plan, tiles, vals, o, st);
 }
 
 hipError_t launch_finalize(int ta, const double *norms, int64_t M, const int32_t *row_ptr, int64_t N, int64_t nnz,
-                           const int32_t *perm, const unsigned long long *keys, const float *dots, int32_t *bmu,
-                           double *dist, hipStream_t st)
+                           const int32_t *perm, const double *xsq, const SweepOut &o, int32_t *bmu, double *dist,
+                           int32_t *bmu2, double *dist2, hipStream_t st)
 {
     int64_t blocks = (N + 255) / 256;
     if (blocks > (1 << 22)) blocks = 1 << 22;
-    hipLaunchKernelGGL(k_finalize, dim3((unsigned)blocks), dim3(256), 0, st, norms, M, row_ptr, N, nnz, perm, keys, dots,
-                       n_strips(M, ta), bmu, dist);
+    if (bmu2)
+        hipLaunchKernelGGL(k_finalize2, dim3((unsigned)blocks), dim3(256), 0, st, norms, M, row_ptr, N, nnz, perm, xsq,
+                           o.keys, o.dots, o.keys2, o.dots2, n_strips(M, ta), bmu, dist, bmu2, dist2);
+    else
+        hipLaunchKernelGGL(k_finalize, dim3((unsigned)blocks), dim3(256), 0, st, norms, M, row_ptr, N, nnz, perm, xsq,
+                           o.keys, o.dots, n_strips(M, ta), bmu, dist);
     return hipGetLastError();
 }
 
-hipError_t launch_finalize2(int ta, const double *norms, int64_t M, const int32_t *row_ptr, int64_t N, int64_t nnz,
-                            const int32_t *perm, const unsigned long long *keys, const float *dots,
-                            const unsigned long long *keys2, const float *dots2, int32_t *bmu, double *dist,
-                            int32_t *bmu2, double *dist2, hipStream_t st)
-{
-    int64_t blocks = (N + 255) / 256;
-    if (blocks > (1 << 22)) blocks = 1 << 22;
-    hipLaunchKernelGGL(k_finalize2, dim3((unsigned)blocks), dim3(256), 0, st, norms, M, row_ptr, N, nnz, perm, keys,
-                       dots, keys2, dots2, n_strips(M, ta), bmu, dist, bmu2, dist2);
-    return hipGetLastError();
-}
-
-hipError_t launch_order(const int32_t *row_ptr, const int32_t *col_idx, int64_t N, int64_t nnz, int64_t V,
-                        const OrderBuffers &ob, uint32_t *flags, hipStream_t st)
+hipError_t launch_order(const int32_t *row_ptr, const int32_t *col_idx, const float *values, int64_t N, int64_t nnz,
+                        int64_t V, const OrderBuffers &ob, uint32_t *flags, hipStream_t st)
 {
     const int64_t nb = V + 1;  // one bucket per feature, one for rows without a valid feature
     int64_t fb = (nb + 255) / 256;
@@ -1113,7 +1175,7 @@ hipError_t launch_order(const int32_t *row_ptr, const int32_t *col_idx, int64_t 
     hipLaunchKernelGGL(k_place, dim3((unsigned)sb), dim3(256), 0, st, row_ptr, N, nnz, ob.skey, ob.bucket, ob.perm,
                        ob.prp);
     hipLaunchKernelGGL(k_gather, dim3((unsigned)sb), dim3(256), 0, st, row_ptr, col_idx, N, nnz, ob.perm, ob.prp,
-                       ob.pci);
+                       ob.pci, values, values ? ob.pvals : nullptr);
     return hipGetLastError();
 }
 

@@ -26,7 +26,8 @@ EXPORTS = (
     "som_bmu_workspace_bytes", "som_codebook_norms", "som_bmu_search", "som_bmu_plan", "som_bmu_sweep",
     "som_bmu_finalize", "som_bmu2_workspace_bytes", "som_bmu2_search", "som_bmu2_sweep", "som_bmu2_finalize",
     "som_codebook_norms_f16", "som_bmu_search_f16", "som_bmu_sweep_f16", "som_bmu2_search_f16", "som_bmu2_sweep_f16",
-    "som_bmu_input_flags",
+    "som_bmu_sf_workspace_bytes", "som_bmu_sf_search", "som_bmu_sf_search_f16", "som_bmu_sf_plan", "som_bmu_sf_sweep",
+    "som_bmu_sf_sweep_f16", "som_bmu_sf_finalize", "som_bmu_input_flags",
     "som_validate_csr_host", "som_last_error",
 )
 
@@ -74,6 +75,18 @@ def load():
     for name in ("som_codebook_norms", "som_bmu_search", "som_bmu_sweep", "som_bmu2_search", "som_bmu2_sweep"):
         getattr(lib, name + "_f16").argtypes = getattr(lib, name).argtypes
         getattr(lib, name + "_f16").restype = ctypes.c_int
+    i32 = ctypes.c_int32
+    lib.som_bmu_sf_workspace_bytes.argtypes = [i64, i64, i64, i64, cfgp]
+    lib.som_bmu_sf_workspace_bytes.restype = sz
+    lib.som_bmu_sf_search.argtypes = [vp, vp, i64, i64, vp, vp, vp, i64, i64, vp, vp, vp, vp, vp, sz, cfgp, vp]
+    lib.som_bmu_sf_search_f16.argtypes = lib.som_bmu_sf_search.argtypes
+    lib.som_bmu_sf_plan.argtypes = [vp, vp, vp, i64, i64, i64, i64, vp, sz, cfgp, vp]
+    lib.som_bmu_sf_sweep.argtypes = [vp, vp, i64, i64, i64, i64, i32, vp, sz, cfgp, vp]
+    lib.som_bmu_sf_sweep_f16.argtypes = lib.som_bmu_sf_sweep.argtypes
+    lib.som_bmu_sf_finalize.argtypes = [vp, i64, i64, vp, i64, i64, vp, vp, vp, vp, vp, sz, cfgp, vp]
+    for name in ("som_bmu_sf_search", "som_bmu_sf_search_f16", "som_bmu_sf_plan", "som_bmu_sf_sweep",
+                 "som_bmu_sf_sweep_f16", "som_bmu_sf_finalize"):
+        getattr(lib, name).restype = ctypes.c_int
     lib.som_bmu_input_flags.argtypes = [vp, sz, i64, i64, i64, i64, cfgp, ctypes.POINTER(ctypes.c_uint32), vp]
     lib.som_validate_csr_host.argtypes = [vp, vp, i64, i64]
     for name in ("som_codebook_norms", "som_bmu_search", "som_bmu_plan", "som_bmu_sweep", "som_bmu_finalize",
@@ -287,3 +300,77 @@ def validate_csr_host(row_ptr, col_idx, V: int) -> None:
     N = rp.shape[0] - 1
     st = load().som_validate_csr_host(rp.ctypes.data, ci.ctypes.data if ci.size else None, N, V)
     _check(st, "som_validate_csr_host")
+
+
+# ------------------------------------------------------------ sparse real-valued rows
+
+def workspace_sf_bytes(N: int, M: int, V: int, nnz: int, tile_samples: int = 0, keep_order: bool = False) -> int:
+    n = load().som_bmu_sf_workspace_bytes(N, M, V, nnz, _cfg(tile_samples, keep_order))
+    if n == 0:
+        raise ValueError("som_bmu_sf_workspace_bytes: invalid sizes or config")
+    return n
+
+
+def alloc_workspace_sf(N: int, M: int, V: int, nnz: int, device, tile_samples: int = 0,
+                       keep_order: bool = False) -> torch.Tensor:
+    return torch.empty(workspace_sf_bytes(N, M, V, nnz, tile_samples, keep_order), dtype=torch.uint8, device=device)
+
+
+def bmu_sf_search(W, norms, row_ptr, col_idx, values, V: int, M: int, nnz: int | None = None, two_best: bool = False,
+                  out=None, workspace=None, tile_samples: int = 0, keep_order: bool = False):
+    """BMU search over sparse real-valued rows (values[p] belongs to col_idx[p]).
+
+    Returns (bmu, dist), or (bmu, dist, bmu2, dist2) with two_best. W float32 or float16.
+    """
+    N = row_ptr.numel() - 1
+    nnz = _nnz(row_ptr, N, nnz)
+    dev = W.device
+    if out is None:
+        out = (torch.empty(N, dtype=torch.int32, device=dev), torch.empty(N, dtype=torch.float64, device=dev))
+        if two_best:
+            out = out + (torch.empty(N, dtype=torch.int32, device=dev), torch.empty(N, dtype=torch.float64, device=dev))
+    if workspace is None:
+        workspace = alloc_workspace_sf(N, M, V, nnz, dev, tile_samples, keep_order)
+    if values.numel() < nnz:
+        raise ValueError(f"values holds {values.numel()} entries, nnz is {nnz}")
+    fn, wp, name = _book(W, V, M, "som_bmu_sf_search")
+    rp, ci = _csr(row_ptr, col_idx, N, nnz)
+    vp = _dev(values, "values", torch.float32) if values.numel() else None
+    b2 = _dev(out[2], "bmu2", torch.int32, N) if two_best else None
+    d2 = _dev(out[3], "dist2", torch.float64, N) if two_best else None
+    st = fn(wp, _dev(norms, "norms", torch.float64, M), V, M, rp, ci, vp, N, nnz,
+            _dev(out[0], "bmu", torch.int32, N), _dev(out[1], "dist", torch.float64, N), b2, d2,
+            _dev(workspace, "workspace", torch.uint8), workspace.numel(), _cfg(tile_samples, keep_order), _stream(W))
+    _check(st, name)
+    return out
+
+
+def bmu_sf_plan(row_ptr, col_idx, values, V: int, M: int, nnz: int, workspace, tile_samples: int = 0,
+                keep_order: bool = False):
+    N = row_ptr.numel() - 1
+    rp, ci = _csr(row_ptr, col_idx, N, nnz)
+    vp = _dev(values, "values", torch.float32) if values.numel() else None
+    st = load().som_bmu_sf_plan(rp, ci, vp, N, nnz, V, M, _dev(workspace, "workspace", torch.uint8), workspace.numel(),
+                                _cfg(tile_samples, keep_order), _stream(row_ptr))
+    _check(st, "som_bmu_sf_plan")
+
+
+def bmu_sf_sweep(W, norms, V: int, M: int, N: int, nnz: int, workspace, two_best: bool = False,
+                 tile_samples: int = 0, keep_order: bool = False):
+    fn, wp, name = _book(W, V, M, "som_bmu_sf_sweep")
+    st = fn(wp, _dev(norms, "norms", torch.float64, M), V, M, N, nnz, 1 if two_best else 0,
+            _dev(workspace, "workspace", torch.uint8), workspace.numel(), _cfg(tile_samples, keep_order), _stream(W))
+    _check(st, name)
+
+
+def bmu_sf_finalize(norms, row_ptr, V: int, M: int, nnz: int, out, workspace, tile_samples: int = 0,
+                    keep_order: bool = False):
+    """out = (bmu, dist) or (bmu, dist, bmu2, dist2) tensors, written."""
+    N = row_ptr.numel() - 1
+    b2 = _dev(out[2], "bmu2", torch.int32, N) if len(out) == 4 else None
+    d2 = _dev(out[3], "dist2", torch.float64, N) if len(out) == 4 else None
+    st = load().som_bmu_sf_finalize(
+        _dev(norms, "norms", torch.float64, M), V, M, _dev(row_ptr, "row_ptr", torch.int32, N + 1), N, nnz,
+        _dev(out[0], "bmu", torch.int32, N), _dev(out[1], "dist", torch.float64, N), b2, d2,
+        _dev(workspace, "workspace", torch.uint8), workspace.numel(), _cfg(tile_samples, keep_order), _stream(norms))
+    _check(st, "som_bmu_sf_finalize")

@@ -166,3 +166,46 @@ def compare2(W, row_ptr, col_idx, g, exact: bool, what="", rows=None, nthreads=1
         return oracle.distance_at(W[:, i], sub_ci[sub_rp[k]:sub_rp[k + 1]])
 
     return check_top2(gs, ref, dist_at, exact, what)
+
+
+def gpu_run_sf(W, row_ptr, col_idx, values, dev, two_best=True, tile_samples: int = 0, keep_order: bool = False):
+    """Norms + real-valued search on the GPU; returns numpy outputs (2 or 4 arrays)."""
+    Wd = W if isinstance(W, torch.Tensor) else to_dev(W, dev)
+    V, M = Wd.shape
+    rp = to_dev(np.asarray(row_ptr, dtype=np.int32), dev)
+    ci = to_dev(np.asarray(col_idx, dtype=np.int32), dev)
+    vs = to_dev(np.asarray(values, dtype=np.float32), dev)
+    N = rp.numel() - 1
+    nnz = int(row_ptr[-1]) - int(row_ptr[0])
+    norms = som.codebook_norms(Wd, V, M)
+    out = som.bmu_sf_search(Wd, norms, rp, ci, vs, V, M, nnz=nnz, two_best=two_best, tile_samples=tile_samples,
+                            keep_order=keep_order)
+    torch.cuda.synchronize()
+    return tuple(t.cpu().numpy() for t in out)
+
+
+def compare_sf(W, row_ptr, col_idx, values, g, exact: bool, what="", rows=None, nthreads=1):
+    """Real-valued oracle on the given rows against GPU outputs g (two-best form)."""
+    row_ptr = np.asarray(row_ptr, dtype=np.int32)
+    col_idx = np.asarray(col_idx, dtype=np.int32)
+    values = np.asarray(values, dtype=np.float32)
+    if rows is None:
+        rows = np.arange(len(row_ptr) - 1)
+    rows = np.asarray(rows)
+    sub_rp = np.zeros(len(rows) + 1, dtype=np.int32)
+    sub_rp[1:] = np.cumsum(row_ptr[rows + 1] - row_ptr[rows])
+    pick = [np.arange(row_ptr[r], row_ptr[r + 1]) for r in rows]
+    idx = np.concatenate(pick) if len(rows) else np.zeros(0, np.int64)
+    sub_ci, sub_v = col_idx[idx], values[idx]
+    M = W.shape[1]
+    if nthreads > 1:
+        ref = oracle.bmu_sf_streamed(lambda i0, i1: np.ascontiguousarray(W[:, i0:i1]), M, sub_rp, sub_ci, sub_v,
+                                     block=max(256, -(-M // nthreads)), nthreads=nthreads)
+    else:
+        ref = oracle.bmu_sf(W, sub_rp, sub_ci, sub_v)
+    gs = tuple(np.asarray(x)[rows] for x in g)
+
+    def dist_at(k, i):
+        return oracle.distance_sf_at(W[:, i], sub_ci[sub_rp[k]:sub_rp[k + 1]], sub_v[sub_rp[k]:sub_rp[k + 1]])
+
+    return check_top2(gs, ref, dist_at, exact, what)

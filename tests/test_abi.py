@@ -75,6 +75,25 @@ def test_f16_entry_points_check_alignment():
     assert lib.som_bmu_sweep(two, FAKE, 100, 64, 10, 50, FAKE, 100, None, None) == som.SOM_ERR_INVALID_ARG
 
 
+def test_real_valued_workspace_and_checks():
+    lib = som.load()
+    n2 = som.workspace2_bytes(10_000, 4096, 2000, 120_000)
+    nsf = som.workspace_sf_bytes(10_000, 4096, 2000, 120_000)
+    # per-entry values (8 per id), ||x||^2 per sample and the regrouped values on top of the two-best layout
+    assert nsf >= n2 + 32 * 120_000 + 8 * 10_000 + 4 * 120_000
+    assert lib.som_bmu_sf_workspace_bytes(10, 64, 100, 50, _cfg(16)) == 0  # tiles of 8 only
+    assert lib.som_bmu_sf_search(FAKE, FAKE, 100, 64, FAKE, FAKE, None, 10, 50, FAKE, FAKE, None, None, FAKE,
+                                 1 << 30, None, None) == som.SOM_ERR_INVALID_ARG  # no values
+    small2 = som.workspace2_bytes(10, 64, 100, 50)  # two-best room, but not the values
+    assert lib.som_bmu_sf_search(FAKE, FAKE, 100, 64, FAKE, FAKE, FAKE, 10, 50, FAKE, FAKE, None, None, FAKE, small2,
+                                 None, None) == som.SOM_ERR_WORKSPACE
+    assert lib.som_bmu_sf_plan(FAKE, FAKE, FAKE, 10, 50, 100, 64, FAKE, 1 << 30, _cfg(32),
+                               None) == som.SOM_ERR_INVALID_ARG
+    assert lib.som_bmu_sf_sweep(FAKE, FAKE, 100, 64, 10, 50, 1, FAKE, 100, None, None) == som.SOM_ERR_WORKSPACE
+    assert lib.som_bmu_sf_search(None, None, 100, 64, None, None, None, 0, 0, None, None, None, None, None, 0, None,
+                                 None) == som.SOM_OK
+
+
 def test_two_best_workspace_and_checks():
     lib = som.load()
     for tile, keep in ((0, False), (16, False), (32, True)):
