@@ -16,6 +16,11 @@ merged answer equals one oracle call over the whole map.
 ``bmu_sf`` ranks the same way for sparse real-valued rows (a value with each
 feature id; the Discussion's gather-multiply variant).
 
+``update`` performs one batch update of the codebook for binary rows (the
+factorised box-blur update: scatter, three running-sum box passes per
+lattice axis, quotient, zero-denominator units unchanged) in fp32 as the paper
+fixes it.
+
 ``bmu2`` returns the two best units per sample in the order (distance,
 index) -- the pair the paper's fused sweep produces (Figure 2 caption), which
 defines the topographic error -- plus the third distance, for margin checks.
@@ -66,6 +71,8 @@ def load(path: str | None = None):
     lib.som_bmu2_oracle_host.restype = ctypes.c_int
     lib.som_bmu_sf_oracle_host.argtypes = [vp, i64, i64, i64, i64, vp, vp, vp, i64, vp, vp, vp, vp, vp]
     lib.som_bmu_sf_oracle_host.restype = ctypes.c_int
+    lib.som_update_oracle_host.argtypes = [vp, i64, i64, vp, vp, i64, vp, i64, vp]
+    lib.som_update_oracle_host.restype = ctypes.c_int
     lib.som_norms_oracle_host.argtypes = [vp, i64, i64, i64, i64, vp]
     lib.som_norms_oracle_host.restype = ctypes.c_int
     return lib
@@ -183,6 +190,25 @@ def distance_sf_at(column: np.ndarray, ids: np.ndarray, vals: np.ndarray) -> flo
     col = np.ascontiguousarray(column, dtype=np.float32).reshape(-1, 1)
     rp = np.array([0, len(ids)], dtype=np.int32)
     return float(bmu_sf(col, rp, np.asarray(ids, dtype=np.int32), np.asarray(vals, dtype=np.float32))[1][0])
+
+
+def update(W: np.ndarray, E: int, row_ptr: np.ndarray, col_idx: np.ndarray, bmu: np.ndarray, radius: int, lib=None):
+    """One batch update of the V x (E*E) feature-major codebook W (binary rows, their best units); returns the new W."""
+    W = np.ascontiguousarray(W, dtype=np.float32)
+    V, M = W.shape
+    if M != E * E:
+        raise ValueError("W must have E*E columns")
+    row_ptr = np.ascontiguousarray(row_ptr, dtype=np.int32)
+    col_idx = np.ascontiguousarray(col_idx, dtype=np.int32)
+    bmu = np.ascontiguousarray(bmu, dtype=np.int32)
+    N = row_ptr.shape[0] - 1
+    out = np.empty_like(W)
+    rc = _lib(lib).som_update_oracle_host(W.ctypes.data, V, E, row_ptr.ctypes.data if N >= 0 else None,
+                                          col_idx.ctypes.data if col_idx.size else None, N,
+                                          bmu.ctypes.data if N else None, radius, out.ctypes.data)
+    if rc != OK:
+        raise ValueError(f"som_update_oracle_host returned {rc}")
+    return out
 
 
 def norms(W: np.ndarray, lib=None) -> np.ndarray:

@@ -15,6 +15,12 @@
  *     the two best units of every sample (the second feeds the topographic
  *     error). som_bmu2_oracle_host ranks units by (D_i, i) and returns the
  *     first two, plus the third distance for margin checks.
+ *   - Factorised box-blur section and Algorithm 2, steps 8-9: the batch update.
+ *     som_update_oracle_host scatters the batch onto the lattice (per unit, the
+ *     count of assigned samples and, per feature, of those holding it), blurs
+ *     both fields with three running-sum box passes along the rows and three
+ *     along the columns (clamped window, unnormalised, fp32 as the paper
+ *     fixes), and divides, leaving units with a zero denominator unchanged.
  *   - Discussion, sparse real-valued inputs: som_bmu_sf_oracle_host takes a
  *     value with every feature id (x_v real instead of 1) and ranks the same
  *     squared distance.
@@ -224,4 +230,84 @@ int som_norms_oracle_host(const float *W, int64_t ldw, int64_t V, int64_t i0, in
         }
     }
     return SOM_ORACLE_OK;
+}
+
+/* ------------------------------------------------------------------ update */
+
+/* One box pass over n values of a lattice line (stride apart), half-width r,
+ * clamped: out[i] = sum of line[j] for |j - i| <= r, 0 <= j < n, kept as a
+ * running window sum in fp32 -- the window's first sum in ascending j, then per
+ * step the element entering is added and the one leaving subtracted. */
+static void box_pass(float *line, int64_t n, int64_t stride, int64_t r, float *tmp)
+{
+    float s = 0.0f;
+    for (int64_t j = 0; j <= r && j < n; ++j) s += line[j * stride];
+    tmp[0] = s;
+    for (int64_t i = 1; i < n; ++i) {
+        if (i + r < n) s += line[(i + r) * stride];
+        if (i - r - 1 >= 0) s -= line[(i - r - 1) * stride];
+        tmp[i] = s;
+    }
+    for (int64_t i = 0; i < n; ++i) line[i * stride] = tmp[i];
+}
+
+/* Three passes along every lattice row, then three along every lattice column. */
+static void blur_field(float *f, int64_t E, int64_t r, float *tmp)
+{
+    for (int64_t row = 0; row < E; ++row)
+        for (int pass = 0; pass < 3; ++pass) box_pass(f + row * E, E, 1, r, tmp);
+    for (int64_t col = 0; col < E; ++col)
+        for (int pass = 0; pass < 3; ++pass) box_pass(f + col, E, E, r, tmp);
+}
+
+int som_update_oracle_host(const float *W_in, int64_t V, int64_t E, const int32_t *row_ptr, const int32_t *col_idx,
+                           int64_t N, const int32_t *bmu, int64_t radius, float *W_out)
+{
+    if (!W_in || !W_out || V < 1 || E < 1 || N < 0 || radius < 1 || (N > 0 && (!row_ptr || !bmu)))
+        return SOM_ORACLE_BAD_ARG;
+    const int64_t M = E * E;
+    for (int64_t s = 0; s < N; ++s) {
+        if (row_ptr[s + 1] < row_ptr[s]) return SOM_ORACLE_BAD_CSR;
+        if (bmu[s] < 0 || bmu[s] >= M) return SOM_ORACLE_BAD_ARG;
+    }
+    if (N > 0 && row_ptr[N] > row_ptr[0] && !col_idx) return SOM_ORACLE_BAD_ARG;
+
+    int64_t *cnt = (int64_t *)calloc((size_t)M, sizeof(int64_t));
+    float *den = (float *)malloc((size_t)M * sizeof(float));
+    float *num = (float *)malloc((size_t)M * sizeof(float));
+    float *tmp = (float *)malloc((size_t)E * sizeof(float));
+    int rc = SOM_ORACLE_OK;
+    if (!cnt || !den || !num || !tmp) {
+        rc = SOM_ORACLE_NO_MEM;
+        goto done;
+    }
+
+    /* den: samples per unit (Algorithm 2, step 8), blurred */
+    for (int64_t s = 0; s < N; ++s) cnt[bmu[s]] += 1;
+    for (int64_t i = 0; i < M; ++i) den[i] = (float)cnt[i];
+    blur_field(den, E, radius, tmp);
+
+    /* num, one feature at a time: samples per unit holding feature v (x binary) */
+    for (int64_t v = 0; v < V; ++v) {
+        for (int64_t i = 0; i < M; ++i) cnt[i] = 0;
+        for (int64_t s = 0; s < N; ++s)
+            for (int64_t p = row_ptr[s]; p < row_ptr[s + 1]; ++p) {
+                if (col_idx[p] < 0 || col_idx[p] >= V) {
+                    rc = SOM_ORACLE_BAD_CSR;
+                    goto done;
+                }
+                if (col_idx[p] == v) cnt[bmu[s]] += 1;
+            }
+        for (int64_t i = 0; i < M; ++i) num[i] = (float)cnt[i];
+        blur_field(num, E, radius, tmp);
+        /* the prototype becomes the neighbourhood mean; a unit whose blurred
+         * denominator is zero keeps its prototype */
+        for (int64_t i = 0; i < M; ++i) W_out[v * M + i] = den[i] > 0.0f ? num[i] / den[i] : W_in[v * M + i];
+    }
+done:
+    free(cnt);
+    free(den);
+    free(num);
+    free(tmp);
+    return rc;
 }

@@ -75,6 +75,24 @@ int som_bmu_sf_oracle_host(const float *W, int64_t ldw, int64_t V, int64_t i0, i
                            int32_t *bmu2, double *dist2, double *dist3);
 
 /*
+ * One batch-SOM update for binary rows (Algorithm 2, steps 8-9; the factorised
+ * box-blur update section), on an E x E lattice, neuron i = row*E + col,
+ * feature-major codebook W[v*M + i] with M = E*E.
+ *   bmu     host int32[N], the best unit of every sample (from a search).
+ *   radius  box half-width r >= 1 (the schedule's sigma rounded to whole cells,
+ *           at least one).
+ *   W_out   host float[V*M]: num/den where the blurred den > 0, else W_in.
+ * num[v][i] = number of samples at unit i holding feature v, den[i] = number of
+ * samples at unit i, both converted to fp32, then blurred: three box passes
+ * along every lattice row, then three along every lattice column, each pass a
+ * running window sum over the clamped window (first window summed in ascending
+ * order, then add the element entering, subtract the one leaving), unnormalised,
+ * in fp32; the quotient is an fp32 division. Plain loops, one thread.
+ */
+int som_update_oracle_host(const float *W_in, int64_t V, int64_t E, const int32_t *row_ptr, const int32_t *col_idx,
+                           int64_t N, const int32_t *bmu, int64_t radius, float *W_out);
+
+/*
  * Per-neuron squared norms n_i = sum_v w_{v,i}^2 in fp64, v ascending, for
  * i in [i0, i1): norms[i - i0]. Same W layout as above.
  */

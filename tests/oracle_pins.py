@@ -372,6 +372,78 @@ def check_sf_cdist_and_planted(lib):
     assert np.array_equal(r2[1], 4 * d1) and np.array_equal(r2[3], 4 * d2)
 
 
+# ----------------------------------------------------------- batch update
+
+def box3_direct(field, r, axis):
+    """Three clamped, unnormalised box passes of half-width r along one axis, by direct window sums in int64."""
+    f = np.asarray(field, dtype=np.int64)
+    n = f.shape[axis]
+    for _ in range(3):
+        c = np.cumsum(f, axis=axis)
+        c = np.concatenate([np.zeros_like(np.take(c, [0], axis=axis)), c], axis=axis)  # c[k] = sum of the first k
+        hi = np.minimum(np.arange(n) + r + 1, n)
+        lo = np.maximum(np.arange(n) - r, 0)
+        f = np.take(c, hi, axis=axis) - np.take(c, lo, axis=axis)
+    return f
+
+
+def update_direct(W, E, rp, ci, bmu, r):
+    """The update by its definition, in exact integers: counts, direct window sums (rows, then columns), fp32 quotient."""
+    V, M = W.shape
+    den = np.bincount(bmu, minlength=M).reshape(E, E)
+    num = np.zeros((V, E, E), dtype=np.int64)
+    for s in range(len(bmu)):
+        for v in ci[rp[s]:rp[s + 1]]:
+            num[v, bmu[s] // E, bmu[s] % E] += 1
+    den_b = box3_direct(box3_direct(den, r, 1), r, 0)
+    num_b = box3_direct(box3_direct(num, r, 2), r, 1)
+    assert den_b.max() < 2 ** 24 and num_b.max() < 2 ** 24  # every partial sum exact in fp32 too
+    q = num_b.astype(np.float32) / np.maximum(den_b, 1).astype(np.float32)[None]
+    return np.where(den_b[None] > 0, q, W.reshape(V, E, E)).reshape(V, M)
+
+
+def check_update_direct_windows(lib):
+    """Integer counts small enough for exact fp32: the running-sum blur equals direct window sums, for several radii;
+    units without a sample in reach keep their prototype."""
+    E, V, N = 9, 24, 40
+    rp, ci = synth.make_csr(29, N, V)
+    W = synth.codebook(29, synth.UNIFORM, V, E * E)
+    rng = np.random.default_rng(29)
+    bmu = rng.integers(0, E * E // 3, N).astype(np.int32)  # the lower third of the lattice only
+    for r in (1, 2, 4):
+        got = oracle.update(W, E, rp, ci, bmu, r, lib=lib)
+        ref = update_direct(W, E, rp, ci, bmu, r)
+        assert np.array_equal(got, ref), f"radius {r}"
+    got = oracle.update(W, E, rp, ci, bmu, 1, lib=lib)
+    assert np.array_equal(got[:, -E:], W[:, -E:]), "units out of reach must keep their prototype"
+
+
+def check_update_impulse_and_pair(lib):
+    """One sample: its unit's neighbourhood becomes exactly its input (1 on its features, 0 elsewhere), the clamped
+    support (3r cells per axis, no wrap) ends at the lattice edge. Two samples with disjoint features: the new
+    prototype is each one's kernel weight over the sum."""
+    E, V = 12, 10
+    W = synth.codebook(30, synth.UNIFORM, V, E * E)
+    rp = np.array([0, 3], dtype=np.int32)
+    ci = np.array([1, 4, 7], dtype=np.int32)
+    r = 1
+    got = oracle.update(W, E, rp, ci, np.array([0], dtype=np.int32), r, lib=lib).reshape(V, E, E)
+    reach = np.zeros((E, E), dtype=bool)
+    reach[:3 * r + 1, :3 * r + 1] = True  # corner unit: support [0, 3r] on both axes
+    for v in range(V):
+        want = 1.0 if v in (1, 4, 7) else 0.0
+        assert (got[v][reach] == want).all()
+        assert np.array_equal(got[v][~reach], W.reshape(V, E, E)[v][~reach])
+    rp2 = np.array([0, 2, 4], dtype=np.int32)
+    ci2 = np.array([0, 2, 5, 9], dtype=np.int32)
+    bmu2 = np.array([E + 1, 3 * E + 5], dtype=np.int32)  # units (1,1) and (3,5)
+    got2 = oracle.update(W, E, rp2, ci2, bmu2, 2, lib=lib)
+    ref2 = update_direct(W, E, rp2, ci2, bmu2, 2)
+    assert np.array_equal(got2, ref2)
+    k1 = update_direct(W, E, rp2[:2], ci2[:2], bmu2[:1], 2)[0]  # sample 1 alone: weight-1 field on feature 0
+    assert np.allclose(got2[0][k1 == 1.0] + got2[5][k1 == 1.0], 1.0, rtol=0, atol=1e-6)
+
+
 ALL_CHECKS = [
     check_exact_integer_direct,
     check_cdist_node_major,
@@ -392,4 +464,6 @@ ALL_CHECKS = [
     check_sf_exact_integer,
     check_sf_binary_values_reduce,
     check_sf_cdist_and_planted,
+    check_update_direct_windows,
+    check_update_impulse_and_pair,
 ]

@@ -47,6 +47,14 @@ MUTANTS = [
     ("rank3_ignored", "} else if (r3 < 0 || D[k] < D[r3]) {", "} else if (r3 < 0) {"),
     ("sf_value_ignored", "x[v] = (double)values[p];", "x[v] = 1.0;"),
     ("sf_value_squared", "x[v] = (double)values[p];", "x[v] = (double)values[p] * (double)values[p];"),
+    ("box_window_off_by_one", "if (i - r - 1 >= 0) s -= line[(i - r - 1) * stride];",
+     "if (i - r >= 0) s -= line[(i - r) * stride];"),
+    ("zero_den_filled", "? num[i] / den[i] : W_in[v * M + i];", "? num[i] / den[i] : 0.0f;"),
+    ("two_row_passes", "for (int pass = 0; pass < 3; ++pass) box_pass(f + row * E, E, 1, r, tmp);",
+     "for (int pass = 0; pass < 2; ++pass) box_pass(f + row * E, E, 1, r, tmp);"),
+    ("columns_skipped", "for (int pass = 0; pass < 3; ++pass) box_pass(f + col, E, E, r, tmp);",
+     "for (int pass = 0; pass < 0; ++pass) box_pass(f + col, E, E, r, tmp);"),
+    ("den_not_blurred", "    blur_field(den, E, radius, tmp);\n", "\n"),
     ("sf_rank2_tie_highest_index", "} else if (q2 < 0 || D[k] < D[q2]) {", "} else if (q2 < 0 || D[k] <= D[q2]) {"),
 ]
 
