@@ -291,6 +291,44 @@ som_status som_bmu_sf_finalize(const double *norms, int64_t V, int64_t M, const 
                                size_t workspace_bytes, const som_bmu_config *config, void *stream);
 
 /*
+ * The batch-SOM update for binary rows (Algorithm 2, steps 8-9; the factorised
+ * box-blur update section), in place on the codebook W (fp32, or binary16 for
+ * som_update_f16), lattice E x E with neuron i = row*E + col (M = E*E).
+ *   bmu             device int32 [N]: each sample's best unit (from a search on
+ *                   the same batch; values outside [0, M) are skipped).
+ *   radius          box half-width r >= 1: som_radius(som_sigma(epoch, ...)).
+ *   chunk_features  features blurred per pass (0 = all V); the workspace holds
+ *                   three chunk x M fields, so smaller chunks need less memory.
+ * Per unit, den = samples assigned to it and num[v] = those holding feature v
+ * (exact integer counts), both converted to fp32 and blurred by three
+ * running-sum box passes along every lattice row and then three along every
+ * column, each over the clamped window [k-r, k+r] and unnormalised (the paper's
+ * four rules: unnormalised sums, clamped boundary, a unit whose blurred den is
+ * zero keeps its prototype, fp32 accumulation with the binary16 conversion only
+ * at the final write). W = num / den. The passes run in a fixed order, so the
+ * result is the same bits on every run. Norms must be recomputed afterwards.
+ */
+size_t som_update_workspace_bytes(int64_t V, int64_t E, int64_t chunk_features);
+
+som_status som_update(float *W, int64_t V, int64_t E, const int32_t *row_ptr, const int32_t *col_idx, int64_t N,
+                      int64_t nnz, const int32_t *bmu, int32_t radius, int64_t chunk_features, void *workspace,
+                      size_t workspace_bytes, void *stream);
+
+som_status som_update_f16(uint16_t *W, int64_t V, int64_t E, const int32_t *row_ptr, const int32_t *col_idx, int64_t N,
+                          int64_t nnz, const int32_t *bmu, int32_t radius, int64_t chunk_features, void *workspace,
+                          size_t workspace_bytes, void *stream);
+
+/*
+ * The neighbourhood schedule (factorised box-blur section: an exponential
+ * endpoint schedule from sigma0 = 0.5*E towards sigma_min, rate 0.3), read as
+ * sigma(e) = sigma_min + (sigma0 - sigma_min) * exp(-rate * (e - 1)) for epochs
+ * e = 1, 2, ... (e < 1 is taken as 1), and the box half-width it gives: sigma
+ * rounded to the nearest whole cell (halves up), never below 1. Host functions.
+ */
+double som_sigma(int32_t epoch, double sigma0, double sigma_min, double rate);
+int32_t som_radius(double sigma);
+
+/*
  * Input flags (SOM_FLAG_*) the last plan on this workspace recorded. Waits
  * for `stream`, then copies one word to *flags (host). 0 means the device
  * saw a valid CSR.

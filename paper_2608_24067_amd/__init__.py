@@ -25,6 +25,10 @@ from .som import (  # noqa: F401
     last_error,
     library_path,
     load,
+    radius,
+    sigma,
+    update,
+    update_workspace_bytes,
     validate_csr_host,
     workspace2_bytes,
     workspace_sf_bytes,

@@ -5,6 +5,7 @@
 
 #include <cstdarg>
 #include <cstdio>
+#include <cmath>
 #include <cstring>
 
 #include "../../include/som.h"
@@ -457,6 +458,79 @@ som_status som_bmu_input_flags(const void *workspace, size_t workspace_bytes, in
     e = hipMemcpy(flags, c.flags, sizeof(uint32_t), hipMemcpyDeviceToHost);
     if (e != hipSuccess) return hip_fail(e, "som_bmu_input_flags: copy");
     return ok();
+}
+
+size_t som_update_workspace_bytes(int64_t V, int64_t E, int64_t chunk_features)
+{
+    if (V < 1 || V >= INT32_MAX || E < 1 || E * E > SOM_MAX_NEURONS || chunk_features < 0) return 0;
+    const int64_t chunk = chunk_features == 0 || chunk_features > V ? V : chunk_features;
+    return som::update_layout(E * E, chunk).total;
+}
+
+static som_status update_impl(const Book &b, void *W, int64_t V, int64_t E, const int32_t *row_ptr,
+                              const int32_t *col_idx, int64_t N, int64_t nnz, const int32_t *bmu, int32_t radius,
+                              int64_t chunk_features, void *workspace, size_t workspace_bytes, void *stream,
+                              const char *who)
+{
+    if (!W) return fail(SOM_ERR_INVALID_ARG, "%s: W is NULL", who);
+    if (V < 1 || V >= INT32_MAX || E < 1 || E * E > SOM_MAX_NEURONS)
+        return fail(SOM_ERR_INVALID_ARG, "%s: need 1 <= V < 2^31-1 and 1 <= E*E <= %d", who, SOM_MAX_NEURONS);
+    if (N < 0 || N >= INT32_MAX || nnz < 0 || nnz > INT32_MAX)
+        return fail(SOM_ERR_INVALID_ARG, "%s: N or nnz out of range", who);
+    if (radius < 1) return fail(SOM_ERR_INVALID_ARG, "%s: radius must be >= 1 (got %d)", who, (int)radius);
+    if (chunk_features < 0) return fail(SOM_ERR_INVALID_ARG, "%s: chunk_features must be >= 0", who);
+    if (N > 0 && (!row_ptr || !bmu || (nnz > 0 && !col_idx))) return fail(SOM_ERR_INVALID_ARG, "%s: null pointer", who);
+    som_status st = check_book(b, who);
+    if (st != SOM_OK) return st;
+    const int64_t M = E * E;
+    const int64_t chunk = chunk_features == 0 || chunk_features > V ? V : chunk_features;
+    const som::UpdateLayout L = som::update_layout(M, chunk);
+    if (!workspace) return fail(SOM_ERR_WORKSPACE, "%s: workspace is NULL", who);
+    if (reinterpret_cast<uintptr_t>(workspace) & 255) return fail(SOM_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+    if (workspace_bytes < L.total)
+        return fail(SOM_ERR_WORKSPACE, "%s: workspace holds %zu bytes, the update needs %zu", who, workspace_bytes,
+                    L.total);
+    char *w = static_cast<char *>(workspace);
+    som::UpdateBuffers ub;
+    ub.den_cnt = reinterpret_cast<int32_t *>(w + L.den_cnt);
+    ub.den_a = reinterpret_cast<float *>(w + L.den_a);
+    ub.den_b = reinterpret_cast<float *>(w + L.den_b);
+    ub.cnt = reinterpret_cast<int32_t *>(w + L.cnt);
+    ub.a = reinterpret_cast<float *>(w + L.a);
+    ub.b = reinterpret_cast<float *>(w + L.b);
+    hipError_t e = som::launch_update(b.f16, W, V, E, row_ptr, col_idx, N, nnz, bmu, radius, chunk, ub,
+                                      static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, who);
+    return ok();
+}
+
+som_status som_update(float *W, int64_t V, int64_t E, const int32_t *row_ptr, const int32_t *col_idx, int64_t N,
+                      int64_t nnz, const int32_t *bmu, int32_t radius, int64_t chunk_features, void *workspace,
+                      size_t workspace_bytes, void *stream)
+{
+    return update_impl(Book{W, false}, W, V, E, row_ptr, col_idx, N, nnz, bmu, radius, chunk_features, workspace,
+                       workspace_bytes, stream, "som_update");
+}
+
+som_status som_update_f16(uint16_t *W, int64_t V, int64_t E, const int32_t *row_ptr, const int32_t *col_idx, int64_t N,
+                          int64_t nnz, const int32_t *bmu, int32_t radius, int64_t chunk_features, void *workspace,
+                          size_t workspace_bytes, void *stream)
+{
+    return update_impl(Book{W, true}, W, V, E, row_ptr, col_idx, N, nnz, bmu, radius, chunk_features, workspace,
+                       workspace_bytes, stream, "som_update_f16");
+}
+
+double som_sigma(int32_t epoch, double sigma0, double sigma_min, double rate)
+{
+    if (epoch < 1) epoch = 1;
+    return sigma_min + (sigma0 - sigma_min) * exp(-rate * (double)(epoch - 1));
+}
+
+int32_t som_radius(double sigma)
+{
+    if (!(sigma >= 1.0)) return 1;  // also NaN
+    const double r = floor(sigma + 0.5);
+    return r > (double)INT32_MAX ? INT32_MAX : (int32_t)r;
 }
 
 som_status som_validate_csr_host(const int32_t *row_ptr, const int32_t *col_idx, int64_t N, int64_t V)

@@ -115,4 +115,44 @@ hipError_t launch_finalize(int ta, const double *norms, int64_t M, const int32_t
 hipError_t launch_order(const int32_t *row_ptr, const int32_t *col_idx, const float *values, int64_t N, int64_t nnz,
                         int64_t V, const OrderBuffers &ob, uint32_t *flags, hipStream_t st);
 
+// ----------------------------------------------------------------- update
+
+// Workspace of the batch update (som_update.hip): the den field (counts and two
+// float buffers, M each) and, for one chunk of features, counts and two float
+// buffers of chunk * M.
+struct UpdateBuffers {
+    int32_t *den_cnt;
+    float *den_a, *den_b;
+    int32_t *cnt;
+    float *a, *b;
+};
+
+struct UpdateLayout {
+    size_t den_cnt, den_a, den_b, cnt, a, b, total;
+};
+
+inline UpdateLayout update_layout(int64_t M, int64_t chunk)
+{
+    UpdateLayout L;
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        const size_t at = off;
+        off += align256(bytes);
+        return at;
+    };
+    L.den_cnt = take((size_t)M * 4);
+    L.den_a = take((size_t)M * 4);
+    L.den_b = take((size_t)M * 4);
+    L.cnt = take((size_t)chunk * (size_t)M * 4);
+    L.a = take((size_t)chunk * (size_t)M * 4);
+    L.b = take((size_t)chunk * (size_t)M * 4);
+    L.total = off;
+    return L;
+}
+
+// f16: W holds binary16 values. radius >= 1; chunk >= 1 features per pass.
+hipError_t launch_update(bool f16, void *W, int64_t V, int64_t E, const int32_t *row_ptr, const int32_t *col_idx,
+                         int64_t N, int64_t nnz, const int32_t *bmu, int64_t radius, int64_t chunk,
+                         const UpdateBuffers &ub, hipStream_t st);
+
 }  // namespace som

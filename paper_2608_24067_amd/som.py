@@ -27,7 +27,8 @@ EXPORTS = (
     "som_bmu_finalize", "som_bmu2_workspace_bytes", "som_bmu2_search", "som_bmu2_sweep", "som_bmu2_finalize",
     "som_codebook_norms_f16", "som_bmu_search_f16", "som_bmu_sweep_f16", "som_bmu2_search_f16", "som_bmu2_sweep_f16",
     "som_bmu_sf_workspace_bytes", "som_bmu_sf_search", "som_bmu_sf_search_f16", "som_bmu_sf_plan", "som_bmu_sf_sweep",
-    "som_bmu_sf_sweep_f16", "som_bmu_sf_finalize", "som_bmu_input_flags",
+    "som_bmu_sf_sweep_f16", "som_bmu_sf_finalize", "som_update_workspace_bytes", "som_update", "som_update_f16",
+    "som_sigma", "som_radius", "som_bmu_input_flags",
     "som_validate_csr_host", "som_last_error",
 )
 
@@ -87,6 +88,16 @@ def load():
     for name in ("som_bmu_sf_search", "som_bmu_sf_search_f16", "som_bmu_sf_plan", "som_bmu_sf_sweep",
                  "som_bmu_sf_sweep_f16", "som_bmu_sf_finalize"):
         getattr(lib, name).restype = ctypes.c_int
+    lib.som_update_workspace_bytes.argtypes = [i64, i64, i64]
+    lib.som_update_workspace_bytes.restype = sz
+    lib.som_update.argtypes = [vp, i64, i64, vp, vp, i64, i64, vp, i32, i64, vp, sz, vp]
+    lib.som_update.restype = ctypes.c_int
+    lib.som_update_f16.argtypes = lib.som_update.argtypes
+    lib.som_update_f16.restype = ctypes.c_int
+    lib.som_sigma.argtypes = [i32, ctypes.c_double, ctypes.c_double, ctypes.c_double]
+    lib.som_sigma.restype = ctypes.c_double
+    lib.som_radius.argtypes = [ctypes.c_double]
+    lib.som_radius.restype = ctypes.c_int32
     lib.som_bmu_input_flags.argtypes = [vp, sz, i64, i64, i64, i64, cfgp, ctypes.POINTER(ctypes.c_uint32), vp]
     lib.som_validate_csr_host.argtypes = [vp, vp, i64, i64]
     for name in ("som_codebook_norms", "som_bmu_search", "som_bmu_plan", "som_bmu_sweep", "som_bmu_finalize",
@@ -374,3 +385,39 @@ def bmu_sf_finalize(norms, row_ptr, V: int, M: int, nnz: int, out, workspace, ti
         _dev(out[0], "bmu", torch.int32, N), _dev(out[1], "dist", torch.float64, N), b2, d2,
         _dev(workspace, "workspace", torch.uint8), workspace.numel(), _cfg(tile_samples, keep_order), _stream(norms))
     _check(st, "som_bmu_sf_finalize")
+
+
+# ------------------------------------------------------------------- batch update
+
+def update_workspace_bytes(V: int, E: int, chunk_features: int = 0) -> int:
+    n = load().som_update_workspace_bytes(V, E, chunk_features)
+    if n == 0:
+        raise ValueError("som_update_workspace_bytes: invalid sizes")
+    return n
+
+
+def update(W, row_ptr, col_idx, bmu, V: int, E: int, radius: int, nnz: int | None = None, chunk_features: int = 0,
+           workspace=None):
+    """One batch update of the feature-major V x E*E codebook W in place (float32 or float16); returns W."""
+    N = row_ptr.numel() - 1
+    nnz = _nnz(row_ptr, N, nnz)
+    if not isinstance(W, torch.Tensor) or W.numel() != V * E * E:
+        raise ValueError("W must be a tensor of V*E*E elements")
+    if workspace is None:
+        workspace = torch.empty(update_workspace_bytes(V, E, chunk_features), dtype=torch.uint8, device=W.device)
+    f16 = W.dtype == torch.float16
+    wp = _dev(W, "W", torch.float16 if f16 else torch.float32)
+    rp, ci = _csr(row_ptr, col_idx, N, nnz)
+    fn = load().som_update_f16 if f16 else load().som_update
+    st = fn(wp, V, E, rp, ci, N, nnz, _dev(bmu, "bmu", torch.int32, N), int(radius), chunk_features,
+            _dev(workspace, "workspace", torch.uint8), workspace.numel(), _stream(W))
+    _check(st, "som_update_f16" if f16 else "som_update")
+    return W
+
+
+def sigma(epoch: int, sigma0: float, sigma_min: float, rate: float = 0.3) -> float:
+    return float(load().som_sigma(epoch, sigma0, sigma_min, rate))
+
+
+def radius(sigma_value: float) -> int:
+    return int(load().som_radius(sigma_value))

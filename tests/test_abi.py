@@ -94,6 +94,29 @@ def test_real_valued_workspace_and_checks():
                                  None) == som.SOM_OK
 
 
+def test_schedule_and_radius():
+    assert som.sigma(1, 512.0, 0.5) == 512.0
+    vals = [som.sigma(e, 512.0, 0.5) for e in range(1, 60)]
+    assert all(a > b for a, b in zip(vals, vals[1:])) and abs(vals[-1] - 0.5) < 1e-3
+    assert abs(som.sigma(3, 32.0, 0.5, 0.3) - (0.5 + 31.5 * np.exp(-0.6))) < 1e-12
+    assert som.sigma(0, 10.0, 1.0) == 10.0  # epochs below 1 count as the first
+    assert [som.radius(x) for x in (0.0, 0.4, 1.0, 1.49, 1.5, 2.5, 512.3, float("nan"))] == [1, 1, 1, 1, 2, 3, 512, 1]
+
+
+def test_update_workspace_and_checks():
+    lib = som.load()
+    full = som.update_workspace_bytes(300, 16)
+    part = som.update_workspace_bytes(300, 16, 10)
+    assert full > part > 0 and full >= 3 * 300 * 256 * 4
+    assert lib.som_update_workspace_bytes(0, 16, 0) == 0
+    assert lib.som_update_workspace_bytes(10, 1025, 0) == 0  # E*E beyond 2^20
+    assert lib.som_update(FAKE, 300, 16, FAKE, FAKE, 10, 50, FAKE, 0, 0, FAKE, 1 << 30, None) == som.SOM_ERR_INVALID_ARG
+    assert lib.som_update(FAKE, 300, 16, FAKE, FAKE, 10, 50, None, 1, 0, FAKE, 1 << 30, None) == som.SOM_ERR_INVALID_ARG
+    assert lib.som_update(FAKE, 300, 16, FAKE, FAKE, 10, 50, FAKE, 1, 0, FAKE, part, None) == som.SOM_ERR_WORKSPACE
+    odd = ctypes.c_void_p((1 << 20) + 1)
+    assert lib.som_update_f16(odd, 300, 16, FAKE, FAKE, 10, 50, FAKE, 1, 0, FAKE, 1 << 30, None) == som.SOM_ERR_INVALID_ARG
+
+
 def test_two_best_workspace_and_checks():
     lib = som.load()
     for tile, keep in ((0, False), (16, False), (32, True)):

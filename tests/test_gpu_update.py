@@ -1,0 +1,95 @@
+"""GPU parity of the batch update (som_update, som_update_f16) against the update oracle.
+
+The oracle runs the paper's steps in their order and precision (integer
+counts, fp32 running-sum box passes along rows then columns, fp32 quotient),
+and the kernels run the same operations in the same order, so the new
+codebook must agree bit for bit -- also where the blurred sums exceed 2^24
+and fp32 rounds. An fp16 codebook gets the fp32 quotient rounded once.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2608_24067_amd.som as som
+import synth
+from parity import to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+def update_case(seed, N, V, E, kind=synth.UNIFORM, spread=1.0):
+    rp, ci = synth.make_csr(seed, N, V)
+    W = synth.codebook(seed, kind, V, E * E)
+    rng = np.random.default_rng(seed)
+    bmu = rng.integers(0, max(1, int(E * E * spread)), N).astype(np.int32)
+    return rp, ci, W, bmu
+
+
+def gpu_update(W, rp, ci, bmu, E, r, dev, chunk=0):
+    V = W.shape[0]
+    Wd = to_dev(W, dev)
+    som.update(Wd, to_dev(rp, dev), to_dev(ci, dev), to_dev(bmu, dev), V, E, r, nnz=int(rp[-1] - rp[0]),
+               chunk_features=chunk)
+    torch.cuda.synchronize()
+    return Wd.cpu().numpy()
+
+
+@pytest.mark.parametrize("seed,N,V,E,r,chunk,spread", [
+    (91, 300, 40, 9, 1, 0, 1.0),
+    (92, 2000, 300, 16, 2, 0, 1.0),
+    (93, 2000, 300, 16, 5, 7, 0.3),    # a third of the lattice holds every sample: zero-den units stay
+    (94, 500, 120, 12, 1, 1, 0.1),
+    (95, 30000, 500, 64, 32, 64, 1.0),  # sums far beyond 2^24: fp32 rounding, same order on both sides
+    (96, 5000, 2000, 32, 16, 0, 1.0),
+    (97, 1, 30, 5, 3, 0, 1.0),         # one sample
+    (98, 400, 64, 1, 1, 0, 1.0),       # a one-unit map
+])
+def test_update_bit_exact(dev, seed, N, V, E, r, chunk, spread):
+    rp, ci, W, bmu = update_case(seed, N, V, E, spread=spread)
+    got = gpu_update(W, rp, ci, bmu, E, r, dev, chunk)
+    ref = oracle.update(W, E, rp, ci, bmu, r)
+    bad = np.flatnonzero(got != ref)
+    assert bad.size == 0, f"{bad.size} weights differ, first {bad[:5]}: {got.reshape(-1)[bad[:5]]} vs {ref.reshape(-1)[bad[:5]]}"
+
+
+def test_update_f16(dev):
+    rp, ci, W, bmu = update_case(99, 3000, 400, 24, spread=0.5)
+    W16 = W.astype(np.float16)
+    got = gpu_update(W16, rp, ci, bmu, 24, 3, dev, chunk=50)
+    ref = oracle.update(W16.astype(np.float32), 24, rp, ci, bmu, 3)
+    assert np.array_equal(got, ref.astype(np.float16))
+
+
+def test_update_repeatable_and_chunk_invariant(dev):
+    rp, ci, W, bmu = update_case(100, 8000, 700, 32, spread=1.0)
+    a = gpu_update(W, rp, ci, bmu, 32, 9, dev, chunk=0)
+    b = gpu_update(W, rp, ci, bmu, 32, 9, dev, chunk=33)
+    c = gpu_update(W, rp, ci, bmu, 32, 9, dev, chunk=0)
+    assert np.array_equal(a, b) and np.array_equal(a, c)
+
+
+def test_one_epoch_on_the_tiny_workload(dev):
+    # search -> update -> norms -> search, against the oracle chain
+    cfg = synth.CONFIGS["tiny"]
+    rp, ci = synth.make_csr(cfg.seed, cfg.N, cfg.V)
+    W = synth.codebook(cfg.seed, cfg.kind, cfg.V, cfg.M)
+    r = som.radius(som.sigma(1, 0.5 * cfg.edge, 0.5))
+    Wd, rpd, cid = to_dev(W, dev), to_dev(rp, dev), to_dev(ci, dev)
+    norms = som.codebook_norms(Wd, cfg.V, cfg.M)
+    b, _ = som.bmu_search(Wd, norms, rpd, cid, cfg.V, cfg.M)
+    som.update(Wd, rpd, cid, b, cfg.V, cfg.edge, r)
+    norms = som.codebook_norms(Wd, cfg.V, cfg.M)
+    b2, d2 = som.bmu_search(Wd, norms, rpd, cid, cfg.V, cfg.M)
+    torch.cuda.synchronize()
+    b_ref, _, _ = oracle.bmu(W, rp, ci)
+    assert np.array_equal(b.cpu().numpy(), b_ref)
+    W1 = oracle.update(W, cfg.edge, rp, ci, b_ref, r)
+    assert np.array_equal(Wd.cpu().numpy(), W1)
+    b2_ref, d2_ref, dd2_ref = oracle.bmu(W1, rp, ci)
+    from parity import check_margin_rule
+
+    def dist_at(k, i):
+        return oracle.distance_at(W1[:, i], ci[rp[k]:rp[k + 1]])
+
+    check_margin_rule(b2.cpu().numpy(), d2.cpu().numpy(), b2_ref, d2_ref, dd2_ref, dist_at, what="epoch 2")
