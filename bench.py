@@ -117,11 +117,16 @@ def main():
                     help="codebook storage: fp32 (the workloads' own) or fp16 (rounded from it; fp32 accumulation)")
     ap.add_argument("--values", action="store_true",
                     help="sparse real-valued rows: a U(0,1] value with every id (the gather-multiply variant)")
+    ap.add_argument("--epoch", action="store_true",
+                    help="time one whole batch-SOM epoch: the two-best search plus the batch update (first-epoch radius)")
+    ap.add_argument("--update-chunk-gb", type=float, default=16.0, help="workspace budget of the update, GB")
     ap.add_argument("--top2", action="store_true",
                     help="time the two-best search (som_bmu2_*) instead of the single-best one")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="first run one plain 1 GiB device-to-device copy, the reference for HBM byte counters")
     args = ap.parse_args()
+    if args.epoch:
+        args.top2 = True
 
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; multi-GPU sharding is designed, not built "
@@ -186,7 +191,12 @@ def main():
         del src, dst
         log("calibration copy: 1073741824 bytes read, 1073741824 bytes written")
 
-    phases = ("norms", "plan", "sweep", "finalize")
+    if args.epoch:
+        r_epoch = som.radius(som.sigma(1, 0.5 * cfg.edge, 0.5))
+        chunk = int(max(1, min(V, args.update_chunk_gb * 1e9 / (12.0 * M))))
+        uws = torch.empty(som.update_workspace_bytes(V, cfg.edge, chunk), dtype=torch.uint8, device=dev)
+        log(f"update: radius {r_epoch}, {chunk} features per chunk, workspace {uws.numel() / 1e9:.2f} GB")
+    phases = ("norms", "plan", "sweep", "finalize") + (("update",) if args.epoch else ())
 
     def step(ev=None):
         if ev is not None:
@@ -216,12 +226,16 @@ def main():
             som.bmu_finalize(norms, rp, V, M, nnz, bmu, dist, ws, tile_samples=args.tile)
         if ev is not None:
             ev[4].record()
+        if args.epoch:
+            som.update(W, rp, ci, bmu, V, cfg.edge, r_epoch, nnz=nnz, chunk_features=chunk, workspace=uws)
+            if ev is not None:
+                ev[5].record()
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
 
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(len(phases) + 1)] for _ in range(args.steps)]
     torch.cuda.synchronize()
     t_start = time.perf_counter()
     for k in range(args.steps):
@@ -233,7 +247,7 @@ def main():
         raise RuntimeError("the device flagged the generated CSR as invalid")
 
     phase_ms = {p: float(np.mean([e[i].elapsed_time(e[i + 1]) for e in events])) for i, p in enumerate(phases)}
-    step_ms = float(np.mean([e[0].elapsed_time(e[4]) for e in events]))
+    step_ms = float(np.mean([e[0].elapsed_time(e[len(phases)]) for e in events]))
     ms_per_step = 1e3 * elapsed / args.steps
     value = N / (ms_per_step / 1e3)
     eff_gbps = alg_bytes / (ms_per_step / 1e3) / 1e9
@@ -258,7 +272,8 @@ def main():
         "config": {"workload": workload, "map": f"{cfg.edge}x{cfg.edge}", "M": M, "V": V, "N": N, "nnz": nnz,
                    "tile_samples": args.tile or som.DEFAULT_TILE_SAMPLES,
                    "keep_order": False, "alg_tile_samples": ALG_TILE, "parallelism": "single GPU",
-                   "search": "two best units" if args.top2 else "best unit", "codebook": args.dtype,
+                   "search": ("two best units + batch update (one epoch)" if args.epoch else
+                              "two best units" if args.top2 else "best unit"), "codebook": args.dtype,
                    "rows": "real-valued" if args.values else "binary"},
         "effective_codebook_GBps": eff_gbps,
         "effective_pct_of_hbm_peak": 100.0 * eff_gbps / HBM_PEAK_GBPS,

@@ -15,7 +15,8 @@
 //      rounded once to binary16 at this final write.
 // A lane owns one lattice line (row or column) of one field and runs its three
 // passes sequentially, exactly in the order above, so the result is the same
-// bits on every run. Features are processed in chunks, so the workspace holds
+// bits on every run. The row passes run on a transposed copy, so that in every
+// pass neighbouring lanes read neighbouring addresses. Features are processed in chunks, so the workspace holds
 // three fields of chunk * M values rather than V * M.
 
 #include <climits>
@@ -70,22 +71,34 @@ __device__ __forceinline__ void box_pass(const In *in, float *out, int64_t n, in
     }
 }
 
-// Three passes along lattice rows: counts -> A -> B -> A. One lane per (field, row).
-__global__ __launch_bounds__(256) void k_blur_rows(const int32_t *__restrict__ cnt, float *__restrict__ a,
-                                                   float *__restrict__ b, int64_t fields, int64_t E, int64_t r)
+// Transpose of every field's E x E lattice, 64 x 64 tiles through LDS (padded
+// against bank conflicts); the first use also converts the counts to fp32.
+template <typename In>
+__global__ __launch_bounds__(256) void k_transpose(const In *__restrict__ in, float *__restrict__ out, int64_t fields,
+                                                   int64_t E)
 {
-    const int64_t lines = fields * E;
-    for (int64_t l = (int64_t)blockIdx.x * 256 + threadIdx.x; l < lines; l += (int64_t)gridDim.x * 256) {
-        const int64_t off = l * E;  // field f = l / E, row l % E: rows are contiguous
-        box_pass(cnt + off, a + off, E, 1, r);
-        box_pass(a + off, b + off, E, 1, r);
-        box_pass(b + off, a + off, E, 1, r);
+    __shared__ float tile[64][65];
+    const int64_t tiles_axis = (E + 63) / 64;
+    const int64_t per_field = tiles_axis * tiles_axis;
+    const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;  // 64 x 4 threads
+    for (int64_t t = blockIdx.x; t < fields * per_field; t += gridDim.x) {
+        const int64_t f = t / per_field;
+        const int64_t r0 = (t % per_field) / tiles_axis * 64, c0 = (t % per_field) % tiles_axis * 64;
+        const In *src = in + f * E * E;
+        float *dst = out + f * E * E;
+        for (int y = ty; y < 64; y += 4)
+            if (r0 + y < E && c0 + tx < E) tile[y][tx] = (float)src[(r0 + y) * E + c0 + tx];
+        __syncthreads();
+        for (int y = ty; y < 64; y += 4)
+            if (c0 + y < E && r0 + tx < E) dst[(c0 + y) * E + r0 + tx] = tile[tx][y];
+        __syncthreads();
     }
 }
 
-// Three passes along lattice columns: A -> B -> A -> B. One lane per (field, column):
-// neighbouring lanes take neighbouring columns, so every step is one coalesced row read.
-__global__ __launch_bounds__(256) void k_blur_cols(float *__restrict__ a, float *__restrict__ b, int64_t fields,
+// Three passes along the lines that run down the lattice's second index, A -> B -> A
+// -> B. One lane per (field, line): neighbouring lanes take neighbouring lines, so
+// every step is one coalesced read. On a transposed field these are the row passes.
+__global__ __launch_bounds__(256) void k_blur_down(float *__restrict__ a, float *__restrict__ b, int64_t fields,
                                                    int64_t E, int64_t r)
 {
     const int64_t lines = fields * E;
@@ -117,12 +130,26 @@ __global__ __launch_bounds__(256) void k_zero_i32(int32_t *__restrict__ p, int64
     for (int64_t k = (int64_t)blockIdx.x * 256 + threadIdx.x; k < n; k += (int64_t)gridDim.x * 256) p[k] = 0;
 }
 
+// Both fields' blur: counts (rows r, columns c) -> transposed fp32 (T[c][r]) -> row
+// passes as passes down T -> transposed back -> column passes. Result in b.
+void blur(const int32_t *cnt, float *a, float *b, int64_t fields, int64_t E, int64_t r, hipStream_t st);
+
 unsigned grid_for(int64_t n)
 {
     int64_t b = (n + 255) / 256;
     if (b < 1) b = 1;
     if (b > (1 << 20)) b = 1 << 20;
     return (unsigned)b;
+}
+
+void blur(const int32_t *cnt, float *a, float *b, int64_t fields, int64_t E, int64_t r, hipStream_t st)
+{
+    const int64_t tiles = fields * ((E + 63) / 64) * ((E + 63) / 64);
+    const unsigned tg = (unsigned)(tiles < (1 << 20) ? tiles : (1 << 20));
+    hipLaunchKernelGGL(k_transpose<int32_t>, dim3(tg), dim3(256), 0, st, cnt, a, fields, E);
+    hipLaunchKernelGGL(k_blur_down, dim3(grid_for(fields * E)), dim3(256), 0, st, a, b, fields, E, r);
+    hipLaunchKernelGGL(k_transpose<float>, dim3(tg), dim3(256), 0, st, b, a, fields, E);
+    hipLaunchKernelGGL(k_blur_down, dim3(grid_for(fields * E)), dim3(256), 0, st, a, b, fields, E, r);
 }
 
 }  // namespace
@@ -135,16 +162,13 @@ hipError_t launch_update(bool f16, void *W, int64_t V, int64_t E, const int32_t 
     // den: counts, blur, kept in ub.den_b
     hipLaunchKernelGGL(k_zero_i32, dim3(grid_for(M)), dim3(256), 0, st, ub.den_cnt, M);
     hipLaunchKernelGGL(k_count_units, dim3(grid_for(N)), dim3(256), 0, st, bmu, N, M, ub.den_cnt);
-    hipLaunchKernelGGL(k_blur_rows, dim3(grid_for(E)), dim3(256), 0, st, ub.den_cnt, ub.den_a, ub.den_b, (int64_t)1, E,
-                       radius);
-    hipLaunchKernelGGL(k_blur_cols, dim3(grid_for(E)), dim3(256), 0, st, ub.den_a, ub.den_b, (int64_t)1, E, radius);
+    blur(ub.den_cnt, ub.den_a, ub.den_b, 1, E, radius, st);
     for (int64_t v0 = 0; v0 < V; v0 += chunk) {
         const int64_t f = V - v0 < chunk ? V - v0 : chunk;
         hipLaunchKernelGGL(k_zero_i32, dim3(grid_for(f * M)), dim3(256), 0, st, ub.cnt, f * M);
         hipLaunchKernelGGL(k_count_features, dim3(grid_for(N)), dim3(256), 0, st, row_ptr, col_idx, N, nnz, bmu, M,
                            (int32_t)v0, (int32_t)(v0 + f), ub.cnt);
-        hipLaunchKernelGGL(k_blur_rows, dim3(grid_for(f * E)), dim3(256), 0, st, ub.cnt, ub.a, ub.b, f, E, radius);
-        hipLaunchKernelGGL(k_blur_cols, dim3(grid_for(f * E)), dim3(256), 0, st, ub.a, ub.b, f, E, radius);
+        blur(ub.cnt, ub.a, ub.b, f, E, radius, st);
         if (f16)
             hipLaunchKernelGGL(k_quotient<_Float16>, dim3(grid_for(f * M)), dim3(256), 0, st,
                                static_cast<_Float16 *>(W), ub.b, ub.den_b, f, M, v0);
