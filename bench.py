@@ -194,7 +194,7 @@ def main():
     if args.epoch:
         r_epoch = som.radius(som.sigma(1, 0.5 * cfg.edge, 0.5))
         chunk = int(max(1, min(V, args.update_chunk_gb * 1e9 / (12.0 * M))))
-        uws = torch.empty(som.update_workspace_bytes(V, cfg.edge, chunk), dtype=torch.uint8, device=dev)
+        uws = torch.empty(som.update_workspace_bytes(V, cfg.edge, N, chunk), dtype=torch.uint8, device=dev)
         log(f"update: radius {r_epoch}, {chunk} features per chunk, workspace {uws.numel() / 1e9:.2f} GB")
     phases = ("norms", "plan", "sweep", "finalize") + (("update",) if args.epoch else ())
 

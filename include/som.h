@@ -299,6 +299,9 @@ som_status som_bmu_sf_finalize(const double *norms, int64_t V, int64_t M, const 
  *   radius          box half-width r >= 1: som_radius(som_sigma(epoch, ...)).
  *   chunk_features  features blurred per pass (0 = all V); the workspace holds
  *                   three chunk x M fields, so smaller chunks need less memory.
+ * som_update_workspace_bytes(V, E, N, chunk_features) sizes the workspace for a
+ * batch of N samples (three chunk x M fields, four M-sized buffers and N int32
+ * positions for sorting the samples of crowded units); 0 for invalid sizes.
  * Per unit, den = samples assigned to it and num[v] = those holding feature v
  * (exact integer counts), both converted to fp32 and blurred by three
  * running-sum box passes along every lattice row and then three along every
@@ -308,7 +311,7 @@ som_status som_bmu_sf_finalize(const double *norms, int64_t V, int64_t M, const 
  * at the final write). W = num / den. The passes run in a fixed order, so the
  * result is the same bits on every run. Norms must be recomputed afterwards.
  */
-size_t som_update_workspace_bytes(int64_t V, int64_t E, int64_t chunk_features);
+size_t som_update_workspace_bytes(int64_t V, int64_t E, int64_t N, int64_t chunk_features);
 
 som_status som_update(float *W, int64_t V, int64_t E, const int32_t *row_ptr, const int32_t *col_idx, int64_t N,
                       int64_t nnz, const int32_t *bmu, int32_t radius, int64_t chunk_features, void *workspace,

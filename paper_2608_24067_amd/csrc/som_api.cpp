@@ -460,11 +460,12 @@ som_status som_bmu_input_flags(const void *workspace, size_t workspace_bytes, in
     return ok();
 }
 
-size_t som_update_workspace_bytes(int64_t V, int64_t E, int64_t chunk_features)
+size_t som_update_workspace_bytes(int64_t V, int64_t E, int64_t N, int64_t chunk_features)
 {
-    if (V < 1 || V >= INT32_MAX || E < 1 || E * E > SOM_MAX_NEURONS || chunk_features < 0) return 0;
+    if (V < 1 || V >= INT32_MAX || E < 1 || E * E > SOM_MAX_NEURONS || N < 0 || N >= INT32_MAX || chunk_features < 0)
+        return 0;
     const int64_t chunk = chunk_features == 0 || chunk_features > V ? V : chunk_features;
-    return som::update_layout(E * E, chunk).total;
+    return som::update_layout(E * E, N, chunk).total;
 }
 
 static som_status update_impl(const Book &b, void *W, int64_t V, int64_t E, const int32_t *row_ptr,
@@ -484,7 +485,7 @@ static som_status update_impl(const Book &b, void *W, int64_t V, int64_t E, cons
     if (st != SOM_OK) return st;
     const int64_t M = E * E;
     const int64_t chunk = chunk_features == 0 || chunk_features > V ? V : chunk_features;
-    const som::UpdateLayout L = som::update_layout(M, chunk);
+    const som::UpdateLayout L = som::update_layout(M, N, chunk);
     if (!workspace) return fail(SOM_ERR_WORKSPACE, "%s: workspace is NULL", who);
     if (reinterpret_cast<uintptr_t>(workspace) & 255) return fail(SOM_ERR_WORKSPACE, "workspace must be 256-byte aligned");
     if (workspace_bytes < L.total)
@@ -495,6 +496,9 @@ static som_status update_impl(const Book &b, void *W, int64_t V, int64_t E, cons
     ub.den_cnt = reinterpret_cast<int32_t *>(w + L.den_cnt);
     ub.den_a = reinterpret_cast<float *>(w + L.den_a);
     ub.den_b = reinterpret_cast<float *>(w + L.den_b);
+    ub.start = reinterpret_cast<int32_t *>(w + L.start);
+    ub.cursor = reinterpret_cast<int32_t *>(w + L.cursor);
+    ub.order = reinterpret_cast<int32_t *>(w + L.order);
     ub.cnt = reinterpret_cast<int32_t *>(w + L.cnt);
     ub.a = reinterpret_cast<float *>(w + L.a);
     ub.b = reinterpret_cast<float *>(w + L.b);

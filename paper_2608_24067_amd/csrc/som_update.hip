@@ -4,7 +4,13 @@
 // After a search has given every sample its best unit, the update
 //   1. scatters the batch onto the E x E lattice: den[i] = samples at unit i and,
 //      feature by feature, num[v][i] = samples at unit i holding feature v (integer
-//      atomics: exact and independent of their order);
+//      counts: exact and independent of the order they are taken in). Units that
+//      hold many samples (on an untrained codebook a handful of units can take the
+//      whole batch) are counted in LDS: their samples are sorted by unit and each
+//      workgroup histograms a run of one unit's samples, then adds the non-zero
+//      bins to global memory; the other units take one global atomic per feature.
+//      The counts are unit-major (cnt[i][v]); the first transpose of the blur turns
+//      them into feature-major lattices;
 //   2. converts both fields to fp32 and blurs them: three box passes along every
 //      lattice row, then three along every lattice column, each a running window
 //      sum over the clamped window (the first window summed in ascending order,
@@ -27,33 +33,180 @@
 namespace som {
 namespace {
 
-// Samples per unit.
+typedef unsigned long long u64;
+
+// A unit with at least kHeavy samples is counted through LDS; kRunSamples sorted
+// samples per workgroup there, and kLdsBins feature bins (64 KB) per LDS pass.
+constexpr int32_t kHeavy = 1024;
+constexpr int64_t kRunSamples = 16384;
+constexpr int kLdsBins = 16384;
+
+__device__ __forceinline__ int lane_id() { return (int)(threadIdx.x & 63); }
+
+// Clamped id range of sample s (relative to row_ptr[0]).
+__device__ __forceinline__ void sample_ids(const int32_t *row_ptr, int64_t base, int64_t nnz, int64_t s, int64_t &rb,
+                                           int64_t &re)
+{
+    rb = (int64_t)row_ptr[s] - base;
+    re = (int64_t)row_ptr[s + 1] - base;
+    rb = rb < 0 ? 0 : (rb > nnz ? nnz : rb);
+    re = re < rb ? rb : (re > nnz ? nnz : re);
+}
+
+// Samples per unit. The lanes of a wave that share a unit add their count with one
+// atomic (one per distinct unit in the wave), so a unit that takes most of the
+// batch does not serialise the whole grid on one address.
 __global__ __launch_bounds__(256) void k_count_units(const int32_t *__restrict__ bmu, int64_t N, int64_t M,
                                                      int32_t *__restrict__ cnt)
 {
-    for (int64_t s = (int64_t)blockIdx.x * 256 + threadIdx.x; s < N; s += (int64_t)gridDim.x * 256) {
-        const int32_t u = bmu[s];
-        if (u >= 0 && u < M) atomicAdd(cnt + u, 1);
+    const int lane = lane_id();
+    for (int64_t s0 = (int64_t)blockIdx.x * 256; s0 < N; s0 += (int64_t)gridDim.x * 256) {  // uniform loop
+        const int64_t s = s0 + threadIdx.x;
+        int32_t u = -1;
+        if (s < N) {
+            u = bmu[s];
+            if (u < 0 || u >= M) u = -1;
+        }
+        u64 todo = __ballot(u >= 0);
+        while (todo) {
+            const int leader = __builtin_ctzll(todo);
+            const int32_t lu = __builtin_amdgcn_readlane(u, leader);
+            const u64 same = __ballot(u == lu) & todo;
+            if (lane == leader) atomicAdd(cnt + lu, (int32_t)__popcll(same));
+            todo &= ~same;
+        }
     }
 }
 
-// num[v - v0][unit of s] += 1 for every id v in [v0, v1) of every sample s.
-__global__ __launch_bounds__(256) void k_count_features(const int32_t *__restrict__ row_ptr,
-                                                        const int32_t *__restrict__ col_idx, int64_t N, int64_t nnz,
-                                                        const int32_t *__restrict__ bmu, int64_t M, int32_t v0,
-                                                        int32_t v1, int32_t *__restrict__ cnt)
+// One workgroup: start[u] = number of samples of heavy units below u (heavy: at least
+// kHeavy samples), start[M] = all samples of heavy units; cursor = start.
+__global__ __launch_bounds__(1024) void k_heavy_scan(const int32_t *__restrict__ cnt, int64_t M,
+                                                     int32_t *__restrict__ start, int32_t *__restrict__ cursor)
+{
+    __shared__ int64_t ss[1024];
+    const int t = threadIdx.x;
+    const int64_t per = (M + 1023) / 1024;
+    const int64_t b0 = t * per < M ? t * per : M;
+    const int64_t b1 = b0 + per < M ? b0 + per : M;
+    int64_t n = 0;
+    for (int64_t u = b0; u < b1; ++u) n += cnt[u] >= kHeavy ? cnt[u] : 0;
+    ss[t] = n;
+    __syncthreads();
+    for (int d = 1; d < 1024; d <<= 1) {  // inclusive Hillis-Steele scan
+        const int64_t a = t >= d ? ss[t - d] : 0;
+        __syncthreads();
+        ss[t] += a;
+        __syncthreads();
+    }
+    int64_t o = ss[t] - n;
+    for (int64_t u = b0; u < b1; ++u) {
+        start[u] = (int32_t)o;
+        cursor[u] = (int32_t)o;
+        o += cnt[u] >= kHeavy ? cnt[u] : 0;
+    }
+    if (t == 1023) start[M] = (int32_t)ss[1023];
+}
+
+// order[start[u] ...] = the samples of every heavy unit u, grouped by unit (in any
+// order within a unit: the counts do not depend on it). One atomic per distinct unit
+// in a wave reserves that unit's positions for all its lanes.
+__global__ __launch_bounds__(256) void k_heavy_scatter(const int32_t *__restrict__ bmu, int64_t N, int64_t M,
+                                                       const int32_t *__restrict__ cnt, int32_t *__restrict__ cursor,
+                                                       int32_t *__restrict__ order)
+{
+    const int lane = lane_id();
+    const u64 below = (1ull << lane) - 1ull;
+    for (int64_t s0 = (int64_t)blockIdx.x * 256; s0 < N; s0 += (int64_t)gridDim.x * 256) {  // uniform loop
+        const int64_t s = s0 + threadIdx.x;
+        int32_t u = -1;
+        if (s < N) {
+            u = bmu[s];
+            if (u < 0 || u >= M || cnt[u] < kHeavy) u = -1;
+        }
+        u64 todo = __ballot(u >= 0);
+        while (todo) {
+            const int leader = __builtin_ctzll(todo);
+            const int32_t lu = __builtin_amdgcn_readlane(u, leader);
+            const u64 same = __ballot(u == lu) & todo;
+            int32_t at = 0;
+            if (lane == leader) at = atomicAdd(cursor + lu, (int32_t)__popcll(same));
+            at = __builtin_amdgcn_readlane(at, leader);
+            if ((same >> lane) & 1ull) order[at + __popcll(same & below)] = (int32_t)s;
+            todo &= ~same;
+        }
+    }
+}
+
+// cnt[u][v - v0] += 1 (unit-major, f = v1 - v0 per unit) for every id v in [v0, v1)
+// of every sample whose unit is not heavy.
+__global__ __launch_bounds__(256) void k_count_light(const int32_t *__restrict__ row_ptr,
+                                                     const int32_t *__restrict__ col_idx, int64_t N, int64_t nnz,
+                                                     const int32_t *__restrict__ bmu, int64_t M,
+                                                     const int32_t *__restrict__ units, int32_t v0, int32_t v1,
+                                                     int32_t *__restrict__ cnt)
 {
     const int64_t base = row_ptr[0];
+    const int64_t f = (int64_t)v1 - v0;
     for (int64_t s = (int64_t)blockIdx.x * 256 + threadIdx.x; s < N; s += (int64_t)gridDim.x * 256) {
         const int32_t u = bmu[s];
-        if (u < 0 || u >= M) continue;
-        int64_t rb = (int64_t)row_ptr[s] - base, re = (int64_t)row_ptr[s + 1] - base;
-        rb = rb < 0 ? 0 : (rb > nnz ? nnz : rb);
-        re = re < rb ? rb : (re > nnz ? nnz : re);
+        if (u < 0 || u >= M || units[u] >= kHeavy) continue;
+        int64_t rb, re;
+        sample_ids(row_ptr, base, nnz, s, rb, re);
         for (int64_t p = rb; p < re; ++p) {
             const int32_t v = col_idx[base + p];
-            if (v >= v0 && v < v1) atomicAdd(cnt + (int64_t)(v - v0) * M + u, 1);
+            if (v >= v0 && v < v1) atomicAdd(cnt + (int64_t)u * f + (v - v0), 1);
         }
+    }
+}
+
+// Heavy units: workgroup b takes the sorted positions [b * kRunSamples, ...) of
+// order; each run of one unit's samples in that range is histogrammed in LDS, in
+// passes of kLdsBins features, and the non-zero bins are added to cnt[u][.].
+__global__ __launch_bounds__(256) void k_count_heavy(const int32_t *__restrict__ row_ptr,
+                                                     const int32_t *__restrict__ col_idx, int64_t nnz,
+                                                     const int32_t *__restrict__ bmu, int64_t M,
+                                                     const int32_t *__restrict__ units,
+                                                     const int32_t *__restrict__ start,
+                                                     const int32_t *__restrict__ order, int32_t v0, int32_t v1,
+                                                     int32_t *__restrict__ cnt)
+{
+    __shared__ uint32_t hist[kLdsBins];
+    const int64_t base = row_ptr[0];
+    const int64_t f = (int64_t)v1 - v0;
+    const int64_t total = start[M];
+    const int64_t p0 = (int64_t)blockIdx.x * kRunSamples;
+    if (p0 >= total) return;  // uniform
+    const int64_t p1 = p0 + kRunSamples < total ? p0 + kRunSamples : total;
+    for (int64_t p = p0; p < p1;) {  // uniform: every thread reads the same run bounds
+        const int32_t u = bmu[order[p]];
+        int64_t re = p + 1;
+        if (u >= 0 && u < M) {
+            const int64_t end = (int64_t)start[u] + units[u];
+            re = end < p1 ? end : p1;
+            if (re <= p) re = p + 1;
+        }
+        if (u >= 0 && u < M) {
+            for (int64_t h0 = v0; h0 < v1; h0 += kLdsBins) {
+                const int hb = (int)((int64_t)v1 - h0 < kLdsBins ? (int64_t)v1 - h0 : kLdsBins);
+                for (int b = threadIdx.x; b < hb; b += 256) hist[b] = 0u;
+                __syncthreads();
+                for (int64_t q = p + threadIdx.x; q < re; q += 256) {
+                    int64_t rb, rend;
+                    sample_ids(row_ptr, base, nnz, order[q], rb, rend);
+                    for (int64_t k = rb; k < rend; ++k) {
+                        const int64_t v = col_idx[base + k];
+                        if (v >= h0 && v < h0 + hb) atomicAdd(&hist[v - h0], 1u);
+                    }
+                }
+                __syncthreads();
+                for (int b = threadIdx.x; b < hb; b += 256) {
+                    const uint32_t c = hist[b];
+                    if (c) atomicAdd(cnt + (int64_t)u * f + (h0 - v0 + b), (int32_t)c);
+                }
+                __syncthreads();
+            }
+        }
+        p = re;
     }
 }
 
@@ -95,6 +248,28 @@ __global__ __launch_bounds__(256) void k_transpose(const In *__restrict__ in, fl
     }
 }
 
+// Unit-major counts cnt[i][v] (i = r * E + c, f features per unit) to transposed
+// fp32 lattices out[v][c][r], in 64 (r) x 64 (v) tiles through LDS for each c: reads
+// run along v, writes along r.
+__global__ __launch_bounds__(256) void k_transpose_units(const int32_t *__restrict__ cnt, float *__restrict__ out,
+                                                         int64_t f, int64_t E)
+{
+    __shared__ float tile[64][65];
+    const int64_t rt = (E + 63) / 64, vt = (f + 63) / 64;
+    const int64_t M = E * E;
+    const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;  // 64 x 4 threads
+    for (int64_t t = blockIdx.x; t < E * rt * vt; t += gridDim.x) {
+        const int64_t c = t / (rt * vt);
+        const int64_t r0 = (t % (rt * vt)) / vt * 64, w0 = (t % vt) * 64;
+        for (int y = ty; y < 64; y += 4)
+            if (r0 + y < E && w0 + tx < f) tile[y][tx] = (float)cnt[((r0 + y) * E + c) * f + w0 + tx];
+        __syncthreads();
+        for (int y = ty; y < 64; y += 4)
+            if (w0 + y < f && r0 + tx < E) out[(w0 + y) * M + c * E + r0 + tx] = tile[tx][y];
+        __syncthreads();
+    }
+}
+
 // Three passes along the lines that run down the lattice's second index, A -> B -> A
 // -> B. One lane per (field, line): neighbouring lanes take neighbouring lines, so
 // every step is one coalesced read. On a transposed field these are the row passes.
@@ -130,9 +305,11 @@ __global__ __launch_bounds__(256) void k_zero_i32(int32_t *__restrict__ p, int64
     for (int64_t k = (int64_t)blockIdx.x * 256 + threadIdx.x; k < n; k += (int64_t)gridDim.x * 256) p[k] = 0;
 }
 
-// Both fields' blur: counts (rows r, columns c) -> transposed fp32 (T[c][r]) -> row
-// passes as passes down T -> transposed back -> column passes. Result in b.
-void blur(const int32_t *cnt, float *a, float *b, int64_t fields, int64_t E, int64_t r, hipStream_t st);
+// Blur of `fields` lattices: counts (rows r, columns c) -> transposed fp32 (T[c][r])
+// -> row passes as passes down T -> transposed back -> column passes. Result in b.
+// unit_major: cnt is cnt[i][field] rather than cnt[field][i].
+void blur(const int32_t *cnt, bool unit_major, float *a, float *b, int64_t fields, int64_t E, int64_t r,
+          hipStream_t st);
 
 unsigned grid_for(int64_t n)
 {
@@ -142,11 +319,18 @@ unsigned grid_for(int64_t n)
     return (unsigned)b;
 }
 
-void blur(const int32_t *cnt, float *a, float *b, int64_t fields, int64_t E, int64_t r, hipStream_t st)
+void blur(const int32_t *cnt, bool unit_major, float *a, float *b, int64_t fields, int64_t E, int64_t r,
+          hipStream_t st)
 {
     const int64_t tiles = fields * ((E + 63) / 64) * ((E + 63) / 64);
     const unsigned tg = (unsigned)(tiles < (1 << 20) ? tiles : (1 << 20));
-    hipLaunchKernelGGL(k_transpose<int32_t>, dim3(tg), dim3(256), 0, st, cnt, a, fields, E);
+    if (unit_major) {
+        const int64_t ut = E * ((E + 63) / 64) * ((fields + 63) / 64);
+        hipLaunchKernelGGL(k_transpose_units, dim3((unsigned)(ut < (1 << 20) ? ut : (1 << 20))), dim3(256), 0, st, cnt,
+                           a, fields, E);
+    } else {
+        hipLaunchKernelGGL(k_transpose<int32_t>, dim3(tg), dim3(256), 0, st, cnt, a, fields, E);
+    }
     hipLaunchKernelGGL(k_blur_down, dim3(grid_for(fields * E)), dim3(256), 0, st, a, b, fields, E, r);
     hipLaunchKernelGGL(k_transpose<float>, dim3(tg), dim3(256), 0, st, b, a, fields, E);
     hipLaunchKernelGGL(k_blur_down, dim3(grid_for(fields * E)), dim3(256), 0, st, a, b, fields, E, r);
@@ -159,16 +343,23 @@ hipError_t launch_update(bool f16, void *W, int64_t V, int64_t E, const int32_t 
                          const UpdateBuffers &ub, hipStream_t st)
 {
     const int64_t M = E * E;
-    // den: counts, blur, kept in ub.den_b
+    // den: counts, blur, kept in ub.den_b; the samples of heavy units sorted by unit
+    const unsigned sg = grid_for(N < (1 << 26) ? N : (1 << 26));
     hipLaunchKernelGGL(k_zero_i32, dim3(grid_for(M)), dim3(256), 0, st, ub.den_cnt, M);
-    hipLaunchKernelGGL(k_count_units, dim3(grid_for(N)), dim3(256), 0, st, bmu, N, M, ub.den_cnt);
-    blur(ub.den_cnt, ub.den_a, ub.den_b, 1, E, radius, st);
+    hipLaunchKernelGGL(k_count_units, dim3(sg), dim3(256), 0, st, bmu, N, M, ub.den_cnt);
+    hipLaunchKernelGGL(k_heavy_scan, dim3(1), dim3(1024), 0, st, ub.den_cnt, M, ub.start, ub.cursor);
+    hipLaunchKernelGGL(k_heavy_scatter, dim3(sg), dim3(256), 0, st, bmu, N, M, ub.den_cnt, ub.cursor, ub.order);
+    blur(ub.den_cnt, false, ub.den_a, ub.den_b, 1, E, radius, st);
+    const int64_t runs = (N + kRunSamples - 1) / kRunSamples;
     for (int64_t v0 = 0; v0 < V; v0 += chunk) {
         const int64_t f = V - v0 < chunk ? V - v0 : chunk;
         hipLaunchKernelGGL(k_zero_i32, dim3(grid_for(f * M)), dim3(256), 0, st, ub.cnt, f * M);
-        hipLaunchKernelGGL(k_count_features, dim3(grid_for(N)), dim3(256), 0, st, row_ptr, col_idx, N, nnz, bmu, M,
-                           (int32_t)v0, (int32_t)(v0 + f), ub.cnt);
-        blur(ub.cnt, ub.a, ub.b, f, E, radius, st);
+        hipLaunchKernelGGL(k_count_light, dim3(grid_for(N)), dim3(256), 0, st, row_ptr, col_idx, N, nnz, bmu, M,
+                           ub.den_cnt, (int32_t)v0, (int32_t)(v0 + f), ub.cnt);
+        if (runs > 0)
+            hipLaunchKernelGGL(k_count_heavy, dim3((unsigned)runs), dim3(256), 0, st, row_ptr, col_idx, nnz, bmu, M,
+                               ub.den_cnt, ub.start, ub.order, (int32_t)v0, (int32_t)(v0 + f), ub.cnt);
+        blur(ub.cnt, true, ub.a, ub.b, f, E, radius, st);
         if (f16)
             hipLaunchKernelGGL(k_quotient<_Float16>, dim3(grid_for(f * M)), dim3(256), 0, st,
                                static_cast<_Float16 *>(W), ub.b, ub.den_b, f, M, v0);

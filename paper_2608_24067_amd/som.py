@@ -88,7 +88,7 @@ def load():
     for name in ("som_bmu_sf_search", "som_bmu_sf_search_f16", "som_bmu_sf_plan", "som_bmu_sf_sweep",
                  "som_bmu_sf_sweep_f16", "som_bmu_sf_finalize"):
         getattr(lib, name).restype = ctypes.c_int
-    lib.som_update_workspace_bytes.argtypes = [i64, i64, i64]
+    lib.som_update_workspace_bytes.argtypes = [i64, i64, i64, i64]
     lib.som_update_workspace_bytes.restype = sz
     lib.som_update.argtypes = [vp, i64, i64, vp, vp, i64, i64, vp, i32, i64, vp, sz, vp]
     lib.som_update.restype = ctypes.c_int
@@ -389,8 +389,8 @@ def bmu_sf_finalize(norms, row_ptr, V: int, M: int, nnz: int, out, workspace, ti
 
 # ------------------------------------------------------------------- batch update
 
-def update_workspace_bytes(V: int, E: int, chunk_features: int = 0) -> int:
-    n = load().som_update_workspace_bytes(V, E, chunk_features)
+def update_workspace_bytes(V: int, E: int, N: int, chunk_features: int = 0) -> int:
+    n = load().som_update_workspace_bytes(V, E, N, chunk_features)
     if n == 0:
         raise ValueError("som_update_workspace_bytes: invalid sizes")
     return n
@@ -404,7 +404,7 @@ def update(W, row_ptr, col_idx, bmu, V: int, E: int, radius: int, nnz: int | Non
     if not isinstance(W, torch.Tensor) or W.numel() != V * E * E:
         raise ValueError("W must be a tensor of V*E*E elements")
     if workspace is None:
-        workspace = torch.empty(update_workspace_bytes(V, E, chunk_features), dtype=torch.uint8, device=W.device)
+        workspace = torch.empty(update_workspace_bytes(V, E, N, chunk_features), dtype=torch.uint8, device=W.device)
     f16 = W.dtype == torch.float16
     wp = _dev(W, "W", torch.float16 if f16 else torch.float32)
     rp, ci = _csr(row_ptr, col_idx, N, nnz)

@@ -105,11 +105,14 @@ def test_schedule_and_radius():
 
 def test_update_workspace_and_checks():
     lib = som.load()
-    full = som.update_workspace_bytes(300, 16)
-    part = som.update_workspace_bytes(300, 16, 10)
+    full = som.update_workspace_bytes(300, 16, 10)
+    part = som.update_workspace_bytes(300, 16, 10, 10)
     assert full > part > 0 and full >= 3 * 300 * 256 * 4
-    assert lib.som_update_workspace_bytes(0, 16, 0) == 0
-    assert lib.som_update_workspace_bytes(10, 1025, 0) == 0  # E*E beyond 2^20
+    # the sort of crowded units' samples holds one int32 per sample
+    assert som.update_workspace_bytes(300, 16, 10 + 10**6) >= full + 4 * 10**6
+    assert lib.som_update_workspace_bytes(0, 16, 10, 0) == 0
+    assert lib.som_update_workspace_bytes(10, 1025, 10, 0) == 0  # E*E beyond 2^20
+    assert lib.som_update_workspace_bytes(10, 16, -1, 0) == 0
     assert lib.som_update(FAKE, 300, 16, FAKE, FAKE, 10, 50, FAKE, 0, 0, FAKE, 1 << 30, None) == som.SOM_ERR_INVALID_ARG
     assert lib.som_update(FAKE, 300, 16, FAKE, FAKE, 10, 50, None, 1, 0, FAKE, 1 << 30, None) == som.SOM_ERR_INVALID_ARG
     assert lib.som_update(FAKE, 300, 16, FAKE, FAKE, 10, 50, FAKE, 1, 0, FAKE, part, None) == som.SOM_ERR_WORKSPACE

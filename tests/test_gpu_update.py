@@ -53,6 +53,37 @@ def test_update_bit_exact(dev, seed, N, V, E, r, chunk, spread):
     assert bad.size == 0, f"{bad.size} weights differ, first {bad[:5]}: {got.reshape(-1)[bad[:5]]} vs {ref.reshape(-1)[bad[:5]]}"
 
 
+def crowded_bmu(seed, N, M, shares):
+    """Best units where unit u takes the fraction shares[u] (or the exact count, if an int)
+    of the batch and the rest spread uniformly: crowded units take the LDS-counting path
+    (1024 samples or more), runs of 16384 sorted samples split one unit across workgroups."""
+    rng = np.random.default_rng(seed)
+    rest = np.setdiff1d(np.arange(M), list(shares))
+    bmu = rest[rng.integers(0, rest.size, N)].astype(np.int32) if rest.size else np.zeros(N, np.int32)
+    at = 0
+    for u, share in shares.items():
+        n = share if isinstance(share, int) else int(share * N)
+        bmu[at:at + n] = u
+        at += n
+    return bmu[rng.permutation(N)]
+
+
+@pytest.mark.parametrize("seed,N,V,E,r,chunk,shares", [
+    (101, 20000, 17000, 8, 2, 0, {0: 1.0}),            # one unit takes all: two runs, two LDS passes
+    (102, 30000, 600, 16, 3, 250, {7: 0.55, 200: 0.25}),  # two crowded units, the rest spread; 3 chunks
+    (103, 3400, 90, 12, 1, 1, {3: 1023, 4: 1024, 5: 1025}),  # either side of the threshold
+    (104, 40000, 300, 32, 5, 0, {1023: 0.5}),          # the last unit, runs ending at the batch end
+])
+def test_update_crowded_units(dev, seed, N, V, E, r, chunk, shares):
+    rp, ci = synth.make_csr(seed, N, V)
+    W = synth.codebook(seed, synth.UNIFORM, V, E * E)
+    bmu = crowded_bmu(seed, N, E * E, shares)
+    got = gpu_update(W, rp, ci, bmu, E, r, dev, chunk)
+    ref = oracle.update(W, E, rp, ci, bmu, r)
+    bad = np.flatnonzero(got != ref)
+    assert bad.size == 0, f"{bad.size} weights differ, first {bad[:5]}"
+
+
 def test_update_f16(dev):
     rp, ci, W, bmu = update_case(99, 3000, 400, 24, spread=0.5)
     W16 = W.astype(np.float16)
