@@ -498,6 +498,8 @@ static som_status update_impl(const Book &b, void *W, int64_t V, int64_t E, cons
     ub.den_b = reinterpret_cast<float *>(w + L.den_b);
     ub.start = reinterpret_cast<int32_t *>(w + L.start);
     ub.cursor = reinterpret_cast<int32_t *>(w + L.cursor);
+    ub.slot = reinterpret_cast<int32_t *>(w + L.slot);
+    ub.hunit = reinterpret_cast<int32_t *>(w + L.hunit);
     ub.order = reinterpret_cast<int32_t *>(w + L.order);
     ub.cnt = reinterpret_cast<int32_t *>(w + L.cnt);
     ub.a = reinterpret_cast<float *>(w + L.a);

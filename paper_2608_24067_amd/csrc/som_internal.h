@@ -118,19 +118,19 @@ hipError_t launch_order(const int32_t *row_ptr, const int32_t *col_idx, const fl
 // ----------------------------------------------------------------- update
 
 // Workspace of the batch update (som_update.hip): the den field (counts and two
-// float buffers, M each), the sort of heavy units' samples (start[M + 1],
-// cursor[M], order[N]) and, for one chunk of features, counts and two float
-// buffers of chunk * M.
+// float buffers, M each), the sort of heavy units' samples (start[M + 2],
+// cursor[M], slot[M], hunit[M], order[N]) and, for one chunk of features, counts
+// and two float buffers of chunk * M.
 struct UpdateBuffers {
     int32_t *den_cnt;
     float *den_a, *den_b;
-    int32_t *start, *cursor, *order;
+    int32_t *start, *cursor, *slot, *hunit, *order;
     int32_t *cnt;
     float *a, *b;
 };
 
 struct UpdateLayout {
-    size_t den_cnt, den_a, den_b, start, cursor, order, cnt, a, b, total;
+    size_t den_cnt, den_a, den_b, start, cursor, slot, hunit, order, cnt, a, b, total;
 };
 
 inline UpdateLayout update_layout(int64_t M, int64_t N, int64_t chunk)
@@ -145,8 +145,10 @@ inline UpdateLayout update_layout(int64_t M, int64_t N, int64_t chunk)
     L.den_cnt = take((size_t)M * 4);
     L.den_a = take((size_t)M * 4);
     L.den_b = take((size_t)M * 4);
-    L.start = take((size_t)(M + 1) * 4);
+    L.start = take((size_t)(M + 2) * 4);
     L.cursor = take((size_t)M * 4);
+    L.slot = take((size_t)M * 4);
+    L.hunit = take((size_t)M * 4);
     L.order = take((size_t)N * 4);
     L.cnt = take((size_t)chunk * (size_t)M * 4);
     L.a = take((size_t)chunk * (size_t)M * 4);

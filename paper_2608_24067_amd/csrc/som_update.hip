@@ -53,17 +53,33 @@ __device__ __forceinline__ void sample_ids(const int32_t *row_ptr, int64_t base,
     re = re < rb ? rb : (re > nnz ? nnz : re);
 }
 
+// Each wave takes a contiguous range of samples, 64 at a time; kScanBlocks blocks.
+constexpr int64_t kScanBlocks = 2048;
+
+__device__ __forceinline__ void wave_range(int64_t N, int64_t &w0, int64_t &w1)
+{
+    const int64_t waves = (int64_t)gridDim.x * (blockDim.x >> 6);
+    const int64_t w = (int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
+    const int64_t per = ((N + waves - 1) / waves + 63) / 64 * 64;
+    w0 = w * per < N ? w * per : N;
+    w1 = w0 + per < N ? w0 + per : N;
+}
+
 // Samples per unit. The lanes of a wave that share a unit add their count with one
-// atomic (one per distinct unit in the wave), so a unit that takes most of the
-// batch does not serialise the whole grid on one address.
+// atomic, and a wave carries a unit's count over as long as consecutive samples keep
+// it, so a unit that takes most of the batch does not serialise the grid on one
+// address.
 __global__ __launch_bounds__(256) void k_count_units(const int32_t *__restrict__ bmu, int64_t N, int64_t M,
                                                      int32_t *__restrict__ cnt)
 {
     const int lane = lane_id();
-    for (int64_t s0 = (int64_t)blockIdx.x * 256; s0 < N; s0 += (int64_t)gridDim.x * 256) {  // uniform loop
-        const int64_t s = s0 + threadIdx.x;
+    int64_t w0, w1;
+    wave_range(N, w0, w1);
+    int32_t pu = -1, pn = 0;  // the unit whose count is carried, and the count (wave-uniform)
+    for (int64_t s0 = w0; s0 < w1; s0 += 64) {
+        const int64_t s = s0 + lane;
         int32_t u = -1;
-        if (s < N) {
+        if (s < w1) {
             u = bmu[s];
             if (u < 0 || u >= M) u = -1;
         }
@@ -72,56 +88,133 @@ __global__ __launch_bounds__(256) void k_count_units(const int32_t *__restrict__
             const int leader = __builtin_ctzll(todo);
             const int32_t lu = __builtin_amdgcn_readlane(u, leader);
             const u64 same = __ballot(u == lu) & todo;
-            if (lane == leader) atomicAdd(cnt + lu, (int32_t)__popcll(same));
+            if (lu == pu) {
+                pn += (int32_t)__popcll(same);
+            } else {
+                if (pu >= 0 && lane == 0) atomicAdd(cnt + pu, pn);
+                pu = lu;
+                pn = (int32_t)__popcll(same);
+            }
             todo &= ~same;
         }
     }
+    if (pu >= 0 && lane == 0) atomicAdd(cnt + pu, pn);
+}
+
+// Samples per unit for maps of at most kLdsUnits units: a histogram in LDS per
+// workgroup (1024 threads), then one global atomic per non-zero bin.
+constexpr int kLdsUnits = 16384;
+
+__global__ __launch_bounds__(1024) void k_count_units_lds(const int32_t *__restrict__ bmu, int64_t N, int64_t M,
+                                                          int32_t *__restrict__ cnt)
+{
+    __shared__ uint32_t h[kLdsUnits];
+    for (int64_t i = threadIdx.x; i < M; i += 1024) h[i] = 0u;
+    __syncthreads();
+    for (int64_t s = (int64_t)blockIdx.x * 1024 + threadIdx.x; s < N; s += (int64_t)gridDim.x * 1024) {
+        const int32_t u = bmu[s];
+        if (u >= 0 && u < M) atomicAdd(&h[u], 1u);
+    }
+    __syncthreads();
+    for (int64_t i = threadIdx.x; i < M; i += 1024)
+        if (h[i]) atomicAdd(cnt + i, (int32_t)h[i]);
 }
 
 // One workgroup: start[u] = number of samples of heavy units below u (heavy: at least
-// kHeavy samples), start[M] = all samples of heavy units; cursor = start.
+// kHeavy samples), start[M] = all samples of heavy units, start[M + 1] = number of
+// heavy units; cursor = start; slot[u] = the heavy unit's rank among heavy units (-1
+// for the others) and hunit[slot] = u.
 __global__ __launch_bounds__(1024) void k_heavy_scan(const int32_t *__restrict__ cnt, int64_t M,
-                                                     int32_t *__restrict__ start, int32_t *__restrict__ cursor)
+                                                     int32_t *__restrict__ start, int32_t *__restrict__ cursor,
+                                                     int32_t *__restrict__ slot, int32_t *__restrict__ hunit)
 {
-    __shared__ int64_t ss[1024];
+    __shared__ int64_t ss[1024], sk[1024];
     const int t = threadIdx.x;
     const int64_t per = (M + 1023) / 1024;
     const int64_t b0 = t * per < M ? t * per : M;
     const int64_t b1 = b0 + per < M ? b0 + per : M;
-    int64_t n = 0;
-    for (int64_t u = b0; u < b1; ++u) n += cnt[u] >= kHeavy ? cnt[u] : 0;
+    int64_t n = 0, k = 0;
+    for (int64_t u = b0; u < b1; ++u)
+        if (cnt[u] >= kHeavy) {
+            n += cnt[u];
+            ++k;
+        }
     ss[t] = n;
+    sk[t] = k;
     __syncthreads();
-    for (int d = 1; d < 1024; d <<= 1) {  // inclusive Hillis-Steele scan
-        const int64_t a = t >= d ? ss[t - d] : 0;
+    for (int d = 1; d < 1024; d <<= 1) {  // inclusive Hillis-Steele scans
+        const int64_t a = t >= d ? ss[t - d] : 0, c = t >= d ? sk[t - d] : 0;
         __syncthreads();
         ss[t] += a;
+        sk[t] += c;
         __syncthreads();
     }
-    int64_t o = ss[t] - n;
+    int64_t o = ss[t] - n, q = sk[t] - k;
     for (int64_t u = b0; u < b1; ++u) {
         start[u] = (int32_t)o;
         cursor[u] = (int32_t)o;
-        o += cnt[u] >= kHeavy ? cnt[u] : 0;
+        if (cnt[u] >= kHeavy) {
+            o += cnt[u];
+            slot[u] = (int32_t)q;
+            hunit[q] = (int32_t)u;
+            ++q;
+        } else {
+            slot[u] = -1;
+        }
     }
-    if (t == 1023) start[M] = (int32_t)ss[1023];
+    if (t == 1023) {
+        start[M] = (int32_t)ss[1023];
+        start[M + 1] = (int32_t)sk[1023];
+    }
 }
 
 // order[start[u] ...] = the samples of every heavy unit u, grouped by unit (in any
-// order within a unit: the counts do not depend on it). One atomic per distinct unit
-// in a wave reserves that unit's positions for all its lanes.
-__global__ __launch_bounds__(256) void k_heavy_scatter(const int32_t *__restrict__ bmu, int64_t N, int64_t M,
-                                                       const int32_t *__restrict__ cnt, int32_t *__restrict__ cursor,
-                                                       int32_t *__restrict__ order)
+// order within a unit: the counts do not depend on it). A workgroup (1024 threads)
+// takes a contiguous range of samples. With at most kLdsUnits heavy units it counts
+// them per heavy unit in LDS, reserves each unit's positions with one global atomic,
+// and hands them out from LDS in a second pass over the range. Otherwise each wave
+// reserves, per 64 samples, one run of positions per distinct unit.
+__global__ __launch_bounds__(1024) void k_heavy_scatter(const int32_t *__restrict__ bmu, int64_t N, int64_t M,
+                                                        const int32_t *__restrict__ start,
+                                                        const int32_t *__restrict__ slot,
+                                                        const int32_t *__restrict__ hunit, int32_t *__restrict__ cursor,
+                                                        int32_t *__restrict__ order)
 {
+    __shared__ int32_t h[kLdsUnits];
+    const int64_t per = (N + gridDim.x - 1) / gridDim.x;
+    const int64_t b0 = (int64_t)blockIdx.x * per < N ? (int64_t)blockIdx.x * per : N;
+    const int64_t b1 = b0 + per < N ? b0 + per : N;
+    const int32_t heavy = start[M + 1];
+    auto slot_of = [&](int64_t s) {
+        const int32_t u = bmu[s];
+        return u >= 0 && u < M ? slot[u] : -1;
+    };
+    if (heavy <= kLdsUnits) {  // uniform
+        for (int i = threadIdx.x; i < heavy; i += 1024) h[i] = 0;
+        __syncthreads();
+        for (int64_t s = b0 + threadIdx.x; s < b1; s += 1024) {
+            const int32_t k = slot_of(s);
+            if (k >= 0 && k < heavy) atomicAdd(&h[k], 1);
+        }
+        __syncthreads();
+        for (int i = threadIdx.x; i < heavy; i += 1024)
+            if (h[i]) h[i] = atomicAdd(cursor + hunit[i], h[i]);
+        __syncthreads();
+        for (int64_t s = b0 + threadIdx.x; s < b1; s += 1024) {
+            const int32_t k = slot_of(s);
+            if (k >= 0 && k < heavy) order[atomicAdd(&h[k], 1)] = (int32_t)s;
+        }
+        return;
+    }
     const int lane = lane_id();
     const u64 below = (1ull << lane) - 1ull;
-    for (int64_t s0 = (int64_t)blockIdx.x * 256; s0 < N; s0 += (int64_t)gridDim.x * 256) {  // uniform loop
-        const int64_t s = s0 + threadIdx.x;
+    const int64_t wb = b0 + (int64_t)(threadIdx.x >> 6) * 64;
+    for (int64_t s0 = wb; s0 < b1; s0 += 1024) {
+        const int64_t s = s0 + lane;
         int32_t u = -1;
-        if (s < N) {
+        if (s < b1) {
             u = bmu[s];
-            if (u < 0 || u >= M || cnt[u] < kHeavy) u = -1;
+            if (u < 0 || u >= M || slot[u] < 0) u = -1;
         }
         u64 todo = __ballot(u >= 0);
         while (todo) {
@@ -344,11 +437,17 @@ hipError_t launch_update(bool f16, void *W, int64_t V, int64_t E, const int32_t 
 {
     const int64_t M = E * E;
     // den: counts, blur, kept in ub.den_b; the samples of heavy units sorted by unit
-    const unsigned sg = grid_for(N < (1 << 26) ? N : (1 << 26));
+    const unsigned sg = (unsigned)((N + 255) / 256 < kScanBlocks ? (N + 255) / 256 + 1 : kScanBlocks);
+    const unsigned lg = (unsigned)((N + 1023) / 1024 < 512 ? (N + 1023) / 1024 + 1 : 512);
     hipLaunchKernelGGL(k_zero_i32, dim3(grid_for(M)), dim3(256), 0, st, ub.den_cnt, M);
-    hipLaunchKernelGGL(k_count_units, dim3(sg), dim3(256), 0, st, bmu, N, M, ub.den_cnt);
-    hipLaunchKernelGGL(k_heavy_scan, dim3(1), dim3(1024), 0, st, ub.den_cnt, M, ub.start, ub.cursor);
-    hipLaunchKernelGGL(k_heavy_scatter, dim3(sg), dim3(256), 0, st, bmu, N, M, ub.den_cnt, ub.cursor, ub.order);
+    if (M <= kLdsUnits)
+        hipLaunchKernelGGL(k_count_units_lds, dim3(lg), dim3(1024), 0, st, bmu, N, M, ub.den_cnt);
+    else
+        hipLaunchKernelGGL(k_count_units, dim3(sg), dim3(256), 0, st, bmu, N, M, ub.den_cnt);
+    hipLaunchKernelGGL(k_heavy_scan, dim3(1), dim3(1024), 0, st, ub.den_cnt, M, ub.start, ub.cursor, ub.slot,
+                       ub.hunit);
+    hipLaunchKernelGGL(k_heavy_scatter, dim3(lg), dim3(1024), 0, st, bmu, N, M, ub.start, ub.slot, ub.hunit, ub.cursor,
+                       ub.order);
     blur(ub.den_cnt, false, ub.den_a, ub.den_b, 1, E, radius, st);
     const int64_t runs = (N + kRunSamples - 1) / kRunSamples;
     for (int64_t v0 = 0; v0 < V; v0 += chunk) {
