@@ -9,8 +9,8 @@
 //      whole batch) are counted in LDS: their samples are sorted by unit and each
 //      workgroup histograms a run of one unit's samples, then adds the non-zero
 //      bins to global memory; the other units take one global atomic per feature.
-//      The counts are unit-major (cnt[i][v]); the first transpose of the blur turns
-//      them into feature-major lattices;
+//      The counts are unit-major (cnt[i][v]), and so are the blurred fields: in
+//      every pass neighbouring lanes take neighbouring features;
 //   2. converts both fields to fp32 and blurs them: three box passes along every
 //      lattice row, then three along every lattice column, each a running window
 //      sum over the clamped window (the first window summed in ascending order,
@@ -21,9 +21,9 @@
 //      rounded once to binary16 at this final write.
 // A lane owns one lattice line (row or column) of one field and runs its three
 // passes sequentially, exactly in the order above, so the result is the same
-// bits on every run. The row passes run on a transposed copy, so that in every
-// pass neighbouring lanes read neighbouring addresses. Features are processed in chunks, so the workspace holds
-// three fields of chunk * M values rather than V * M.
+// bits on every run. The quotient is fused with the one transpose, from the
+// unit-major fields to the feature-major codebook. Features are processed in
+// chunks, so the workspace holds three fields of chunk * M values rather than V * M.
 
 #include <climits>
 
@@ -317,79 +317,48 @@ __device__ __forceinline__ void box_pass(const In *in, float *out, int64_t n, in
     }
 }
 
-// Transpose of every field's E x E lattice, 64 x 64 tiles through LDS (padded
-// against bank conflicts); the first use also converts the counts to fp32.
+// Three box passes along lines of n values, `stride` apart: src -> x -> y -> x (src
+// is the integer counts for the row passes). Fields are unit-major: element (r, c) of feature v
+// is at (r * E + c) * f + v. Line l is feature v = l % f of the line k = l / f, and
+// starts at k * outer + v; neighbouring lanes take neighbouring features, so every
+// step of every pass is one coalesced read. Row passes (along c): outer = E * f,
+// stride = f; column passes (along r): outer = f, stride = E * f.
+// Result in x. src may be y (its line is read in full before y is written); the
+// lines of different lanes are disjoint.
 template <typename In>
-__global__ __launch_bounds__(256) void k_transpose(const In *__restrict__ in, float *__restrict__ out, int64_t fields,
-                                                   int64_t E)
+__global__ __launch_bounds__(256) void k_blur3(const In *src, float *x, float *y, int64_t lines, int64_t f,
+                                               int64_t outer, int64_t n, int64_t stride, int64_t r)
 {
-    __shared__ float tile[64][65];
-    const int64_t tiles_axis = (E + 63) / 64;
-    const int64_t per_field = tiles_axis * tiles_axis;
-    const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;  // 64 x 4 threads
-    for (int64_t t = blockIdx.x; t < fields * per_field; t += gridDim.x) {
-        const int64_t f = t / per_field;
-        const int64_t r0 = (t % per_field) / tiles_axis * 64, c0 = (t % per_field) % tiles_axis * 64;
-        const In *src = in + f * E * E;
-        float *dst = out + f * E * E;
-        for (int y = ty; y < 64; y += 4)
-            if (r0 + y < E && c0 + tx < E) tile[y][tx] = (float)src[(r0 + y) * E + c0 + tx];
-        __syncthreads();
-        for (int y = ty; y < 64; y += 4)
-            if (c0 + y < E && r0 + tx < E) dst[(c0 + y) * E + r0 + tx] = tile[tx][y];
-        __syncthreads();
-    }
-}
-
-// Unit-major counts cnt[i][v] (i = r * E + c, f features per unit) to transposed
-// fp32 lattices out[v][c][r], in 64 (r) x 64 (v) tiles through LDS for each c: reads
-// run along v, writes along r.
-__global__ __launch_bounds__(256) void k_transpose_units(const int32_t *__restrict__ cnt, float *__restrict__ out,
-                                                         int64_t f, int64_t E)
-{
-    __shared__ float tile[64][65];
-    const int64_t rt = (E + 63) / 64, vt = (f + 63) / 64;
-    const int64_t M = E * E;
-    const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;  // 64 x 4 threads
-    for (int64_t t = blockIdx.x; t < E * rt * vt; t += gridDim.x) {
-        const int64_t c = t / (rt * vt);
-        const int64_t r0 = (t % (rt * vt)) / vt * 64, w0 = (t % vt) * 64;
-        for (int y = ty; y < 64; y += 4)
-            if (r0 + y < E && w0 + tx < f) tile[y][tx] = (float)cnt[((r0 + y) * E + c) * f + w0 + tx];
-        __syncthreads();
-        for (int y = ty; y < 64; y += 4)
-            if (w0 + y < f && r0 + tx < E) out[(w0 + y) * M + c * E + r0 + tx] = tile[tx][y];
-        __syncthreads();
-    }
-}
-
-// Three passes along the lines that run down the lattice's second index, A -> B -> A
-// -> B. One lane per (field, line): neighbouring lanes take neighbouring lines, so
-// every step is one coalesced read. On a transposed field these are the row passes.
-__global__ __launch_bounds__(256) void k_blur_down(float *__restrict__ a, float *__restrict__ b, int64_t fields,
-                                                   int64_t E, int64_t r)
-{
-    const int64_t lines = fields * E;
-    const int64_t M = E * E;
     for (int64_t l = (int64_t)blockIdx.x * 256 + threadIdx.x; l < lines; l += (int64_t)gridDim.x * 256) {
-        const int64_t off = (l / E) * M + l % E;
-        box_pass(a + off, b + off, E, E, r);
-        box_pass(b + off, a + off, E, E, r);
-        box_pass(a + off, b + off, E, E, r);
+        const int64_t off = (l / f) * outer + l % f;
+        box_pass(src + off, x + off, n, stride, r);
+        box_pass(x + off, y + off, n, stride, r);
+        box_pass(y + off, x + off, n, stride, r);
     }
 }
 
-// W[v0 + f][i] = num[f][i] / den[i] where den[i] > 0 (fp32; rounded once to binary16
-// for an fp16 codebook), unchanged elsewhere.
+// W[v0 + v][i] = num[i][v] / den[i] where den[i] > 0 (fp32; rounded once to binary16
+// for an fp16 codebook), unchanged elsewhere: the quotient fused with the transpose
+// from unit-major to feature-major, in 64 (units) x 64 (features) tiles through LDS.
 template <typename E>
-__global__ __launch_bounds__(256) void k_quotient(E *__restrict__ W, const float *__restrict__ num,
-                                                  const float *__restrict__ den, int64_t fields, int64_t M, int64_t v0)
+__global__ __launch_bounds__(256) void k_quotient_t(E *__restrict__ W, const float *__restrict__ num,
+                                                    const float *__restrict__ den, int64_t f, int64_t M, int64_t v0)
 {
-    const int64_t total = fields * M;
-    for (int64_t k = (int64_t)blockIdx.x * 256 + threadIdx.x; k < total; k += (int64_t)gridDim.x * 256) {
-        const int64_t i = k % M;
-        const float d = den[i];
-        if (d > 0.0f) W[v0 * M + k] = (E)(num[k] / d);
+    __shared__ float tile[64][65];
+    const int64_t it = (M + 63) / 64, vt = (f + 63) / 64;
+    const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;  // 64 x 4 threads
+    for (int64_t t = blockIdx.x; t < it * vt; t += gridDim.x) {
+        const int64_t i0 = (t / vt) * 64, w0 = (t % vt) * 64;
+        for (int y = ty; y < 64; y += 4)
+            if (i0 + y < M && w0 + tx < f) tile[y][tx] = num[(i0 + y) * f + w0 + tx];
+        __syncthreads();
+        if (i0 + tx < M) {
+            const float d = den[i0 + tx];
+            if (d > 0.0f)
+                for (int y = ty; y < 64; y += 4)
+                    if (w0 + y < f) W[(v0 + w0 + y) * M + i0 + tx] = (E)(tile[tx][y] / d);
+        }
+        __syncthreads();
     }
 }
 
@@ -397,12 +366,6 @@ __global__ __launch_bounds__(256) void k_zero_i32(int32_t *__restrict__ p, int64
 {
     for (int64_t k = (int64_t)blockIdx.x * 256 + threadIdx.x; k < n; k += (int64_t)gridDim.x * 256) p[k] = 0;
 }
-
-// Blur of `fields` lattices: counts (rows r, columns c) -> transposed fp32 (T[c][r])
-// -> row passes as passes down T -> transposed back -> column passes. Result in b.
-// unit_major: cnt is cnt[i][field] rather than cnt[field][i].
-void blur(const int32_t *cnt, bool unit_major, float *a, float *b, int64_t fields, int64_t E, int64_t r,
-          hipStream_t st);
 
 unsigned grid_for(int64_t n)
 {
@@ -412,21 +375,13 @@ unsigned grid_for(int64_t n)
     return (unsigned)b;
 }
 
-void blur(const int32_t *cnt, bool unit_major, float *a, float *b, int64_t fields, int64_t E, int64_t r,
-          hipStream_t st)
+// The blur of f unit-major lattices (E x E) of counts: three row passes, then three
+// column passes. Result in b.
+void blur(const int32_t *cnt, float *a, float *b, int64_t f, int64_t E, int64_t r, hipStream_t st)
 {
-    const int64_t tiles = fields * ((E + 63) / 64) * ((E + 63) / 64);
-    const unsigned tg = (unsigned)(tiles < (1 << 20) ? tiles : (1 << 20));
-    if (unit_major) {
-        const int64_t ut = E * ((E + 63) / 64) * ((fields + 63) / 64);
-        hipLaunchKernelGGL(k_transpose_units, dim3((unsigned)(ut < (1 << 20) ? ut : (1 << 20))), dim3(256), 0, st, cnt,
-                           a, fields, E);
-    } else {
-        hipLaunchKernelGGL(k_transpose<int32_t>, dim3(tg), dim3(256), 0, st, cnt, a, fields, E);
-    }
-    hipLaunchKernelGGL(k_blur_down, dim3(grid_for(fields * E)), dim3(256), 0, st, a, b, fields, E, r);
-    hipLaunchKernelGGL(k_transpose<float>, dim3(tg), dim3(256), 0, st, b, a, fields, E);
-    hipLaunchKernelGGL(k_blur_down, dim3(grid_for(fields * E)), dim3(256), 0, st, a, b, fields, E, r);
+    const unsigned g = grid_for(f * E);
+    hipLaunchKernelGGL(k_blur3<int32_t>, dim3(g), dim3(256), 0, st, cnt, a, b, f * E, f, E * f, E, f, r);  // -> a
+    hipLaunchKernelGGL(k_blur3<float>, dim3(g), dim3(256), 0, st, a, b, a, f * E, f, f, E, E * f, r);      // -> b
 }
 
 }  // namespace
@@ -448,7 +403,7 @@ hipError_t launch_update(bool f16, void *W, int64_t V, int64_t E, const int32_t 
                        ub.hunit);
     hipLaunchKernelGGL(k_heavy_scatter, dim3(lg), dim3(1024), 0, st, bmu, N, M, ub.start, ub.slot, ub.hunit, ub.cursor,
                        ub.order);
-    blur(ub.den_cnt, false, ub.den_a, ub.den_b, 1, E, radius, st);
+    blur(ub.den_cnt, ub.den_a, ub.den_b, 1, E, radius, st);
     const int64_t runs = (N + kRunSamples - 1) / kRunSamples;
     for (int64_t v0 = 0; v0 < V; v0 += chunk) {
         const int64_t f = V - v0 < chunk ? V - v0 : chunk;
@@ -458,13 +413,15 @@ hipError_t launch_update(bool f16, void *W, int64_t V, int64_t E, const int32_t 
         if (runs > 0)
             hipLaunchKernelGGL(k_count_heavy, dim3((unsigned)runs), dim3(256), 0, st, row_ptr, col_idx, nnz, bmu, M,
                                ub.den_cnt, ub.start, ub.order, (int32_t)v0, (int32_t)(v0 + f), ub.cnt);
-        blur(ub.cnt, true, ub.a, ub.b, f, E, radius, st);
+        blur(ub.cnt, ub.a, ub.b, f, E, radius, st);
+        const int64_t qt = ((M + 63) / 64) * ((f + 63) / 64);
+        const unsigned qg = (unsigned)(qt < (1 << 20) ? qt : (1 << 20));
         if (f16)
-            hipLaunchKernelGGL(k_quotient<_Float16>, dim3(grid_for(f * M)), dim3(256), 0, st,
-                               static_cast<_Float16 *>(W), ub.b, ub.den_b, f, M, v0);
+            hipLaunchKernelGGL(k_quotient_t<_Float16>, dim3(qg), dim3(256), 0, st, static_cast<_Float16 *>(W), ub.b,
+                               ub.den_b, f, M, v0);
         else
-            hipLaunchKernelGGL(k_quotient<float>, dim3(grid_for(f * M)), dim3(256), 0, st, static_cast<float *>(W),
-                               ub.b, ub.den_b, f, M, v0);
+            hipLaunchKernelGGL(k_quotient_t<float>, dim3(qg), dim3(256), 0, st, static_cast<float *>(W), ub.b,
+                               ub.den_b, f, M, v0);
     }
     return hipGetLastError();
 }
