@@ -24,13 +24,23 @@ FLAGS = [
 ]
 
 
-def build(verbose: bool = False) -> str:
-    tmp = LIB + ".tmp"
-    cmd = [HIPCC, *FLAGS, *SOURCES, "-o", tmp]
+# The benchmark's read-stream probe (its bandwidth denominator), a library of its own.
+PROBE_LIB = os.path.join(HERE, "libsomprobe.so")
+PROBE_SOURCES = [os.path.join(CSRC, "probe.hip")]
+
+
+def _compile(sources, out, verbose):
+    tmp = out + ".tmp"
+    cmd = [HIPCC, *FLAGS, *sources, "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
-    os.replace(tmp, LIB)
+    os.replace(tmp, out)
+
+
+def build(verbose: bool = False) -> str:
+    _compile(SOURCES, LIB, verbose)
+    _compile(PROBE_SOURCES, PROBE_LIB, verbose)
     return LIB
 
 

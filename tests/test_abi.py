@@ -30,6 +30,16 @@ def test_library_exports_every_declared_symbol():
         assert hasattr(lib, n), n
 
 
+def test_read_probe_library_loads():
+    # the benchmark's read-stream probe: its own library, one entry point, argument checks on the host
+    from paper_2608_24067_amd import build as pkg_build
+
+    lib = ctypes.CDLL(pkg_build.PROBE_LIB)
+    lib.somprobe_read.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_void_p]
+    assert lib.somprobe_read(None, 1024, None, None) != 0
+    assert lib.somprobe_read(ctypes.c_void_p(4096 + 8), 1024, ctypes.c_void_p(4096), None) != 0  # misaligned
+
+
 def test_header_constants_match_binding():
     text = open(os.path.join(ROOT, "include", "som.h")).read()
     assert re.search(r"^#define SOM_DEFAULT_TILE_SAMPLES (\d+)$", text, re.M).group(1) == str(som.DEFAULT_TILE_SAMPLES)
