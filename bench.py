@@ -107,7 +107,8 @@ def cpu_baseline(cfg, row_ptr, col_idx, W_host, budget_s: float):
 def sustained_read(dev, reps: int = 5) -> float:
     """HBM read bandwidth a plain stream reaches on this GPU: GB/s of the read-stream probe
     (16-byte loads, eight in flight per thread) over a 4 GiB buffer, far beyond the 256 MB
-    MALL; best of `reps`. The measured denominator beside the published 8 TB/s."""
+    MALL; the best of `reps` runs at each of 4, 8, 16 and 32 workgroups per CU. The measured
+    denominator beside the published 8 TB/s."""
     import ctypes
 
     import torch
@@ -117,28 +118,29 @@ def sustained_read(dev, reps: int = 5) -> float:
     if not os.path.exists(pkg_build.PROBE_LIB):
         raise RuntimeError(f"{pkg_build.PROBE_LIB} is missing: run __graft_entry__.build() first")
     lib = ctypes.CDLL(pkg_build.PROBE_LIB)
-    lib.somprobe_read.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_void_p]
+    lib.somprobe_read.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p]
     lib.somprobe_read.restype = ctypes.c_int
     nbytes = 4 << 30
     x = torch.ones(nbytes // 4, dtype=torch.float32, device=dev)
     sink = torch.zeros(1, dtype=torch.float32, device=dev)
     stream = torch.cuda.current_stream(dev)
 
-    def run():
-        rc = lib.somprobe_read(x.data_ptr(), nbytes, sink.data_ptr(), ctypes.c_void_p(stream.cuda_stream))
+    def run(per_cu):
+        rc = lib.somprobe_read(x.data_ptr(), nbytes, sink.data_ptr(), per_cu, ctypes.c_void_p(stream.cuda_stream))
         if rc != 0:
             raise RuntimeError(f"somprobe_read failed ({rc})")
 
-    run()
-    torch.cuda.synchronize()
     best = float("inf")
-    for _ in range(reps):
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        run()
-        e1.record(stream)
+    for per_cu in (4, 8, 16, 32):
+        run(per_cu)
         torch.cuda.synchronize()
-        best = min(best, e0.elapsed_time(e1))
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            run(per_cu)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            best = min(best, e0.elapsed_time(e1))
     del x, sink
     torch.cuda.empty_cache()
     return nbytes / (best / 1e3) / 1e9

@@ -35,17 +35,19 @@ __global__ __launch_bounds__(256) void k_read_stream(const v4f *__restrict__ p, 
 extern "C" {
 
 // Reads the first `bytes` bytes (rounded down to 16) of the device buffer `buf` (16-byte
-// aligned) once, on `stream`. Returns 0, or a HIP error code. `sink`: one device float,
-// written only for inputs that sum to -1.
-int somprobe_read(const void *buf, size_t bytes, float *sink, void *stream)
+// aligned) once, on `stream`, with `blocks_per_cu` workgroups of 256 threads per compute
+// unit (1 to 64). Returns 0, or a HIP error code. `sink`: one device float, written only
+// for inputs that sum to -1.
+int somprobe_read(const void *buf, size_t bytes, float *sink, int blocks_per_cu, void *stream)
 {
-    if (!buf || !sink || (reinterpret_cast<uintptr_t>(buf) & 15)) return (int)hipErrorInvalidValue;
+    if (!buf || !sink || (reinterpret_cast<uintptr_t>(buf) & 15) || blocks_per_cu < 1 || blocks_per_cu > 64)
+        return (int)hipErrorInvalidValue;
     int dev = 0, cus = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
     if (e != hipSuccess) return (int)e;
     const int64_t n = (int64_t)(bytes / 16);
-    hipLaunchKernelGGL(k_read_stream, dim3((unsigned)(cus * 8)), dim3(256), 0, static_cast<hipStream_t>(stream),
+    hipLaunchKernelGGL(k_read_stream, dim3((unsigned)(cus * blocks_per_cu)), dim3(256), 0, static_cast<hipStream_t>(stream),
                        static_cast<const v4f *>(buf), n, sink);
     return (int)hipGetLastError();
 }

@@ -35,9 +35,10 @@ def test_read_probe_library_loads():
     from paper_2608_24067_amd import build as pkg_build
 
     lib = ctypes.CDLL(pkg_build.PROBE_LIB)
-    lib.somprobe_read.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_void_p]
-    assert lib.somprobe_read(None, 1024, None, None) != 0
-    assert lib.somprobe_read(ctypes.c_void_p(4096 + 8), 1024, ctypes.c_void_p(4096), None) != 0  # misaligned
+    lib.somprobe_read.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p]
+    assert lib.somprobe_read(None, 1024, None, 8, None) != 0
+    assert lib.somprobe_read(ctypes.c_void_p(4096 + 8), 1024, ctypes.c_void_p(4096), 8, None) != 0  # misaligned
+    assert lib.somprobe_read(ctypes.c_void_p(4096), 1024, ctypes.c_void_p(4096), 0, None) != 0  # no workgroups
 
 
 def test_header_constants_match_binding():
