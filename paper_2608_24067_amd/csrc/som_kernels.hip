@@ -14,10 +14,11 @@
 // one key per (sample, strip) leaves the kernel. k_finalize takes the
 // smallest key per sample and recomputes the winner's full squared distance.
 //
-// The four waves of a sweep workgroup take four consecutive tiles of the same
-// strip, and blockIdx.y (the strip) is the slowest-varying dispatch index, so
-// the workgroups in flight all read the same narrow column range of the
-// codebook and its frequently used rows stay in L2.
+// A sweep workgroup takes groups of consecutive tiles of one strip (its four waves
+// interleaved: wave w takes tiles w, w + 4, ...; up to 32 tiles per group), and
+// blockIdx.y (the strip) is the slowest-varying dispatch index, so the workgroups
+// in flight all read the same narrow column range of the codebook and its
+// frequently used rows stay in L2.
 //
 // Keys: the order-preserving image of the fp64 pattern of d (sign flipped
 // for d >= 0, all bits flipped for d < 0), with its low 20 bits replaced by
@@ -542,8 +543,9 @@ __global__ __launch_bounds__(256) void k_plan(const int32_t *__restrict__ row_pt
 
 // ----------------------------------------------------------------- sweep
 
-// Workgroup = 4 waves = 4 consecutive tiles x one strip (blockIdx.y) of 64*NPL
-// neurons; each lane owns NPL of them, in groups of four (see loc below). VEC: M is
+// Workgroup = 4 waves x one strip (blockIdx.y) of 64*NPL neurons, over groups of
+// group_tiles consecutive tiles (a multiple of 4; groups blockIdx.x, blockIdx.x +
+// gridDim.x, ...); each lane owns NPL neurons, in groups of four (see loc below). VEC: M is
 // a multiple of 4 and W 16-byte aligned, so each group is one aligned 16-byte load.
 // The plan is read defensively (offsets, counts and ids clamped to the workspace
 // and the codebook), so even a workspace the plan never wrote cannot drive an
@@ -562,7 +564,7 @@ __global__ __launch_bounds__(256) void k_sweep(const E *__restrict__ W, const do
                                                const uint2 *__restrict__ plan, const int2 *__restrict__ tiles,
                                                int64_t n_tiles, u64 *__restrict__ keys, float *__restrict__ dots,
                                                u64 *__restrict__ keys2, float *__restrict__ dots2,
-                                               const float *__restrict__ vals)
+                                               const float *__restrict__ vals, int64_t group_tiles)
 {
     const int lane = threadIdx.x & 63;
     const int wv = wave_id();
@@ -599,13 +601,23 @@ __global__ __launch_bounds__(256) void k_sweep(const E *__restrict__ W, const do
     const float nmax = wave_max_f32(nmax_l);
     const unsigned vmax = (unsigned)(V - 1);
 
-    // Tiles t, t + 4*gridDim.x, ... of this wave. The next tile's header (its plan
+    // Tiles wv, wv + 4, ... of the workgroup's groups. The next tile's header (its plan
     // offset and union size, and the next tile's offset that bounds it) and its first
     // U plan entries are fetched while the current tile is still being worked on, so
     // no scalar-load latency sits between two tiles.
-    const int64_t tstep = 4 * (int64_t)gridDim.x;
-    int64_t t = (int64_t)blockIdx.x * 4 + wv;
+    int64_t gbeg = (int64_t)blockIdx.x * group_tiles;  // first tile of the current group
+    int64_t t = gbeg + wv;
     if (t >= n_tiles) return;  // wave-uniform; this kernel has no barriers
+    // the wave's tile after t (n_tiles when there is none), and its group's first tile
+    auto next_tile = [&](int64_t &gb) {
+        int64_t n = t + 4;
+        gb = gbeg;
+        if (n >= gbeg + group_tiles) {
+            gb = gbeg + (int64_t)gridDim.x * group_tiles;
+            n = gb + wv;
+        }
+        return n < n_tiles ? n : n_tiles;
+    };
     // header of tile tt from its table entry and the next tile's offset (nnz past the
     // last tile): a tile's union never reaches the next tile's span
     auto header = [&](int2 te, int next_off, int64_t &off_o, int &cnt_o) {
@@ -623,7 +635,8 @@ __global__ __launch_bounds__(256) void k_sweep(const E *__restrict__ W, const do
     }
     for (;;) {
         const uint2 *ent = plan + off;
-        const int64_t tn = t + tstep;
+        int64_t gbeg_n;
+        const int64_t tn = next_tile(gbeg_n);
 
         float acc[TA][NPL];
 #pragma unroll
@@ -924,6 +937,7 @@ __global__ __launch_bounds__(256) void k_sweep(const E *__restrict__ W, const do
         }
         if (tn >= n_tiles) break;
         t = tn;
+        gbeg = gbeg_n;
         off = off_n;
         cnt = cnt_n;
     }
@@ -1071,16 +1085,27 @@ hipError_t launch_plan(int ta, const int32_t *row_ptr, const int32_t *col_idx, c
 }
 
 template <typename E, int TA, int NPL, bool TOP2, bool REAL>
-static void sweep_ta(bool vec, dim3 grid, hipStream_t st, const E *W, const double *norms, int64_t M, int64_t N,
-                     int64_t V, int64_t nnz, const uint2 *plan, const int2 *tiles, int64_t nt, const SweepOut &o,
-                     const float *vals)
+static void sweep_ta(bool vec, dim3 grid, int64_t group_tiles, hipStream_t st, const E *W, const double *norms,
+                     int64_t M, int64_t N, int64_t V, int64_t nnz, const uint2 *plan, const int2 *tiles, int64_t nt,
+                     const SweepOut &o, const float *vals)
 {
     if (vec)
         hipLaunchKernelGGL((k_sweep<E, TA, NPL, 4, true, TOP2, REAL>), grid, dim3(256), 0, st, W, norms, M, N, V, nnz,
-                           plan, tiles, nt, o.keys, o.dots, o.keys2, o.dots2, vals);
+                           plan, tiles, nt, o.keys, o.dots, o.keys2, o.dots2, vals, group_tiles);
     else
         hipLaunchKernelGGL((k_sweep<E, TA, NPL, 4, false, TOP2, REAL>), grid, dim3(256), 0, st, W, norms, M, N, V, nnz,
-                           plan, tiles, nt, o.keys, o.dots, o.keys2, o.dots2, vals);
+                           plan, tiles, nt, o.keys, o.dots, o.keys2, o.dots2, vals, group_tiles);
+}
+
+// Consecutive tiles per sweep workgroup. Longer groups let a wave keep its strip's
+// norms over several tiles and keep the tiles in flight a compact stretch of the
+// (regrouped) batch, but a strip must still span many rounds of resident
+// workgroups, or the chip works on two strips at once and their rows compete for
+// L2: up to 32 tiles, and at least 16,384 groups per strip where there are enough.
+static int64_t sweep_group_tiles(int64_t nt)
+{
+    int64_t g = nt / 16384 / 4 * 4;
+    return g < 4 ? 4 : (g > 32 ? 32 : g);
 }
 
 // Vector loads need M to be a multiple of the group and W aligned to the group's bytes.
@@ -1097,27 +1122,28 @@ static hipError_t sweep_any(int ta, const E *W, const double *norms, int64_t M, 
                             hipStream_t st)
 {
     const int64_t nt = n_tiles(N, ta);
-    int64_t gx = (nt + 3) / 4;
-    if (gx > (1 << 22)) gx = 1 << 22;
+    const int64_t gt = sweep_group_tiles(nt);
+    int64_t gx = (nt + gt - 1) / gt;
+    if (gx > (1 << 20)) gx = 1 << 20;
     const dim3 grid((unsigned)gx, (unsigned)n_strips(M, ta));
     if (vals) {  // real-valued rows: tiles of 8 only (8 values per plan entry in scalar registers)
         if (ta != 8) return hipErrorInvalidValue;
-        sweep_ta<E, 8, 8, TOP2, true>(vector_loads<E, 8>(W, M), grid, st, W, norms, M, N, V, nnz, plan, tiles, nt, o,
-                                      vals);
+        sweep_ta<E, 8, 8, TOP2, true>(vector_loads<E, 8>(W, M), grid, gt, st, W, norms, M, N, V, nnz, plan, tiles,
+                                      nt, o, vals);
         return hipGetLastError();
     }
     switch (ta) {
     case 8:
-        sweep_ta<E, 8, 8, TOP2, false>(vector_loads<E, 8>(W, M), grid, st, W, norms, M, N, V, nnz, plan, tiles, nt, o,
-                                       nullptr);
+        sweep_ta<E, 8, 8, TOP2, false>(vector_loads<E, 8>(W, M), grid, gt, st, W, norms, M, N, V, nnz, plan, tiles,
+                                       nt, o, nullptr);
         break;
     case 16:
-        sweep_ta<E, 16, 4, TOP2, false>(vector_loads<E, 4>(W, M), grid, st, W, norms, M, N, V, nnz, plan, tiles, nt, o,
-                                        nullptr);
+        sweep_ta<E, 16, 4, TOP2, false>(vector_loads<E, 4>(W, M), grid, gt, st, W, norms, M, N, V, nnz, plan, tiles,
+                                        nt, o, nullptr);
         break;
     case 32:
-        sweep_ta<E, 32, 4, TOP2, false>(vector_loads<E, 4>(W, M), grid, st, W, norms, M, N, V, nnz, plan, tiles, nt, o,
-                                        nullptr);
+        sweep_ta<E, 32, 4, TOP2, false>(vector_loads<E, 4>(W, M), grid, gt, st, W, norms, M, N, V, nnz, plan, tiles,
+                                        nt, o, nullptr);
         break;
     default: return hipErrorInvalidValue;
     }
