@@ -84,6 +84,28 @@ def test_update_crowded_units(dev, seed, N, V, E, r, chunk, shares):
     assert bad.size == 0, f"{bad.size} weights differ, first {bad[:5]}"
 
 
+@pytest.mark.parametrize("seed,N,V,E,shares", [
+    (105, 6000, 200, 16, {9: 0.4}),     # a crowded unit among the skipped samples
+    (106, 3000, 150, 12, {}),           # uncrowded units only
+])
+def test_update_skips_invalid_units(dev, seed, N, V, E, shares):
+    # best units outside [0, M) are skipped: the result equals the update of the batch without those samples
+    rp, ci = synth.make_csr(seed, N, V)
+    W = synth.codebook(seed, synth.UNIFORM, V, E * E)
+    bmu = crowded_bmu(seed, N, E * E, shares)
+    rng = np.random.default_rng(seed + 1)
+    bad = rng.random(N) < 0.15
+    bmu[bad] = np.where(rng.random(int(bad.sum())) < 0.5, -1, E * E + rng.integers(0, 5, int(bad.sum())))
+    got = gpu_update(W, rp, ci, bmu, E, 2, dev)
+    keep = np.flatnonzero(~bad)
+    lens = np.diff(rp)[keep]
+    rp_k = np.zeros(keep.size + 1, np.int32)
+    np.cumsum(lens, out=rp_k[1:])
+    ci_k = np.concatenate([ci[rp[k]:rp[k + 1]] for k in keep]).astype(np.int32)
+    ref = oracle.update(W, E, rp_k, ci_k, bmu[keep], 2)
+    assert np.array_equal(got, ref)
+
+
 def test_update_f16(dev):
     rp, ci, W, bmu = update_case(99, 3000, 400, 24, spread=0.5)
     W16 = W.astype(np.float16)
