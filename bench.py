@@ -101,7 +101,21 @@ def cpu_baseline(cfg, row_ptr, col_idx, W_host, budget_s: float):
         "kind": "oracle",
         "sample": (f"first {rows} rows of the batch, whole map (dense fp64 over all V={V} features x M={M} "
                    f"neurons), {spent:.1f} s on one thread of {cpu_model()} ({os.cpu_count()} host cores)"),
+        "projected_full_batch_s": cfg.N * spent / rows,
     }
+
+
+def device_facts(dev) -> dict:
+    """What the runtime reports about the GPU the bench ran on."""
+    import torch
+
+    p = torch.cuda.get_device_properties(dev)
+    out = {"name": p.name, "arch": getattr(p, "gcnArchName", ""), "compute_units": p.multi_processor_count,
+           "hbm_GB": round(p.total_memory / 1e9, 1)}
+    l2 = getattr(p, "L2_cache_size", None)
+    if l2:
+        out["l2_MB_per_xcd"] = round(l2 / 2**20, 1)
+    return out
 
 
 def sustained_read(dev, reps: int = 5) -> float:
@@ -323,6 +337,7 @@ def main():
         "effective_codebook_GBps": eff_gbps,
         "effective_pct_of_hbm_peak": 100.0 * eff_gbps / HBM_PEAK_GBPS,
         "hbm_read_sustained_GBps": sustained,
+        "device": device_facts(dev),
         "sweep_frac_of_sustained": achieved / sustained,
         "effective_codebook_bytes_per_step": alg_bytes,
         "event_ms_per_step": step_ms,
