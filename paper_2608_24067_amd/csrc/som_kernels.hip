@@ -105,6 +105,14 @@ __device__ __forceinline__ int dpp(int x)
     return __builtin_amdgcn_update_dpp(x, x, CTRL, 0xF, 0xF, false);
 }
 
+// The same permutation for code where every lane of the wave is active: with
+// bound_ctrl set the move can fold into the instruction that uses it.
+template <int CTRL>
+__device__ __forceinline__ int dpp_all(int x)
+{
+    return __builtin_amdgcn_mov_dpp(x, CTRL, 0xF, 0xF, true);
+}
+
 template <int CTRL>
 __device__ __forceinline__ u64 dpp64(u64 x)
 {
@@ -142,19 +150,34 @@ __device__ __forceinline__ u64 wave_min_u64(u64 x)
     return r;
 }
 
-// Minimum / maximum of a float over the whole wave, as a scalar (NaN lanes are
-// ignored unless every lane is NaN).
+// Order-preserving integer image of a float (signed comparison of images = comparison
+// of finite values; -0 sorts just below +0, a NaN beyond the infinity of its sign),
+// and its inverse. Integer minima fold into DPP-modified instructions, float ones
+// would need a canonicalising move per step.
+__device__ __forceinline__ int ord_f32(float f)
+{
+    const int b = __float_as_int(f);
+    return b ^ ((b >> 31) & 0x7FFFFFFF);
+}
+__device__ __forceinline__ float from_ord_f32(int k) { return __int_as_float(k ^ ((k >> 31) & 0x7FFFFFFF)); }
+
+// Minimum of a float over the whole wave (every lane active), as a scalar, through
+// the integer images.
 __device__ __forceinline__ float wave_min_f32(float x)
 {
-    x = fminf(x, __int_as_float(dpp<0xB1>(__float_as_int(x))));
-    x = fminf(x, __int_as_float(dpp<0x4E>(__float_as_int(x))));
-    x = fminf(x, __int_as_float(dpp<0x141>(__float_as_int(x))));
-    x = fminf(x, __int_as_float(dpp<0x140>(__float_as_int(x))));
-    float r = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 0));
+    int k = ord_f32(x);
+    k = min(k, dpp_all<0xB1>(k));
+    k = min(k, dpp_all<0x4E>(k));
+    k = min(k, dpp_all<0x141>(k));
+    k = min(k, dpp_all<0x140>(k));
+    int r = __builtin_amdgcn_readlane(k, 0);
 #pragma unroll
-    for (int row = 1; row < 4; ++row) r = fminf(r, __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), row * 16)));
-    return r;
+    for (int row = 1; row < 4; ++row) r = min(r, __builtin_amdgcn_readlane(k, row * 16));
+    return from_ord_f32(r);
 }
+
+// Maximum of a float over the whole wave, as a scalar (NaN lanes are ignored unless
+// every lane is NaN).
 
 __device__ __forceinline__ float wave_max_f32(float x)
 {
@@ -177,34 +200,34 @@ __device__ __forceinline__ u64 readlane_u64(u64 x, int l)
 
 // The two smallest of the wave's values, each lane contributing the pair
 // (a1 <= a2): merging (a1, a2) with (b1, b2) keeps min(a1, b1) and
-// min(max(a1, b1), min(a2, b2)). Results are scalars.
-__device__ __forceinline__ void min2_merge(float &a1, float &a2, float b1, float b2)
+// min(max(a1, b1), min(a2, b2)). On the integer images, every lane active; results
+// are scalars.
+__device__ __forceinline__ void min2_merge(int &a1, int &a2, int b1, int b2)
 {
-    const float lo = fminf(a1, b1);
-    a2 = fminf(fmaxf(a1, b1), fminf(a2, b2));
+    const int lo = min(a1, b1);
+    a2 = min(max(a1, b1), min(a2, b2));
     a1 = lo;
 }
 
 template <int CTRL>
-__device__ __forceinline__ void min2_step(float &a1, float &a2)
+__device__ __forceinline__ void min2_step(int &a1, int &a2)
 {
-    const float b1 = __int_as_float(dpp<CTRL>(__float_as_int(a1)));
-    const float b2 = __int_as_float(dpp<CTRL>(__float_as_int(a2)));
-    min2_merge(a1, a2, b1, b2);
+    min2_merge(a1, a2, dpp_all<CTRL>(a1), dpp_all<CTRL>(a2));
 }
 
-__device__ __forceinline__ void wave_min2_f32(float a1, float a2, float &r1, float &r2)
+__device__ __forceinline__ void wave_min2_f32(float x1, float x2, float &r1, float &r2)
 {
+    int a1 = ord_f32(x1), a2 = ord_f32(x2);
     min2_step<0xB1>(a1, a2);
     min2_step<0x4E>(a1, a2);
     min2_step<0x141>(a1, a2);
     min2_step<0x140>(a1, a2);
-    r1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(a1), 0));
-    r2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(a2), 0));
+    int s1 = __builtin_amdgcn_readlane(a1, 0), s2 = __builtin_amdgcn_readlane(a2, 0);
 #pragma unroll
     for (int row = 1; row < 4; ++row)
-        min2_merge(r1, r2, __int_as_float(__builtin_amdgcn_readlane(__float_as_int(a1), row * 16)),
-                   __int_as_float(__builtin_amdgcn_readlane(__float_as_int(a2), row * 16)));
+        min2_merge(s1, s2, __builtin_amdgcn_readlane(a1, row * 16), __builtin_amdgcn_readlane(a2, row * 16));
+    r1 = from_ord_f32(s1);
+    r2 = from_ord_f32(s2);
 }
 
 // ----------------------------------------------------------------- norms
@@ -812,18 +835,24 @@ __global__ __launch_bounds__(256) void k_sweep(const E *__restrict__ W, const do
                 // neuron is added once the strip's smallest key is known.
                 u64 best = kKeyNone;
                 float bdot = 0.0f;
-#pragma unroll
-                for (int j = 0; j < NPL; ++j) {
-                    const bool cand = every || da[j] <= thr;
-                    if (__builtin_amdgcn_ballot_w64(cand)) {
-                        const double d = fma(-2.0, (double)acc[s][j], nrm[j]);
-                        const bool take = cand && base + loc(j) < Mi;
-                        const u64 key = take ? rank_key(d, (unsigned)loc(j)) : kKeyNone;
-                        if (key < best) {
-                            best = key;
-                            bdot = acc[s][j];
-                        }
+                auto visit = [&](int j, bool cand) {
+                    const double d = fma(-2.0, (double)acc[s][j], nrm[j]);
+                    const bool take = cand && base + loc(j) < Mi;
+                    const u64 key = take ? rank_key(d, (unsigned)loc(j)) : kKeyNone;
+                    if (key < best) {
+                        best = key;
+                        bdot = acc[s][j];
                     }
+                };
+                // The common case tests each neuron group with one compare and skips it
+                // when no lane holds a candidate; a non-finite bound takes every neuron.
+                if (!every) {
+#pragma unroll
+                    for (int j = 0; j < NPL; ++j)
+                        if (__builtin_amdgcn_ballot_w64(da[j] <= thr)) visit(j, da[j] <= thr);
+                } else {
+#pragma unroll
+                    for (int j = 0; j < NPL; ++j) visit(j, true);
                 }
                 // Lane s keeps sample s's smallest key over the strip and the dot
                 // product of the lane that owns it (index within the strip mod 64G =
@@ -859,23 +888,27 @@ __global__ __launch_bounds__(256) void k_sweep(const E *__restrict__ W, const do
                 const bool every = !(fabsf(thr) <= __FLT_MAX__);
                 u64 k1 = kKeyNone, k2 = kKeyNone;
                 float q1 = 0.0f, q2 = 0.0f;
-#pragma unroll
-                for (int j = 0; j < NPL; ++j) {
-                    const bool cand = every || da[j] <= thr;
-                    if (__builtin_amdgcn_ballot_w64(cand)) {
-                        const double d = fma(-2.0, (double)acc[s][j], nrm[j]);
-                        const bool take = cand && base + loc(j) < Mi;
-                        const u64 key = take ? rank_key(d, (unsigned)loc(j)) : kKeyNone;
-                        if (key < k1) {
-                            k2 = k1;
-                            q2 = q1;
-                            k1 = key;
-                            q1 = acc[s][j];
-                        } else if (key < k2) {
-                            k2 = key;
-                            q2 = acc[s][j];
-                        }
+                auto visit = [&](int j, bool cand) {
+                    const double d = fma(-2.0, (double)acc[s][j], nrm[j]);
+                    const bool take = cand && base + loc(j) < Mi;
+                    const u64 key = take ? rank_key(d, (unsigned)loc(j)) : kKeyNone;
+                    if (key < k1) {
+                        k2 = k1;
+                        q2 = q1;
+                        k1 = key;
+                        q1 = acc[s][j];
+                    } else if (key < k2) {
+                        k2 = key;
+                        q2 = acc[s][j];
                     }
+                };
+                if (!every) {
+#pragma unroll
+                    for (int j = 0; j < NPL; ++j)
+                        if (__builtin_amdgcn_ballot_w64(da[j] <= thr)) visit(j, da[j] <= thr);
+                } else {
+#pragma unroll
+                    for (int j = 0; j < NPL; ++j) visit(j, true);
                 }
                 // The two smallest keys of the wave (keys are distinct: each holds its
                 // neuron index), with the dot products of their neurons.
