@@ -120,6 +120,26 @@ def test_empty_rows_rank_by_norm(dev):
     compare(W, rp, ci, b, d, exact=False, what="empty rows")
 
 
+@pytest.mark.parametrize("two_best", [False, True])
+def test_overflowing_fp32_norms(dev, two_best):
+    # Weights of 3e19 square beyond the fp32 range: those neurons' fp32 norms, and so the
+    # strip's bound, are infinite, which sends the strip's neurons to the exact fp64
+    # stage. Strip 1 (neurons 512..599) is all huge; strip 0 has a few huge neurons.
+    from parity import compare2, gpu_run2
+
+    rp, ci, W = case(131, 400, 300, 600, synth.QUANTISED)
+    W[:, 512:] = 3e19
+    W[:40, [3, 77, 300]] = 3e19
+    if two_best:
+        g = gpu_run2(W, rp, ci, dev)
+        compare2(W, rp, ci, g, exact=False, what="overflowing norms, two best")
+        assert (g[0] < 512).all() and (g[2] < 512).all()
+    else:
+        b, d, _ = gpu_run(W, rp, ci, dev)
+        compare(W, rp, ci, b, d, exact=False, what="overflowing norms")
+        assert (b < 512).all() and not np.isin(b, [3, 77, 300]).any()
+
+
 def test_single_neuron(dev):
     rp, ci, W = case(36, 100, 300, 1, synth.QUANTISED)
     b, d, _ = gpu_run(W, rp, ci, dev)
