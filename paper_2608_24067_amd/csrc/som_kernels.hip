@@ -93,6 +93,12 @@ __device__ __forceinline__ int64_t clamp64(int64_t x, int64_t lo, int64_t hi) { 
 // from it (tile index, plan entries, masks) would be treated as divergent.
 __device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }
 
+// A compile-time bool carried as a type, for lambdas instantiated twice.
+template <bool B>
+struct StaticBool {
+    static constexpr bool value = B;
+};
+
 // ---- cross-lane helpers (DPP within a row of 16 lanes, readlane across rows)
 
 // dpp_ctrl codes: quad_perm [1,0,3,2] = 0xB1 (lane ^ 1), quad_perm [2,3,0,1] = 0x4E
@@ -121,14 +127,15 @@ __device__ __forceinline__ u64 dpp64(u64 x)
     return ((u64)(unsigned)hi << 32) | (unsigned)lo;
 }
 
-// Minimum over each aligned group of G lanes (G = 2, 4, 8, 16 or 32), in every lane of the group.
+// Minimum over each aligned group of G lanes (G = 2, 4, 8, 16 or 32), in every lane of the
+// group; every lane of the wave active.
 template <int G>
 __device__ __forceinline__ int group_min_i32(int x)
 {
-    x = min(x, dpp<0xB1>(x));
-    if (G >= 4) x = min(x, dpp<0x4E>(x));
-    if (G >= 8) x = min(x, dpp<0x141>(x));
-    if (G >= 16) x = min(x, dpp<0x140>(x));
+    x = min(x, dpp_all<0xB1>(x));
+    if (G >= 4) x = min(x, dpp_all<0x4E>(x));
+    if (G >= 8) x = min(x, dpp_all<0x141>(x));
+    if (G >= 16) x = min(x, dpp_all<0x140>(x));
     if (G >= 32) x = min(x, __shfl_xor(x, 16));
     return x;
 }
@@ -515,48 +522,63 @@ __global__ __launch_bounds__(256) void k_plan(const int32_t *__restrict__ row_pt
         int cur = INT_MAX;
         float curv = 0.0f;
         double sq = 0.0;
-        // next valid id of this lane's row (INT_MAX once the row is done), with its value
-        auto fetch = [&]() {
-            cur = INT_MAX;
-            while (p < e) {
-                const int id = staged ? stage[wv][p - wlo] : col_idx[base + p];
-                if (id >= 0 && id < V) {
-                    cur = id;
-                    if (values) {
-                        curv = values[base + p];
-                        sq = fma((double)curv, (double)curv, sq);
+        int64_t k = 0;  // union entries written for this lane's tile (equal across its group)
+        // The merge, in two copies: ids read from the LDS stage or from global memory.
+        // (One copy with a select between the two pointers becomes a flat load that
+        // waits on both memory counters at every step.)
+        auto merge = [&](auto from_stage) {
+            constexpr bool STAGED = decltype(from_stage)::value;
+            // next valid id of this lane's row (INT_MAX once the row is done), with its value
+            auto fetch = [&]() {
+                cur = INT_MAX;
+                while (p < e) {
+                    int id;
+                    if constexpr (STAGED)
+                        id = stage[wv][p - wlo];
+                    else
+                        id = col_idx[base + p];
+                    if (id >= 0 && id < V) {
+                        cur = id;
+                        if (values) {
+                            curv = values[base + p];
+                            sq = fma((double)curv, (double)curv, sq);
+                        }
+                        break;
                     }
-                    break;
+                    bad |= SOM_FLAG_ID_RANGE;
+                    ++p;
                 }
-                bad |= SOM_FLAG_ID_RANGE;
-                ++p;
+            };
+            fetch();
+            const int64_t cap = hi - lo;
+            while (true) {
+                int m = group_min_i32<TA>(cur);
+                if (m != INT_MAX && k >= cap) {  // only reachable with repeated or unsorted ids
+                    bad |= SOM_FLAG_UNSORTED;
+                    p = e;
+                    cur = INT_MAX;
+                    m = INT_MAX;
+                }
+                if (__ballot(m != INT_MAX) == 0) break;
+                const u64 bal = __ballot(m != INT_MAX && cur == m);
+                const unsigned mask =
+                    (unsigned)((bal >> (grp * TA)) & (TA == 32 ? 0xFFFFFFFFull : ((1ull << TA) - 1)));
+                if (m != INT_MAX) {
+                    if (sl == 0) plan[lo + k] = make_uint2((unsigned)m, mask);
+                    if (values && cur == m) vals[(lo + k) * TA + sl] = curv;
+                    ++k;
+                    if (cur == m) {
+                        ++p;
+                        fetch();
+                        if (cur != INT_MAX && cur <= m) bad |= SOM_FLAG_UNSORTED;
+                    }
+                }
             }
         };
-        fetch();
-        const int64_t cap = hi - lo;
-        int64_t k = 0;  // union entries written for this lane's tile (equal across its group)
-        while (true) {
-            int m = group_min_i32<TA>(cur);
-            if (m != INT_MAX && k >= cap) {  // only reachable with repeated or unsorted ids
-                bad |= SOM_FLAG_UNSORTED;
-                p = e;
-                cur = INT_MAX;
-                m = INT_MAX;
-            }
-            if (__ballot(m != INT_MAX) == 0) break;
-            const u64 bal = __ballot(m != INT_MAX && cur == m);
-            const unsigned mask = (unsigned)((bal >> (grp * TA)) & (TA == 32 ? 0xFFFFFFFFull : ((1ull << TA) - 1)));
-            if (m != INT_MAX) {
-                if (sl == 0) plan[lo + k] = make_uint2((unsigned)m, mask);
-                if (values && cur == m) vals[(lo + k) * TA + sl] = curv;
-                ++k;
-                if (cur == m) {
-                    ++p;
-                    fetch();
-                    if (cur != INT_MAX && cur <= m) bad |= SOM_FLAG_UNSORTED;
-                }
-            }
-        }
+        if (staged)
+            merge(StaticBool<true>{});
+        else
+            merge(StaticBool<false>{});
         if (live && sl == 0) tiles[t] = make_int2((int)lo, (int)k);
         if (values && live && t * TA + sl < N) xsq[t * TA + sl] = sq;
         __syncthreads();

@@ -120,6 +120,35 @@ def test_empty_rows_rank_by_norm(dev):
     compare(W, rp, ci, b, d, exact=False, what="empty rows")
 
 
+def long_rows(seed, N, V, lo, hi):
+    # rows of lo..hi sorted distinct ids: a wave's 64 rows then hold more ids than
+    # the plan stages in LDS, so the plan reads them from global memory
+    rng = np.random.default_rng(seed)
+    lens = rng.integers(lo, hi + 1, N)
+    rp = np.zeros(N + 1, np.int32)
+    np.cumsum(lens, out=rp[1:])
+    ci = np.concatenate([np.sort(rng.choice(V, n, replace=False)) for n in lens]).astype(np.int32)
+    return rp, ci
+
+
+@pytest.mark.parametrize("tile,keep", [(8, False), (16, False), (32, True)])
+def test_long_rows_plan_from_global_memory(dev, tile, keep):
+    rp, ci = long_rows(141, 300, 600, 30, 70)
+    W = synth.codebook(141, synth.QUANTISED, 600, 700)
+    b, d, _ = gpu_run(W, rp, ci, dev, tile_samples=tile, keep_order=keep)
+    compare(W, rp, ci, b, d, exact=True, what=f"long rows tile {tile}")
+
+
+def test_long_rows_real_values(dev):
+    from parity import compare_sf, gpu_run_sf
+
+    rp, ci = long_rows(142, 200, 500, 30, 70)
+    W = synth.codebook(142, synth.QUANTISED, 500, 300)
+    vals = synth.values(142, len(ci), synth.VAL_QUANTISED)
+    g = gpu_run_sf(W, rp, ci, vals, dev)
+    compare_sf(W, rp, ci, vals, g, exact=True, what="long rows, real values")
+
+
 @pytest.mark.parametrize("two_best", [False, True])
 def test_overflowing_fp32_norms(dev, two_best):
     # Weights of 3e19 square beyond the fp32 range: those neurons' fp32 norms, and so the
