@@ -339,19 +339,26 @@ __global__ __launch_bounds__(256) void k_rarest(const int32_t *__restrict__ row_
                                                 int32_t *__restrict__ skey, u64 *__restrict__ bucket,
                                                 uint32_t *__restrict__ flags)
 {
+    // the four lanes of a quad share a row (lane q of the quad takes ids q, q + 4, ...)
     const int64_t base = row_ptr[0];
+    const int sub = threadIdx.x & 3;
     uint32_t bad = 0;
-    for (int64_t s = (int64_t)blockIdx.x * 256 + threadIdx.x; s < N; s += (int64_t)gridDim.x * 256) {
+    for (int64_t s = (int64_t)blockIdx.x * 64 + (threadIdx.x >> 2); s < N; s += (int64_t)gridDim.x * 64) {
         int64_t rb, re;
         row_range(row_ptr, base, nnz, s, rb, re, bad);
         u64 best = kKeyNone;  // (frequency, V-1-id): smallest frequency, then largest id
-        for (int64_t p = rb; p < re; ++p) {
+        for (int64_t p = rb + sub; p < re; p += 4) {
             const int id = col_idx[base + p];
             if (id >= 0 && id < V) best = min_u64(best, ((u64)freq[id] << 32) | (unsigned)(V - 1 - id));
         }
-        const int key = best == kKeyNone ? V : (int)(V - 1 - (int)(unsigned)(best & 0xFFFFFFFFull));
-        skey[s] = key;
-        atomicAdd(&bucket[key], (1ull << 32) | (u64)(re - rb));
+        // the quad is active or idle as a whole (one row), so the swaps read its own lanes
+        best = min_u64(best, dpp64<0xB1>(best));
+        best = min_u64(best, dpp64<0x4E>(best));
+        if (sub == 0) {
+            const int key = best == kKeyNone ? V : (int)(V - 1 - (int)(unsigned)(best & 0xFFFFFFFFull));
+            skey[s] = key;
+            atomicAdd(&bucket[key], (1ull << 32) | (u64)(re - rb));
+        }
     }
     if (bad) atomicOr(flags, bad);
 }
@@ -411,17 +418,24 @@ __global__ __launch_bounds__(256) void k_place(const int32_t *__restrict__ row_p
 }
 
 // Position k copies the ids of sample perm[k] to pci[prp[k] ...] (and its values to
-// pvals, for real-valued rows): consecutive threads write consecutive rows. Sample
-// indices and offsets are re-checked, so positions never placed (invalid input
-// only) cannot drive an access out of bounds.
+// pvals, for real-valued rows). kGatherLanes lanes share a row, each taking every
+// kGatherLanes-th id, so one load instruction reads a few contiguous pieces of 16
+// rows instead of one id of each of 64 rows. Sample indices and offsets are
+// re-checked, so positions never placed (invalid input only) cannot drive an access
+// out of bounds.
+constexpr int kGatherLanes = 4;
+
 __global__ __launch_bounds__(256) void k_gather(const int32_t *__restrict__ row_ptr, const int32_t *__restrict__ col_idx,
                                                 int64_t N, int64_t nnz, const int32_t *__restrict__ perm,
                                                 const int32_t *__restrict__ prp, int32_t *__restrict__ pci,
                                                 const float *__restrict__ values, float *__restrict__ pvals)
 {
     const int64_t base = row_ptr[0];
+    const int sub = threadIdx.x % kGatherLanes;
+    constexpr int64_t per_block = 256 / kGatherLanes;
     uint32_t bad = 0;
-    for (int64_t k = (int64_t)blockIdx.x * 256 + threadIdx.x; k < N; k += (int64_t)gridDim.x * 256) {
+    for (int64_t k = (int64_t)blockIdx.x * per_block + threadIdx.x / kGatherLanes; k < N;
+         k += (int64_t)gridDim.x * per_block) {
         const int64_t s = perm[k];
         if (s < 0 || s >= N) continue;
         int64_t rb, re;
@@ -430,26 +444,11 @@ __global__ __launch_bounds__(256) void k_gather(const int32_t *__restrict__ row_
         const int64_t n = re - rb < nnz - dst ? re - rb : nnz - dst;
         const int32_t *src = col_idx + base + rb;
         int32_t *out = pci + dst;
-        // the first 16 ids: all loads issued before the first store
-        int32_t v[16];
-#pragma unroll
-        for (int q = 0; q < 16; ++q)
-            if (q < n) v[q] = src[q];
-#pragma unroll
-        for (int q = 0; q < 16; ++q)
-            if (q < n) out[q] = v[q];
-        for (int64_t q = 16; q < n; ++q) out[q] = src[q];
+        for (int64_t q = sub; q < n; q += kGatherLanes) out[q] = src[q];
         if (values) {
             const float *vs = values + base + rb;
             float *vo = pvals + dst;
-            float x[16];
-#pragma unroll
-            for (int q = 0; q < 16; ++q)
-                if (q < n) x[q] = vs[q];
-#pragma unroll
-            for (int q = 0; q < 16; ++q)
-                if (q < n) vo[q] = x[q];
-            for (int64_t q = 16; q < n; ++q) vo[q] = vs[q];
+            for (int64_t q = sub; q < n; q += kGatherLanes) vo[q] = vs[q];
         }
     }
 }
@@ -1250,12 +1249,16 @@ hipError_t launch_order(const int32_t *row_ptr, const int32_t *col_idx, const fl
     hipLaunchKernelGGL(k_freq, dim3((unsigned)hb), dim3(256), 0, st, row_ptr, col_idx, counted, (int32_t)V, ob.freq);
     int64_t sb = (N + 255) / 256;
     if (sb > (1 << 22)) sb = 1 << 22;
-    hipLaunchKernelGGL(k_rarest, dim3((unsigned)sb), dim3(256), 0, st, row_ptr, col_idx, N, nnz, (int32_t)V, ob.freq,
+    int64_t qb = (N + 63) / 64;  // a row per quad of lanes
+    if (qb > (1 << 22)) qb = 1 << 22;
+    hipLaunchKernelGGL(k_rarest, dim3((unsigned)qb), dim3(256), 0, st, row_ptr, col_idx, N, nnz, (int32_t)V, ob.freq,
                        ob.skey, ob.bucket, flags);
     hipLaunchKernelGGL(k_bucket_scan, dim3(1), dim3(1024), 0, st, ob.bucket, nb, nnz, ob.prp + N);
     hipLaunchKernelGGL(k_place, dim3((unsigned)sb), dim3(256), 0, st, row_ptr, N, nnz, ob.skey, ob.bucket, ob.perm,
                        ob.prp);
-    hipLaunchKernelGGL(k_gather, dim3((unsigned)sb), dim3(256), 0, st, row_ptr, col_idx, N, nnz, ob.perm, ob.prp,
+    int64_t gb = (N + 256 / kGatherLanes - 1) / (256 / kGatherLanes);
+    if (gb > (1 << 22)) gb = 1 << 22;
+    hipLaunchKernelGGL(k_gather, dim3((unsigned)gb), dim3(256), 0, st, row_ptr, col_idx, N, nnz, ob.perm, ob.prp,
                        ob.pci, values, values ? ob.pvals : nullptr);
     return hipGetLastError();
 }
