@@ -241,21 +241,26 @@ __device__ __forceinline__ void wave_min2_f32(float x1, float x2, float &r1, flo
 
 // n_i = sum_v W[v*M+i]^2: one thread per neuron, v ascending, fp64. The square of
 // an fp32 (or fp16) value is exact in fp64, so fma(w, w, acc) equals acc + w*w.
+// One wave per workgroup, so a small map (M = 4096: 64 waves) still spreads over
+// 64 compute units, and kNormLoads rows in flight per wave: the sums are sequential,
+// the loads are not.
+constexpr int kNormLoads = 32;
+
 template <typename E>
-__global__ __launch_bounds__(256) void k_norms(const E *__restrict__ W, int64_t V, int64_t M,
-                                               double *__restrict__ norms)
+__global__ __launch_bounds__(64) void k_norms(const E *__restrict__ W, int64_t V, int64_t M,
+                                              double *__restrict__ norms)
 {
-    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    const int64_t i = (int64_t)blockIdx.x * 64 + threadIdx.x;
     if (i >= M) return;
     const E *p = W + i;
     double acc = 0.0;
     int64_t v = 0;
-    for (; v + 8 <= V; v += 8) {
-        float w[8];
+    for (; v + kNormLoads <= V; v += kNormLoads) {
+        float w[kNormLoads];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) w[u] = (float)__builtin_nontemporal_load(p + (v + u) * M);
+        for (int u = 0; u < kNormLoads; ++u) w[u] = (float)__builtin_nontemporal_load(p + (v + u) * M);
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
+        for (int u = 0; u < kNormLoads; ++u) {
             const double x = (double)w[u];
             acc = fma(x, x, acc);
         }
@@ -1091,15 +1096,15 @@ __global__ __launch_bounds__(256) void k_finalize2(const double *__restrict__ no
 
 hipError_t launch_norms(const float *W, int64_t V, int64_t M, double *norms, hipStream_t st)
 {
-    const int64_t blocks = (M + 255) / 256;
-    hipLaunchKernelGGL(k_norms<float>, dim3((unsigned)blocks), dim3(256), 0, st, W, V, M, norms);
+    const int64_t blocks = (M + 63) / 64;
+    hipLaunchKernelGGL(k_norms<float>, dim3((unsigned)blocks), dim3(64), 0, st, W, V, M, norms);
     return hipGetLastError();
 }
 
 hipError_t launch_norms_f16(const uint16_t *W, int64_t V, int64_t M, double *norms, hipStream_t st)
 {
-    const int64_t blocks = (M + 255) / 256;
-    hipLaunchKernelGGL(k_norms<_Float16>, dim3((unsigned)blocks), dim3(256), 0, st,
+    const int64_t blocks = (M + 63) / 64;
+    hipLaunchKernelGGL(k_norms<_Float16>, dim3((unsigned)blocks), dim3(64), 0, st,
                        reinterpret_cast<const _Float16 *>(W), V, M, norms);
     return hipGetLastError();
 }
