@@ -106,6 +106,14 @@ def test_update_skips_invalid_units(dev, seed, N, V, E, shares):
     assert np.array_equal(got, ref)
 
 
+def test_update_empty_batch_keeps_codebook(dev):
+    # no samples: every blurred den is zero, so every prototype stays as it was
+    W = synth.codebook(107, synth.UNIFORM, 50, 64)
+    rp = np.zeros(1, np.int32)
+    got = gpu_update(W, rp, np.zeros(0, np.int32), np.zeros(0, np.int32), 8, 2, dev)
+    assert np.array_equal(got, W)
+
+
 def test_update_f16(dev):
     rp, ci, W, bmu = update_case(99, 3000, 400, 24, spread=0.5)
     W16 = W.astype(np.float16)
