@@ -522,11 +522,15 @@ __global__ __launch_bounds__(256) void k_plan(const int32_t *__restrict__ row_pt
             for (int64_t q = lane; q < whi - wlo; q += 64) stage[wv][q] = col_idx[base + wlo + q];
         __syncthreads();
 
-        int64_t p = b;
+        // positions in 32 bits: every offset lies in [0, nnz] and nnz < 2^31
+        const int32_t *ids = col_idx + base;
+        const float *vsrc = values ? values + base : nullptr;
+        int p = (int)b;
+        const int pe = (int)e, plo = (int)lo, pwlo = (int)wlo;
         int cur = INT_MAX;
         float curv = 0.0f;
         double sq = 0.0;
-        int64_t k = 0;  // union entries written for this lane's tile (equal across its group)
+        int k = 0;  // union entries written for this lane's tile (equal across its group)
         // The merge, in two copies: ids read from the LDS stage or from global memory.
         // (One copy with a select between the two pointers becomes a flat load that
         // waits on both memory counters at every step.)
@@ -535,16 +539,16 @@ __global__ __launch_bounds__(256) void k_plan(const int32_t *__restrict__ row_pt
             // next valid id of this lane's row (INT_MAX once the row is done), with its value
             auto fetch = [&]() {
                 cur = INT_MAX;
-                while (p < e) {
+                while (p < pe) {
                     int id;
                     if constexpr (STAGED)
-                        id = stage[wv][p - wlo];
+                        id = stage[wv][p - pwlo];
                     else
-                        id = col_idx[base + p];
+                        id = ids[p];
                     if (id >= 0 && id < V) {
                         cur = id;
                         if (values) {
-                            curv = values[base + p];
+                            curv = vsrc[p];
                             sq = fma((double)curv, (double)curv, sq);
                         }
                         break;
@@ -554,12 +558,12 @@ __global__ __launch_bounds__(256) void k_plan(const int32_t *__restrict__ row_pt
                 }
             };
             fetch();
-            const int64_t cap = hi - lo;
+            const int cap = (int)(hi - lo);
             while (true) {
                 int m = group_min_i32<TA>(cur);
                 if (m != INT_MAX && k >= cap) {  // only reachable with repeated or unsorted ids
                     bad |= SOM_FLAG_UNSORTED;
-                    p = e;
+                    p = pe;
                     cur = INT_MAX;
                     m = INT_MAX;
                 }
@@ -568,8 +572,8 @@ __global__ __launch_bounds__(256) void k_plan(const int32_t *__restrict__ row_pt
                 const unsigned mask =
                     (unsigned)((bal >> (grp * TA)) & (TA == 32 ? 0xFFFFFFFFull : ((1ull << TA) - 1)));
                 if (m != INT_MAX) {
-                    if (sl == 0) plan[lo + k] = make_uint2((unsigned)m, mask);
-                    if (values && cur == m) vals[(lo + k) * TA + sl] = curv;
+                    if (sl == 0) plan[plo + k] = make_uint2((unsigned)m, mask);
+                    if (values && cur == m) vals[(int64_t)(plo + k) * TA + sl] = curv;
                     ++k;
                     if (cur == m) {
                         ++p;
