@@ -9,6 +9,8 @@ codebooks.
 """
 from __future__ import annotations
 
+import os
+
 import numpy as np
 from scipy.spatial.distance import cdist
 
@@ -444,6 +446,44 @@ def check_update_impulse_and_pair(lib):
     assert np.allclose(got2[0][k1 == 1.0] + got2[5][k1 == 1.0], 1.0, rtol=0, atol=1e-6)
 
 
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+
+def check_update_kernel_width(lib):
+    """The kernel of the update, read out of the oracle: one sample with feature 0 at the centre unit c of a
+    (12r+1)^2 lattice, one sample with feature 1 at every unit. Where c's kernel reaches, every unit's all-ones
+    blur is (2r+1)^6 (its whole support lies inside), so the new feature-0 weight is k/(k + (2r+1)^6) and gives back
+    the integer kernel k. It must be separable, symmetric, of mass (2r+1)^6, of variance exactly r(r+1) per axis
+    (three convolved uniforms on [-r, r]) -- and of the standard deviation the paper gives for three passes of
+    half-width r (Section 3.4), the values in golden/box_blur_width.txt."""
+    rows = [ln.split() for ln in open(os.path.join(GOLDEN, "box_blur_width.txt")) if ln.strip() and ln[0] != "#"]
+    assert rows, "golden file is empty"
+    for r_txt, width_txt in rows:
+        r, width = int(r_txt), float(width_txt)
+        E = 12 * r + 1
+        M, c = E * E, 6 * r
+        rp = np.arange(M + 2, dtype=np.int32)
+        ci = np.array([0] + [1] * M, dtype=np.int32)
+        bmu = np.array([c * E + c] + list(range(M)), dtype=np.int32)
+        W = synth.codebook(31, synth.UNIFORM, 2, M)
+        q = oracle.update(W, E, rp, ci, bmu, r, lib=lib)[0].reshape(E, E).astype(np.float64)
+        C = float((2 * r + 1) ** 6)
+        with np.errstate(divide="ignore", invalid="ignore"):  # a broken oracle may return q = 1
+            k = q * C / (1.0 - q)
+        kr = np.rint(k)
+        assert np.isfinite(k).all() and np.abs(k - kr).max() < 1e-3, f"r={r}: feature-0 weights are not k/(k+C) of an integer kernel"
+        kr = kr.astype(np.int64)
+        assert (kr[np.abs(np.arange(E) - c) > 3 * r, :] == 0).all() and (kr[:, np.abs(np.arange(E) - c) > 3 * r] == 0).all()
+        assert kr.sum() == (2 * r + 1) ** 6, f"r={r}: kernel mass"
+        assert np.array_equal(kr, kr.T) and np.array_equal(kr, kr[::-1, ::-1]), f"r={r}: kernel symmetry"
+        a = kr.sum(axis=0)
+        assert np.array_equal(kr * a.sum(), np.outer(a, a)), f"r={r}: kernel not separable"
+        d = np.arange(E) - c
+        var2 = int((a * d * d).sum())  # var * mass, exact
+        assert var2 == r * (r + 1) * int(a.sum()), f"r={r}: variance {var2 / a.sum()} != r(r+1)"
+        assert abs(np.sqrt(var2 / a.sum()) - width) <= 0.1, f"r={r}: width {np.sqrt(var2 / a.sum())} vs {width}"
+
+
 ALL_CHECKS = [
     check_exact_integer_direct,
     check_cdist_node_major,
@@ -466,4 +506,5 @@ ALL_CHECKS = [
     check_sf_cdist_and_planted,
     check_update_direct_windows,
     check_update_impulse_and_pair,
+    check_update_kernel_width,
 ]

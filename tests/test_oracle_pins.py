@@ -4,8 +4,10 @@ Parity of the HIP path is judged against the oracle, so the oracle is pinned
 first, by checks that do not re-use its own formula (tests/oracle_pins.py),
 and by a mutation check: each plausible slip planted in a copy of oracle.c
 (wrong sign, dropped square, dropped term, transposed stride, wrong
-tie-break, lost block offset, wrong second best, dropped feature, and the
-rank-2/rank-3 slips of the two-best oracle) must make at least one pin fail.
+tie-break, lost block offset, wrong second best, dropped feature, the
+rank-2/rank-3 slips of the two-best oracle, the value slips of the
+real-valued oracle, and the window, pass and quotient slips of the update)
+must make at least one pin fail.
 """
 import os
 import subprocess
