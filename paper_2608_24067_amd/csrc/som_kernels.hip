@@ -403,57 +403,48 @@ __global__ __launch_bounds__(1024) void k_bucket_scan(u64 *__restrict__ bucket, 
     if (t == 1023) *prp_end = (int32_t)(si[1023] < nnz ? si[1023] : nnz);
 }
 
-// Each sample takes the next (position, id offset) of its bucket with one atomic.
-// Positions past N (only reachable with invalid row pointers) are dropped.
-__global__ __launch_bounds__(256) void k_place(const int32_t *__restrict__ row_ptr, int64_t N, int64_t nnz,
-                                               const int32_t *__restrict__ skey, u64 *__restrict__ bucket,
-                                               int32_t *__restrict__ perm, int32_t *__restrict__ prp)
+// Each sample takes the next (position, id offset) of its bucket with one atomic and
+// copies its ids (and values, for real-valued rows) there: position k of the
+// permuted batch holds sample perm[k], whose ids start at pci[prp[k]]. A quad of
+// lanes shares a row: its first lane takes the atomic, the quad copies every
+// fourth id, so the reads of row_ptr and col_idx run in batch order and only the
+// writes scatter, as whole rows. Positions past N and id offsets past nnz (only
+// reachable with invalid row pointers) are dropped or clamped.
+constexpr int kPlaceLanes = 4;
+
+__global__ __launch_bounds__(256) void k_place(const int32_t *__restrict__ row_ptr, const int32_t *__restrict__ col_idx,
+                                               int64_t N, int64_t nnz, const int32_t *__restrict__ skey,
+                                               u64 *__restrict__ bucket, int32_t *__restrict__ perm,
+                                               int32_t *__restrict__ prp, int32_t *__restrict__ pci,
+                                               const float *__restrict__ values, float *__restrict__ pvals)
 {
     const int64_t base = row_ptr[0];
+    const int sub = threadIdx.x % kPlaceLanes;
+    constexpr int64_t per_block = 256 / kPlaceLanes;
     uint32_t bad = 0;
-    for (int64_t s = (int64_t)blockIdx.x * 256 + threadIdx.x; s < N; s += (int64_t)gridDim.x * 256) {
+    for (int64_t s = (int64_t)blockIdx.x * per_block + threadIdx.x / kPlaceLanes; s < N;
+         s += (int64_t)gridDim.x * per_block) {
         int64_t rb, re;
         row_range(row_ptr, base, nnz, s, rb, re, bad);
-        const u64 old = atomicAdd(&bucket[skey[s]], (1ull << 32) | (u64)(re - rb));
+        u64 old = 0;
+        if (sub == 0) old = atomicAdd(&bucket[skey[s]], (1ull << 32) | (u64)(re - rb));
+        // the quad is active or idle as a whole (one row): its lanes read lane 0's word
+        old = dpp64<0x00>(old);
         const int64_t ps = (int64_t)(old >> 32), pi = (int64_t)(old & 0xFFFFFFFFull);
         if (ps >= N) continue;
-        perm[ps] = (int32_t)s;
-        prp[ps] = (int32_t)(pi < nnz ? pi : nnz);
-    }
-}
-
-// Position k copies the ids of sample perm[k] to pci[prp[k] ...] (and its values to
-// pvals, for real-valued rows). kGatherLanes lanes share a row, each taking every
-// kGatherLanes-th id, so one load instruction reads a few contiguous pieces of 16
-// rows instead of one id of each of 64 rows. Sample indices and offsets are
-// re-checked, so positions never placed (invalid input only) cannot drive an access
-// out of bounds.
-constexpr int kGatherLanes = 4;
-
-__global__ __launch_bounds__(256) void k_gather(const int32_t *__restrict__ row_ptr, const int32_t *__restrict__ col_idx,
-                                                int64_t N, int64_t nnz, const int32_t *__restrict__ perm,
-                                                const int32_t *__restrict__ prp, int32_t *__restrict__ pci,
-                                                const float *__restrict__ values, float *__restrict__ pvals)
-{
-    const int64_t base = row_ptr[0];
-    const int sub = threadIdx.x % kGatherLanes;
-    constexpr int64_t per_block = 256 / kGatherLanes;
-    uint32_t bad = 0;
-    for (int64_t k = (int64_t)blockIdx.x * per_block + threadIdx.x / kGatherLanes; k < N;
-         k += (int64_t)gridDim.x * per_block) {
-        const int64_t s = perm[k];
-        if (s < 0 || s >= N) continue;
-        int64_t rb, re;
-        row_range(row_ptr, base, nnz, s, rb, re, bad);
-        const int64_t dst = clamp64(prp[k], 0, nnz);
+        const int64_t dst = pi < nnz ? pi : nnz;
+        if (sub == 0) {
+            perm[ps] = (int32_t)s;
+            prp[ps] = (int32_t)dst;
+        }
         const int64_t n = re - rb < nnz - dst ? re - rb : nnz - dst;
         const int32_t *src = col_idx + base + rb;
         int32_t *out = pci + dst;
-        for (int64_t q = sub; q < n; q += kGatherLanes) out[q] = src[q];
+        for (int64_t q = sub; q < n; q += kPlaceLanes) out[q] = src[q];
         if (values) {
             const float *vs = values + base + rb;
             float *vo = pvals + dst;
-            for (int64_t q = sub; q < n; q += kGatherLanes) vo[q] = vs[q];
+            for (int64_t q = sub; q < n; q += kPlaceLanes) vo[q] = vs[q];
         }
     }
 }
@@ -1256,19 +1247,15 @@ hipError_t launch_order(const int32_t *row_ptr, const int32_t *col_idx, const fl
     if (hb < 1) hb = 1;
     if (hb > 1024) hb = 1024;
     hipLaunchKernelGGL(k_freq, dim3((unsigned)hb), dim3(256), 0, st, row_ptr, col_idx, counted, (int32_t)V, ob.freq);
-    int64_t sb = (N + 255) / 256;
-    if (sb > (1 << 22)) sb = 1 << 22;
     int64_t qb = (N + 63) / 64;  // a row per quad of lanes
     if (qb > (1 << 22)) qb = 1 << 22;
     hipLaunchKernelGGL(k_rarest, dim3((unsigned)qb), dim3(256), 0, st, row_ptr, col_idx, N, nnz, (int32_t)V, ob.freq,
                        ob.skey, ob.bucket, flags);
     hipLaunchKernelGGL(k_bucket_scan, dim3(1), dim3(1024), 0, st, ob.bucket, nb, nnz, ob.prp + N);
-    hipLaunchKernelGGL(k_place, dim3((unsigned)sb), dim3(256), 0, st, row_ptr, N, nnz, ob.skey, ob.bucket, ob.perm,
-                       ob.prp);
-    int64_t gb = (N + 256 / kGatherLanes - 1) / (256 / kGatherLanes);
-    if (gb > (1 << 22)) gb = 1 << 22;
-    hipLaunchKernelGGL(k_gather, dim3((unsigned)gb), dim3(256), 0, st, row_ptr, col_idx, N, nnz, ob.perm, ob.prp,
-                       ob.pci, values, values ? ob.pvals : nullptr);
+    int64_t pb = (N + 256 / kPlaceLanes - 1) / (256 / kPlaceLanes);
+    if (pb > (1 << 22)) pb = 1 << 22;
+    hipLaunchKernelGGL(k_place, dim3((unsigned)pb), dim3(256), 0, st, row_ptr, col_idx, N, nnz, ob.skey, ob.bucket,
+                       ob.perm, ob.prp, ob.pci, values, values ? ob.pvals : nullptr);
     return hipGetLastError();
 }
 
