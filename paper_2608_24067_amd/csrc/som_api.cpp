@@ -113,7 +113,11 @@ som_status carve(void *ws, size_t bytes, int64_t N, int64_t M, int64_t V, int64_
     c->ob.freq = reinterpret_cast<uint32_t *>(b + L.freq);
     c->ob.bucket = reinterpret_cast<unsigned long long *>(b + L.bucket);
     c->ob.skey = reinterpret_cast<int32_t *>(b + L.skey);
-    c->ob.perm = reinterpret_cast<int32_t *>(b + L.perm);
+    c->ob.inv = reinterpret_cast<int32_t *>(b + L.inv);
+    c->ob.rbmu = reinterpret_cast<int32_t *>(b + L.rbmu);
+    c->ob.rdist = reinterpret_cast<double *>(b + L.rdist);
+    c->ob.rbmu2 = k.layout_top2() ? reinterpret_cast<int32_t *>(b + L.rbmu2) : nullptr;
+    c->ob.rdist2 = k.layout_top2() ? reinterpret_cast<double *>(b + L.rdist2) : nullptr;
     c->ob.prp = reinterpret_cast<int32_t *>(b + L.prp);
     c->ob.pci = reinterpret_cast<int32_t *>(b + L.pci);
     c->ob.pvals = k.real ? reinterpret_cast<float *>(b + L.pvals) : nullptr;
@@ -236,8 +240,7 @@ som_status finalize_impl(const Kind &k, const double *norms, int64_t V, int64_t 
     if ((st = setup(N, M, V, nnz, config, workspace, workspace_bytes, k, &o, &c, &noop)) != SOM_OK) return st;
     if (noop) return ok();
     const int32_t *rp = o.order ? c.ob.prp : row_ptr;
-    const int32_t *perm = o.order ? c.ob.perm : nullptr;
-    hipError_t e = som::launch_finalize(o.ta, norms, M, rp, N, nnz, perm, c.xsq, c.out, bmu, dist,
+    hipError_t e = som::launch_finalize(o.ta, norms, M, rp, N, nnz, o.order ? &c.ob : nullptr, c.xsq, c.out, bmu, dist,
                                         k.top2 ? bmu2 : nullptr, k.top2 ? dist2 : nullptr,
                                         static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, who);

@@ -32,11 +32,15 @@ struct Layout {
     size_t freq;    // uint32 [V+1]: feature counts of the batch
     size_t bucket;  // uint64 [V+1]: per-bucket (samples << 32 | ids) counts, then offsets
     size_t skey;    // int32 [N]: each sample's bucket
-    size_t perm;    // int32 [N]: sample at each position of the ordered batch
+    size_t inv;     // int32 [N]: each sample's position in the ordered batch (-1: never placed)
     size_t prp;     // int32 [N+1]: row pointers of the ordered batch
     size_t pci;     // int32 [nnz]: feature ids of the ordered batch
+    size_t rbmu;    // int32 [N]: best unit by position, before the results go back to input order
+    size_t rdist;   // double [N]: its distance
     size_t keys2;   // uint64 [n_strips * N]: per-strip second-smallest keys (two-best search only)
     size_t dots2;   // float [n_strips * N]: their dot products (two-best search only)
+    size_t rbmu2;   // int32 [N]: second unit by position (two-best search, ordered batch only)
+    size_t rdist2;  // double [N]: its distance
     size_t vals;    // float [nnz * TA]: sample values of every plan entry (real-valued rows only)
     size_t xsq;     // double [N]: ||x||^2 by batch position (real-valued rows only)
     size_t pvals;   // float [nnz]: values of the ordered batch (real-valued rows, regrouped only)
@@ -66,12 +70,16 @@ inline Layout layout_for(int64_t N, int64_t M, int64_t V, int64_t nnz, int ta, b
     L.freq = take(o * (size_t)(V + 1) * 4);
     L.bucket = take(o * (size_t)(V + 1) * 8);
     L.skey = take(o * (size_t)N * 4);
-    L.perm = take(o * (size_t)N * 4);
+    L.inv = take(o * (size_t)N * 4);
     L.prp = take(o * (size_t)(N + 1) * 4);
     L.pci = take(o * (size_t)nnz * 4);
+    L.rbmu = take(o * (size_t)N * 4);
+    L.rdist = take(o * (size_t)N * 8);
     const size_t t2 = top2 ? 1 : 0;
     L.keys2 = take(t2 * (size_t)n_strips(M, ta) * (size_t)N * 8);
     L.dots2 = take(t2 * (size_t)n_strips(M, ta) * (size_t)N * 4);
+    L.rbmu2 = take(t2 * o * (size_t)N * 4);
+    L.rdist2 = take(t2 * o * (size_t)N * 8);
     const size_t r = real ? 1 : 0;
     L.vals = take(r * (size_t)nnz * (size_t)ta * 4);
     L.xsq = take(r * (size_t)N * 8);
@@ -83,7 +91,9 @@ inline Layout layout_for(int64_t N, int64_t M, int64_t V, int64_t nnz, int ta, b
 struct OrderBuffers {
     uint32_t *freq;
     unsigned long long *bucket;
-    int32_t *skey, *perm, *prp, *pci;
+    int32_t *skey, *inv, *prp, *pci;
+    int32_t *rbmu, *rbmu2;  // results by position (rbmu2: two-best only)
+    double *rdist, *rdist2;
     float *pvals;  // real-valued rows only
 };
 
@@ -109,8 +119,10 @@ hipError_t launch_sweep(int ta, bool f16, bool top2, const void *W, const double
                         int64_t V, int64_t nnz, const uint2 *plan, const int2 *tiles, const float *vals,
                         const SweepOut &o, hipStream_t st);
 // bmu2/dist2 non-null: the two best units. xsq: real-valued rows (else ||x||^2 = nnz of the row).
+// ob non-null: the batch was regrouped (row_ptr is the ordered batch's); results are staged by
+// position and then moved to their samples.
 hipError_t launch_finalize(int ta, const double *norms, int64_t M, const int32_t *row_ptr, int64_t N, int64_t nnz,
-                           const int32_t *perm, const double *xsq, const SweepOut &o, int32_t *bmu, double *dist,
+                           const OrderBuffers *ob, const double *xsq, const SweepOut &o, int32_t *bmu, double *dist,
                            int32_t *bmu2, double *dist2, hipStream_t st);
 hipError_t launch_order(const int32_t *row_ptr, const int32_t *col_idx, const float *values, int64_t N, int64_t nnz,
                         int64_t V, const OrderBuffers &ob, uint32_t *flags, hipStream_t st);

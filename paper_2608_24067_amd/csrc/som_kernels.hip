@@ -283,7 +283,7 @@ __global__ void k_clear_flags(uint32_t *flags) { flags[threadIdx.x] = 0u; }
 // codebook row is re-read while still in L2. A sample's result does not depend on where it
 // sits (its sum order is fixed by its own features), so the permutation never
 // shows in the output. The permuted batch is written to the workspace as a CSR
-// of its own (prp, pci); k_finalize maps positions back to samples.
+// of its own (prp, pci); k_unpermute moves the results back to their samples.
 
 constexpr int kLdsHistMax = 32768;          // features whose counts fit the LDS histogram
 constexpr int64_t kFreqSample = 1ll << 25;  // ids counted: the ordering needs only a rough rarity rank
@@ -404,8 +404,8 @@ __global__ __launch_bounds__(1024) void k_bucket_scan(u64 *__restrict__ bucket, 
 }
 
 // Each sample takes the next (position, id offset) of its bucket with one atomic and
-// copies its ids (and values, for real-valued rows) there: position k of the
-// permuted batch holds sample perm[k], whose ids start at pci[prp[k]]. A quad of
+// copies its ids (and values, for real-valued rows) there: sample s sits at position
+// inv[s] of the permuted batch, its ids from pci[prp[inv[s]]] on. A quad of
 // lanes shares a row: its first lane takes the atomic, the quad copies every
 // fourth id, so the reads of row_ptr and col_idx run in batch order and only the
 // writes scatter, as whole rows. Positions past N and id offsets past nnz (only
@@ -414,7 +414,7 @@ constexpr int kPlaceLanes = 4;
 
 __global__ __launch_bounds__(256) void k_place(const int32_t *__restrict__ row_ptr, const int32_t *__restrict__ col_idx,
                                                int64_t N, int64_t nnz, const int32_t *__restrict__ skey,
-                                               u64 *__restrict__ bucket, int32_t *__restrict__ perm,
+                                               u64 *__restrict__ bucket, int32_t *__restrict__ inv,
                                                int32_t *__restrict__ prp, int32_t *__restrict__ pci,
                                                const float *__restrict__ values, float *__restrict__ pvals)
 {
@@ -431,12 +431,10 @@ __global__ __launch_bounds__(256) void k_place(const int32_t *__restrict__ row_p
         // the quad is active or idle as a whole (one row): its lanes read lane 0's word
         old = dpp64<0x00>(old);
         const int64_t ps = (int64_t)(old >> 32), pi = (int64_t)(old & 0xFFFFFFFFull);
+        if (sub == 0) inv[s] = ps < N ? (int32_t)ps : -1;
         if (ps >= N) continue;
         const int64_t dst = pi < nnz ? pi : nnz;
-        if (sub == 0) {
-            perm[ps] = (int32_t)s;
-            prp[ps] = (int32_t)dst;
-        }
+        if (sub == 0) prp[ps] = (int32_t)dst;
         const int64_t n = re - rb < nnz - dst ? re - rb : nnz - dst;
         const int32_t *src = col_idx + base + rb;
         int32_t *out = pci + dst;
@@ -1003,33 +1001,39 @@ __global__ __launch_bounds__(256) void k_sweep(const E *__restrict__ W, const do
 // strips; the winner's dot product comes from the sweep (the same fp32 sum of the
 // row's weights in ascending feature order), so the full squared distance is
 // (||w||^2 - 2*dot) + ||x||^2, with ||x||^2 = nnz for binary rows and xsq[k] from the
-// plan for real-valued ones. Results go to sample perm[k] (k without a permutation).
+// plan for real-valued ones. Results are written by position (k_unpermute then moves
+// them to their samples when the batch was regrouped): every write coalesced.
+constexpr int kFinalizeBatch = 8;  // strips whose keys one lane loads at once
+
 __global__ __launch_bounds__(256) void k_finalize(const double *__restrict__ norms, int64_t M,
                                                   const int32_t *__restrict__ row_ptr, int64_t N, int64_t nnz,
-                                                  const int32_t *__restrict__ perm, const double *__restrict__ xsq,
+                                                  const double *__restrict__ xsq,
                                                   const u64 *__restrict__ keys,
                                                   const float *__restrict__ dots, int64_t n_strips,
                                                   int32_t *__restrict__ bmu, double *__restrict__ dist)
 {
     const int64_t base = row_ptr[0];
     for (int64_t k = (int64_t)blockIdx.x * 256 + threadIdx.x; k < N; k += (int64_t)gridDim.x * 256) {
-        const int64_t s = perm ? (int64_t)perm[k] : k;
-        if (s < 0 || s >= N) continue;
         u64 best = kKeyNone;
         int64_t gb = 0;
-        for (int64_t g = 0; g < n_strips; ++g) {
-            const u64 key = keys[g * N + k];
-            if (key < best) {
-                best = key;
-                gb = g;
-            }
+        for (int64_t g0 = 0; g0 < n_strips; g0 += kFinalizeBatch) {
+            // a batch of strips' keys loaded before any is compared
+            u64 kk[kFinalizeBatch];
+#pragma unroll
+            for (int j = 0; j < kFinalizeBatch; ++j) kk[j] = g0 + j < n_strips ? keys[(g0 + j) * N + k] : kKeyNone;
+#pragma unroll
+            for (int j = 0; j < kFinalizeBatch; ++j)
+                if (kk[j] < best) {
+                    best = kk[j];
+                    gb = g0 + j;
+                }
         }
         int64_t b = (int64_t)(best & kIndexMask);
         if (b >= M) b = M - 1;
         const int64_t rb = clamp64((int64_t)row_ptr[k] - base, 0, nnz);
         const int64_t re = clamp64((int64_t)row_ptr[k + 1] - base, rb, nnz);
-        bmu[s] = (int32_t)b;
-        dist[s] = fma(-2.0, (double)dots[gb * N + k], norms[b]) + (xsq ? xsq[k] : (double)(re - rb));
+        bmu[k] = (int32_t)b;
+        dist[k] = fma(-2.0, (double)dots[gb * N + k], norms[b]) + (xsq ? xsq[k] : (double)(re - rb));
     }
 }
 
@@ -1038,7 +1042,7 @@ __global__ __launch_bounds__(256) void k_finalize(const double *__restrict__ nor
 // unit (M == 1) bmu2 = -1 and dist2 = +inf.
 __global__ __launch_bounds__(256) void k_finalize2(const double *__restrict__ norms, int64_t M,
                                                    const int32_t *__restrict__ row_ptr, int64_t N, int64_t nnz,
-                                                   const int32_t *__restrict__ perm, const double *__restrict__ xsq,
+                                                   const double *__restrict__ xsq,
                                                    const u64 *__restrict__ keys,
                                                    const float *__restrict__ dots, const u64 *__restrict__ keys2,
                                                    const float *__restrict__ dots2, int64_t n_strips,
@@ -1047,8 +1051,6 @@ __global__ __launch_bounds__(256) void k_finalize2(const double *__restrict__ no
 {
     const int64_t base = row_ptr[0];
     for (int64_t k = (int64_t)blockIdx.x * 256 + threadIdx.x; k < N; k += (int64_t)gridDim.x * 256) {
-        const int64_t s = perm ? (int64_t)perm[k] : k;
-        if (s < 0 || s >= N) continue;
         u64 b1 = kKeyNone, b2 = kKeyNone;
         float q1 = 0.0f, q2 = 0.0f;
         auto offer = [&](u64 key, float q) {
@@ -1062,25 +1064,62 @@ __global__ __launch_bounds__(256) void k_finalize2(const double *__restrict__ no
                 q2 = q;
             }
         };
-        for (int64_t g = 0; g < n_strips; ++g) {
-            offer(keys[g * N + k], dots[g * N + k]);
-            offer(keys2[g * N + k], dots2[g * N + k]);
+        for (int64_t g0 = 0; g0 < n_strips; g0 += kFinalizeBatch) {
+            // a batch of strips' candidates loaded before any is offered, offered in strip order
+            u64 k1[kFinalizeBatch], k2[kFinalizeBatch];
+            float d1[kFinalizeBatch], d2[kFinalizeBatch];
+#pragma unroll
+            for (int j = 0; j < kFinalizeBatch; ++j) {
+                const bool in = g0 + j < n_strips;
+                const int64_t at = (g0 + j) * N + k;
+                k1[j] = in ? keys[at] : kKeyNone;
+                d1[j] = in ? dots[at] : 0.0f;
+                k2[j] = in ? keys2[at] : kKeyNone;
+                d2[j] = in ? dots2[at] : 0.0f;
+            }
+#pragma unroll
+            for (int j = 0; j < kFinalizeBatch; ++j) {
+                offer(k1[j], d1[j]);
+                offer(k2[j], d2[j]);
+            }
         }
         const int64_t rb = clamp64((int64_t)row_ptr[k] - base, 0, nnz);
         const int64_t re = clamp64((int64_t)row_ptr[k + 1] - base, rb, nnz);
         const double len = xsq ? xsq[k] : (double)(re - rb);
         int64_t i1 = (int64_t)(b1 & kIndexMask);
         if (i1 >= M) i1 = M - 1;
-        bmu[s] = (int32_t)i1;
-        dist[s] = fma(-2.0, (double)q1, norms[i1]) + len;
+        bmu[k] = (int32_t)i1;
+        dist[k] = fma(-2.0, (double)q1, norms[i1]) + len;
         if (b2 == kKeyNone) {
-            bmu2[s] = -1;
-            dist2[s] = __builtin_inf();
+            bmu2[k] = -1;
+            dist2[k] = __builtin_inf();
         } else {
             int64_t i2 = (int64_t)(b2 & kIndexMask);
             if (i2 >= M) i2 = M - 1;
-            bmu2[s] = (int32_t)i2;
-            dist2[s] = fma(-2.0, (double)q2, norms[i2]) + len;
+            bmu2[k] = (int32_t)i2;
+            dist2[k] = fma(-2.0, (double)q2, norms[i2]) + len;
+        }
+    }
+}
+
+// Results of a regrouped batch back to input order: sample s takes what position inv[s]
+// got (bmu2/dist2 too when given). A sample never placed (inv[s] = -1, invalid row
+// pointers only) is left untouched. Reads gather, writes run in sample order.
+__global__ __launch_bounds__(256) void k_unpermute(const int32_t *__restrict__ inv, int64_t N,
+                                                   const int32_t *__restrict__ rbmu, const double *__restrict__ rdist,
+                                                   const int32_t *__restrict__ rbmu2,
+                                                   const double *__restrict__ rdist2, int32_t *__restrict__ bmu,
+                                                   double *__restrict__ dist, int32_t *__restrict__ bmu2,
+                                                   double *__restrict__ dist2)
+{
+    for (int64_t s = (int64_t)blockIdx.x * 256 + threadIdx.x; s < N; s += (int64_t)gridDim.x * 256) {
+        const int64_t k = inv[s];
+        if (k < 0 || k >= N) continue;
+        bmu[s] = rbmu[k];
+        dist[s] = rdist[k];
+        if (bmu2) {
+            bmu2[s] = rbmu2[k];
+            dist2[s] = rdist2[k];
         }
     }
 }
@@ -1219,17 +1258,23 @@ hipError_t launch_sweep(int ta, bool f16, bool top2, const void *W, const double
 }
 
 hipError_t launch_finalize(int ta, const double *norms, int64_t M, const int32_t *row_ptr, int64_t N, int64_t nnz,
-                           const int32_t *perm, const double *xsq, const SweepOut &o, int32_t *bmu, double *dist,
+                           const OrderBuffers *ob, const double *xsq, const SweepOut &o, int32_t *bmu, double *dist,
                            int32_t *bmu2, double *dist2, hipStream_t st)
 {
     int64_t blocks = (N + 255) / 256;
     if (blocks > (1 << 22)) blocks = 1 << 22;
+    // a regrouped batch is finalized by position into the workspace first
+    int32_t *fb = ob ? ob->rbmu : bmu, *fb2 = ob ? ob->rbmu2 : bmu2;
+    double *fd = ob ? ob->rdist : dist, *fd2 = ob ? ob->rdist2 : dist2;
     if (bmu2)
-        hipLaunchKernelGGL(k_finalize2, dim3((unsigned)blocks), dim3(256), 0, st, norms, M, row_ptr, N, nnz, perm, xsq,
-                           o.keys, o.dots, o.keys2, o.dots2, n_strips(M, ta), bmu, dist, bmu2, dist2);
+        hipLaunchKernelGGL(k_finalize2, dim3((unsigned)blocks), dim3(256), 0, st, norms, M, row_ptr, N, nnz, xsq,
+                           o.keys, o.dots, o.keys2, o.dots2, n_strips(M, ta), fb, fd, fb2, fd2);
     else
-        hipLaunchKernelGGL(k_finalize, dim3((unsigned)blocks), dim3(256), 0, st, norms, M, row_ptr, N, nnz, perm, xsq,
-                           o.keys, o.dots, n_strips(M, ta), bmu, dist);
+        hipLaunchKernelGGL(k_finalize, dim3((unsigned)blocks), dim3(256), 0, st, norms, M, row_ptr, N, nnz, xsq,
+                           o.keys, o.dots, n_strips(M, ta), fb, fd);
+    if (ob)
+        hipLaunchKernelGGL(k_unpermute, dim3((unsigned)blocks), dim3(256), 0, st, ob->inv, N, fb, fd,
+                           bmu2 ? fb2 : nullptr, bmu2 ? fd2 : nullptr, bmu, dist, bmu2, dist2);
     return hipGetLastError();
 }
 
@@ -1255,7 +1300,7 @@ hipError_t launch_order(const int32_t *row_ptr, const int32_t *col_idx, const fl
     int64_t pb = (N + 256 / kPlaceLanes - 1) / (256 / kPlaceLanes);
     if (pb > (1 << 22)) pb = 1 << 22;
     hipLaunchKernelGGL(k_place, dim3((unsigned)pb), dim3(256), 0, st, row_ptr, col_idx, N, nnz, ob.skey, ob.bucket,
-                       ob.perm, ob.prp, ob.pci, values, values ? ob.pvals : nullptr);
+                       ob.inv, ob.prp, ob.pci, values, values ? ob.pvals : nullptr);
     return hipGetLastError();
 }
 
