@@ -352,9 +352,18 @@ __global__ __launch_bounds__(256) void k_rarest(const int32_t *__restrict__ row_
         int64_t rb, re;
         row_range(row_ptr, base, nnz, s, rb, re, bad);
         u64 best = kKeyNone;  // (frequency, V-1-id): smallest frequency, then largest id
-        for (int64_t p = rb + sub; p < re; p += 4) {
-            const int id = col_idx[base + p];
-            if (id >= 0 && id < V) best = min_u64(best, ((u64)freq[id] << 32) | (unsigned)(V - 1 - id));
+        // three of the lane's ids, then their counts, per step: a row of up to 12 ids is one
+        // round trip of dependent loads instead of three
+        for (int64_t p = rb + sub; p < re; p += 12) {
+            int id[3];
+#pragma unroll
+            for (int j = 0; j < 3; ++j) id[j] = p + 4 * j < re ? col_idx[base + p + 4 * j] : -1;
+            unsigned f[3];
+#pragma unroll
+            for (int j = 0; j < 3; ++j) f[j] = id[j] >= 0 && id[j] < V ? freq[id[j]] : 0u;
+#pragma unroll
+            for (int j = 0; j < 3; ++j)
+                if (id[j] >= 0 && id[j] < V) best = min_u64(best, ((u64)f[j] << 32) | (unsigned)(V - 1 - id[j]));
         }
         // the quad is active or idle as a whole (one row), so the swaps read its own lanes
         best = min_u64(best, dpp64<0xB1>(best));
@@ -1003,7 +1012,8 @@ __global__ __launch_bounds__(256) void k_sweep(const E *__restrict__ W, const do
 // (||w||^2 - 2*dot) + ||x||^2, with ||x||^2 = nnz for binary rows and xsq[k] from the
 // plan for real-valued ones. Results are written by position (k_unpermute then moves
 // them to their samples when the batch was regrouped): every write coalesced.
-constexpr int kFinalizeBatch = 8;  // strips whose keys one lane loads at once
+constexpr int kFinalizeBatch = 8;   // strips whose keys one lane loads at once
+constexpr int kFinalize2Batch = 4;  // the same for the two-best search (four words per strip)
 
 __global__ __launch_bounds__(256) void k_finalize(const double *__restrict__ norms, int64_t M,
                                                   const int32_t *__restrict__ row_ptr, int64_t N, int64_t nnz,
@@ -1064,12 +1074,12 @@ __global__ __launch_bounds__(256) void k_finalize2(const double *__restrict__ no
                 q2 = q;
             }
         };
-        for (int64_t g0 = 0; g0 < n_strips; g0 += kFinalizeBatch) {
+        for (int64_t g0 = 0; g0 < n_strips; g0 += kFinalize2Batch) {
             // a batch of strips' candidates loaded before any is offered, offered in strip order
-            u64 k1[kFinalizeBatch], k2[kFinalizeBatch];
-            float d1[kFinalizeBatch], d2[kFinalizeBatch];
+            u64 k1[kFinalize2Batch], k2[kFinalize2Batch];
+            float d1[kFinalize2Batch], d2[kFinalize2Batch];
 #pragma unroll
-            for (int j = 0; j < kFinalizeBatch; ++j) {
+            for (int j = 0; j < kFinalize2Batch; ++j) {
                 const bool in = g0 + j < n_strips;
                 const int64_t at = (g0 + j) * N + k;
                 k1[j] = in ? keys[at] : kKeyNone;
@@ -1078,7 +1088,7 @@ __global__ __launch_bounds__(256) void k_finalize2(const double *__restrict__ no
                 d2[j] = in ? dots2[at] : 0.0f;
             }
 #pragma unroll
-            for (int j = 0; j < kFinalizeBatch; ++j) {
+            for (int j = 0; j < kFinalize2Batch; ++j) {
                 offer(k1[j], d1[j]);
                 offer(k2[j], d2[j]);
             }
