@@ -470,11 +470,11 @@ constexpr int kPlanStage = 2048;  // ids staged in LDS per wave
 // writes more entries than its own CSR span, so no input can drive an access out
 // of bounds.
 //
-// Real-valued rows (values != nullptr): every union entry also gets the TA values of
+// Real-valued rows (REAL, values given): every union entry also gets the TA values of
 // its samples (vals[entry*TA + s], written for the samples whose mask bit is set;
 // the other slots are never read), and every row the fp64 sum of its squared
 // values in its own order (xsq, by batch position), which is ||x||^2.
-template <int TA>
+template <int TA, bool REAL>
 __global__ __launch_bounds__(256) void k_plan(const int32_t *__restrict__ row_ptr, const int32_t *__restrict__ col_idx,
                                               int64_t N, int64_t nnz, int32_t V, int64_t n_tiles,
                                               uint2 *__restrict__ plan, int2 *__restrict__ tiles,
@@ -522,7 +522,7 @@ __global__ __launch_bounds__(256) void k_plan(const int32_t *__restrict__ row_pt
 
         // positions in 32 bits: every offset lies in [0, nnz] and nnz < 2^31
         const int32_t *ids = col_idx + base;
-        const float *vsrc = values ? values + base : nullptr;
+        const float *vsrc = REAL ? values + base : nullptr;
         int p = (int)b;
         const int pe = (int)e, plo = (int)lo, pwlo = (int)wlo;
         int cur = INT_MAX;
@@ -534,25 +534,30 @@ __global__ __launch_bounds__(256) void k_plan(const int32_t *__restrict__ row_pt
         // waits on both memory counters at every step.)
         auto merge = [&](auto from_stage) {
             constexpr bool STAGED = decltype(from_stage)::value;
-            // next valid id of this lane's row (INT_MAX once the row is done), with its value
+            auto id_at = [&](int q) {
+                if constexpr (STAGED)
+                    return stage[wv][q - pwlo];
+                else
+                    return ids[q];
+            };
+            // next valid id of this lane's row (INT_MAX once the row is done), with its value;
+            // ids outside [0, V) (invalid input) are skipped on a path of their own
             auto fetch = [&]() {
                 cur = INT_MAX;
-                while (p < pe) {
-                    int id;
-                    if constexpr (STAGED)
-                        id = stage[wv][p - pwlo];
-                    else
-                        id = ids[p];
-                    if (id >= 0 && id < V) {
-                        cur = id;
-                        if (values) {
-                            curv = vsrc[p];
-                            sq = fma((double)curv, (double)curv, sq);
-                        }
-                        break;
+                if (p >= pe) return;
+                int id = id_at(p);
+                if (id < 0 || id >= V) {
+                    for (;;) {
+                        bad |= SOM_FLAG_ID_RANGE;
+                        if (++p >= pe) return;
+                        id = id_at(p);
+                        if (id >= 0 && id < V) break;
                     }
-                    bad |= SOM_FLAG_ID_RANGE;
-                    ++p;
+                }
+                cur = id;
+                if constexpr (REAL) {
+                    curv = vsrc[p];
+                    sq = fma((double)curv, (double)curv, sq);
                 }
             };
             fetch();
@@ -571,7 +576,7 @@ __global__ __launch_bounds__(256) void k_plan(const int32_t *__restrict__ row_pt
                     (unsigned)((bal >> (grp * TA)) & (TA == 32 ? 0xFFFFFFFFull : ((1ull << TA) - 1)));
                 if (m != INT_MAX) {
                     if (sl == 0) plan[plo + k] = make_uint2((unsigned)m, mask);
-                    if (values && cur == m) vals[(int64_t)(plo + k) * TA + sl] = curv;
+                    if (REAL && cur == m) vals[(int64_t)(plo + k) * TA + sl] = curv;
                     ++k;
                     if (cur == m) {
                         ++p;
@@ -586,7 +591,7 @@ __global__ __launch_bounds__(256) void k_plan(const int32_t *__restrict__ row_pt
         else
             merge(StaticBool<false>{});
         if (live && sl == 0) tiles[t] = make_int2((int)lo, (int)k);
-        if (values && live && t * TA + sl < N) xsq[t * TA + sl] = sq;
+        if (REAL && live && t * TA + sl < N) xsq[t * TA + sl] = sq;
         __syncthreads();
     }
     if (bad) atomicOr(flags, bad);
@@ -1169,18 +1174,24 @@ hipError_t launch_plan(int ta, const int32_t *row_ptr, const int32_t *col_idx, c
     if (blocks > (1 << 22)) blocks = 1 << 22;
     const dim3 grid((unsigned)blocks), block(256);
     const int32_t v = (int32_t)V;
+    if (values) {  // real-valued rows: tiles of 8 only
+        if (ta != 8) return hipErrorInvalidValue;
+        hipLaunchKernelGGL((k_plan<8, true>), grid, block, 0, st, row_ptr, col_idx, N, nnz, v, nt, plan, tiles, flags,
+                           values, vals, xsq);
+        return hipGetLastError();
+    }
     switch (ta) {
     case 8:
-        hipLaunchKernelGGL(k_plan<8>, grid, block, 0, st, row_ptr, col_idx, N, nnz, v, nt, plan, tiles, flags, values,
-                           vals, xsq);
+        hipLaunchKernelGGL((k_plan<8, false>), grid, block, 0, st, row_ptr, col_idx, N, nnz, v, nt, plan, tiles, flags,
+                           nullptr, nullptr, nullptr);
         break;
     case 16:
-        hipLaunchKernelGGL(k_plan<16>, grid, block, 0, st, row_ptr, col_idx, N, nnz, v, nt, plan, tiles, flags, values,
-                           vals, xsq);
+        hipLaunchKernelGGL((k_plan<16, false>), grid, block, 0, st, row_ptr, col_idx, N, nnz, v, nt, plan, tiles,
+                           flags, nullptr, nullptr, nullptr);
         break;
     case 32:
-        hipLaunchKernelGGL(k_plan<32>, grid, block, 0, st, row_ptr, col_idx, N, nnz, v, nt, plan, tiles, flags, values,
-                           vals, xsq);
+        hipLaunchKernelGGL((k_plan<32, false>), grid, block, 0, st, row_ptr, col_idx, N, nnz, v, nt, plan, tiles,
+                           flags, nullptr, nullptr, nullptr);
         break;
     default: return hipErrorInvalidValue;
     }
