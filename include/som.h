@@ -73,7 +73,13 @@ typedef enum {
 /* Largest map the 20-bit index field of the argmin key can address. */
 #define SOM_MAX_NEURONS (1 << 20)
 
-/* Bits reported by som_bmu_input_flags. */
+/* Bits reported by som_bmu_input_flags. A flagged batch breaks the CSR
+ * preconditions; its results are defined only as far as stated here: an id
+ * outside [0, V) is left out of the row's dot products (the binary row's
+ * ||x||^2, its length, still counts it), and rows with valid ids get the
+ * results they get in a valid batch. Rows with unsorted or repeated ids, and
+ * every row of a batch with bad row pointers, get in-range but unspecified
+ * results; no input drives an access out of bounds. */
 #define SOM_FLAG_ID_RANGE 0x1u   /* a feature id outside [0, V) was skipped      */
 #define SOM_FLAG_UNSORTED 0x2u   /* a row's ids were not strictly ascending       */
 #define SOM_FLAG_ROW_PTR 0x4u    /* row_ptr decreased or left [row_ptr[0], +nnz]  */

@@ -561,22 +561,21 @@ __global__ __launch_bounds__(256) void k_plan(const int32_t *__restrict__ row_pt
                 }
             };
             fetch();
+            // Every step consumes at least one id of the group, so a tile takes at most as many
+            // steps as its span holds ids; only lanes whose ranges overlap (row pointers that
+            // decrease, flagged above) take more, and their surplus entries are dropped.
             const int cap = (int)(hi - lo);
             while (true) {
-                int m = group_min_i32<TA>(cur);
-                if (m != INT_MAX && k >= cap) {  // only reachable with repeated or unsorted ids
-                    bad |= SOM_FLAG_UNSORTED;
-                    p = pe;
-                    cur = INT_MAX;
-                    m = INT_MAX;
-                }
+                const int m = group_min_i32<TA>(cur);
                 if (__ballot(m != INT_MAX) == 0) break;
                 const u64 bal = __ballot(m != INT_MAX && cur == m);
                 const unsigned mask =
                     (unsigned)((bal >> (grp * TA)) & (TA == 32 ? 0xFFFFFFFFull : ((1ull << TA) - 1)));
                 if (m != INT_MAX) {
-                    if (sl == 0) plan[plo + k] = make_uint2((unsigned)m, mask);
-                    if (REAL && cur == m) vals[(int64_t)(plo + k) * TA + sl] = curv;
+                    if (k < cap) {
+                        if (sl == 0) plan[plo + k] = make_uint2((unsigned)m, mask);
+                        if (REAL && cur == m) vals[(int64_t)(plo + k) * TA + sl] = curv;
+                    }
                     ++k;
                     if (cur == m) {
                         ++p;
@@ -590,7 +589,7 @@ __global__ __launch_bounds__(256) void k_plan(const int32_t *__restrict__ row_pt
             merge(StaticBool<true>{});
         else
             merge(StaticBool<false>{});
-        if (live && sl == 0) tiles[t] = make_int2((int)lo, (int)k);
+        if (live && sl == 0) tiles[t] = make_int2((int)lo, k < (int)(hi - lo) ? k : (int)(hi - lo));
         if (REAL && live && t * TA + sl < N) xsq[t * TA + sl] = sq;
         __syncthreads();
     }

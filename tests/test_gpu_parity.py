@@ -202,6 +202,53 @@ def test_phases_equal_search_and_flags_clean(dev):
     assert torch.equal(b1, b2) and torch.equal(d1, d2)
 
 
+
+@pytest.mark.parametrize("tile,keep", [(8, False), (16, True), (32, False)])
+def test_invalid_ids_are_flagged_and_stay_local(dev, tile, keep):
+    """Ids outside [0, V), unsorted and repeated ids, with valid row pointers: the plan flags them; an id outside
+    [0, V) is left out of the dot products (its row ranks as the row without it; the row's length, its ||x||^2,
+    still counts it), and every other valid row's result is that of the clean batch, bit for bit (a row's result
+    depends on its own ids only)."""
+    V, M, N = 500, 1300, 300
+    rp, ci, W = case(41, N, V, M, synth.UNIFORM)
+    rows = [list(ci[rp[s]:rp[s + 1]]) for s in range(N)]
+    multi = [s for s in range(N) if len(rows[s]) >= 3]
+    r_hi, r_neg, r_uns, r_dup = multi[1], multi[40], multi[90], multi[-1]
+    bad, clean = [list(r) for r in rows], [list(r) for r in rows]
+    bad[r_hi][-1] = V + 5       # past the last feature, still ascending
+    clean[r_hi] = rows[r_hi][:-1]
+    bad[r_neg][0] = -1          # negative, still ascending
+    clean[r_neg] = rows[r_neg][1:]
+    bad[r_uns][0], bad[r_uns][1] = rows[r_uns][1], rows[r_uns][0]
+    bad[r_dup][1] = rows[r_dup][0]
+
+    def csr(rs):
+        ptr = np.zeros(N + 1, np.int32)
+        np.cumsum([len(r) for r in rs], out=ptr[1:])
+        return ptr, np.array([i for r in rs for i in r], dtype=np.int32)
+
+    rp_bad, ci_bad = csr(bad)
+    rp_ok, ci_ok = csr(clean)
+    som.validate_csr_host(rp_ok, ci_ok, V)
+    with pytest.raises(som.SomError):
+        som.validate_csr_host(rp_bad, ci_bad, V)
+    Wd = to_dev(W, dev)
+    norms = som.codebook_norms(Wd, V, M)
+    nnz = int(rp_bad[-1])
+    ws = som.alloc_workspace(N, M, V, nnz, dev, tile, keep)
+    b, d = som.bmu_search(Wd, norms, to_dev(rp_bad, dev), to_dev(ci_bad, dev), V, M, nnz=nnz, workspace=ws,
+                          tile_samples=tile, keep_order=keep)
+    flags = som.input_flags(ws, N, M, V, nnz, tile, keep)
+    assert flags & som.FLAG_ID_RANGE and flags & som.FLAG_UNSORTED and not flags & som.FLAG_ROW_PTR, hex(flags)
+    b_ok, d_ok, _ = gpu_run(Wd, rp_ok, ci_ok, dev, tile_samples=tile, norms=norms, keep_order=keep)
+    b, d = b.cpu().numpy(), d.cpu().numpy()
+    same = np.setdiff1d(np.arange(N), [r_uns, r_dup, r_hi, r_neg])
+    assert np.array_equal(b[same], b_ok[same]) and np.array_equal(d[same], d_ok[same])
+    for r in (r_hi, r_neg):  # one id skipped: same unit, distance one more (the id still counts in ||x||^2)
+        assert b[r] == b_ok[r] and abs(d[r] - (d_ok[r] + 1.0)) <= 1e-12 * abs(d[r]), (r, d[r], d_ok[r])
+    assert ((b >= 0) & (b < M)).all()
+    compare(W, rp_ok, ci_ok, b_ok, d_ok, exact=False, what="clean batch")
+
 @pytest.mark.parametrize("name,rows", [("64", 4096), ("256", 1024), ("512", 256)])
 def test_workload_prefix(dev, name, rows):
     # the first rows of a full-size workload (rows are drawn per (seed, row)), full map
