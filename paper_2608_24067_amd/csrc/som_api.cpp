@@ -114,10 +114,8 @@ som_status carve(void *ws, size_t bytes, int64_t N, int64_t M, int64_t V, int64_
     c->ob.bucket = reinterpret_cast<unsigned long long *>(b + L.bucket);
     c->ob.skey = reinterpret_cast<int32_t *>(b + L.skey);
     c->ob.inv = reinterpret_cast<int32_t *>(b + L.inv);
-    c->ob.rbmu = reinterpret_cast<int32_t *>(b + L.rbmu);
-    c->ob.rdist = reinterpret_cast<double *>(b + L.rdist);
-    c->ob.rbmu2 = k.layout_top2() ? reinterpret_cast<int32_t *>(b + L.rbmu2) : nullptr;
-    c->ob.rdist2 = k.layout_top2() ? reinterpret_cast<double *>(b + L.rdist2) : nullptr;
+    c->ob.res = reinterpret_cast<som::Staged *>(b + L.res);
+    c->ob.res2 = k.layout_top2() ? reinterpret_cast<som::Staged *>(b + L.res2) : nullptr;
     c->ob.prp = reinterpret_cast<int32_t *>(b + L.prp);
     c->ob.pci = reinterpret_cast<int32_t *>(b + L.pci);
     c->ob.pvals = k.real ? reinterpret_cast<float *>(b + L.pvals) : nullptr;

@@ -21,6 +21,15 @@ inline int64_t strip_neurons(int ta) { return 64 * neurons_per_lane(ta); }
 inline int64_t n_strips(int64_t M, int ta) { return (M + strip_neurons(ta) - 1) / strip_neurons(ta); }
 inline int64_t n_tiles(int64_t N, int ta) { return (N + ta - 1) / ta; }
 
+// One position's result of a regrouped batch, staged in the workspace: a whole 16-byte
+// record, so the finalize writes full lines and the move back to input order reads one
+// record per sample.
+struct alignas(16) Staged {
+    double d;
+    int32_t b;
+    int32_t pad;
+};
+
 // Workspace carve-up (offsets in bytes from the workspace base; every section 256-byte aligned).
 // The order sections are empty when the caller keeps the given sample order.
 struct Layout {
@@ -35,12 +44,10 @@ struct Layout {
     size_t inv;     // int32 [N]: each sample's position in the ordered batch (-1: never placed)
     size_t prp;     // int32 [N+1]: row pointers of the ordered batch
     size_t pci;     // int32 [nnz]: feature ids of the ordered batch
-    size_t rbmu;    // int32 [N]: best unit by position, before the results go back to input order
-    size_t rdist;   // double [N]: its distance
+    size_t res;     // Staged [N]: best unit and distance by position, before they go back to input order
     size_t keys2;   // uint64 [n_strips * N]: per-strip second-smallest keys (two-best search only)
     size_t dots2;   // float [n_strips * N]: their dot products (two-best search only)
-    size_t rbmu2;   // int32 [N]: second unit by position (two-best search, ordered batch only)
-    size_t rdist2;  // double [N]: its distance
+    size_t res2;    // Staged [N]: second unit and distance by position (two-best search, ordered batch only)
     size_t vals;    // float [nnz * TA]: sample values of every plan entry (real-valued rows only)
     size_t xsq;     // double [N]: ||x||^2 by batch position (real-valued rows only)
     size_t pvals;   // float [nnz]: values of the ordered batch (real-valued rows, regrouped only)
@@ -73,13 +80,11 @@ inline Layout layout_for(int64_t N, int64_t M, int64_t V, int64_t nnz, int ta, b
     L.inv = take(o * (size_t)N * 4);
     L.prp = take(o * (size_t)(N + 1) * 4);
     L.pci = take(o * (size_t)nnz * 4);
-    L.rbmu = take(o * (size_t)N * 4);
-    L.rdist = take(o * (size_t)N * 8);
+    L.res = take(o * (size_t)N * sizeof(Staged));
     const size_t t2 = top2 ? 1 : 0;
     L.keys2 = take(t2 * (size_t)n_strips(M, ta) * (size_t)N * 8);
     L.dots2 = take(t2 * (size_t)n_strips(M, ta) * (size_t)N * 4);
-    L.rbmu2 = take(t2 * o * (size_t)N * 4);
-    L.rdist2 = take(t2 * o * (size_t)N * 8);
+    L.res2 = take(t2 * o * (size_t)N * sizeof(Staged));
     const size_t r = real ? 1 : 0;
     L.vals = take(r * (size_t)nnz * (size_t)ta * 4);
     L.xsq = take(r * (size_t)N * 8);
@@ -92,8 +97,7 @@ struct OrderBuffers {
     uint32_t *freq;
     unsigned long long *bucket;
     int32_t *skey, *inv, *prp, *pci;
-    int32_t *rbmu, *rbmu2;  // results by position (rbmu2: two-best only)
-    double *rdist, *rdist2;
+    Staged *res, *res2;  // results by position (res2: two-best only)
     float *pvals;  // real-valued rows only
 };
 

@@ -1016,6 +1016,23 @@ __global__ __launch_bounds__(256) void k_sweep(const E *__restrict__ W, const do
 // (||w||^2 - 2*dot) + ||x||^2, with ||x||^2 = nnz for binary rows and xsq[k] from the
 // plan for real-valued ones. Results are written by position (k_unpermute then moves
 // them to their samples when the batch was regrouped): every write coalesced.
+// Where a finalize kernel puts a position's result: the caller's arrays (positions are
+// samples) or, for a regrouped batch, one staged record per position.
+struct FinalOut {
+    int32_t *bmu;
+    double *dist;
+    Staged *rec;  // non-null: staged
+    __device__ void put(int64_t k, int32_t b, double d) const
+    {
+        if (rec) {
+            rec[k] = Staged{d, b, 0};
+        } else {
+            bmu[k] = b;
+            dist[k] = d;
+        }
+    }
+};
+
 constexpr int kFinalizeBatch = 8;   // strips whose keys one lane loads at once
 constexpr int kFinalize2Batch = 4;  // the same for the two-best search (four words per strip)
 
@@ -1024,7 +1041,7 @@ __global__ __launch_bounds__(256) void k_finalize(const double *__restrict__ nor
                                                   const double *__restrict__ xsq,
                                                   const u64 *__restrict__ keys,
                                                   const float *__restrict__ dots, int64_t n_strips,
-                                                  int32_t *__restrict__ bmu, double *__restrict__ dist)
+                                                  FinalOut out)
 {
     const int64_t base = row_ptr[0];
     for (int64_t k = (int64_t)blockIdx.x * 256 + threadIdx.x; k < N; k += (int64_t)gridDim.x * 256) {
@@ -1046,8 +1063,7 @@ __global__ __launch_bounds__(256) void k_finalize(const double *__restrict__ nor
         if (b >= M) b = M - 1;
         const int64_t rb = clamp64((int64_t)row_ptr[k] - base, 0, nnz);
         const int64_t re = clamp64((int64_t)row_ptr[k + 1] - base, rb, nnz);
-        bmu[k] = (int32_t)b;
-        dist[k] = fma(-2.0, (double)dots[gb * N + k], norms[b]) + (xsq ? xsq[k] : (double)(re - rb));
+        out.put(k, (int32_t)b, fma(-2.0, (double)dots[gb * N + k], norms[b]) + (xsq ? xsq[k] : (double)(re - rb)));
     }
 }
 
@@ -1060,8 +1076,7 @@ __global__ __launch_bounds__(256) void k_finalize2(const double *__restrict__ no
                                                    const u64 *__restrict__ keys,
                                                    const float *__restrict__ dots, const u64 *__restrict__ keys2,
                                                    const float *__restrict__ dots2, int64_t n_strips,
-                                                   int32_t *__restrict__ bmu, double *__restrict__ dist,
-                                                   int32_t *__restrict__ bmu2, double *__restrict__ dist2)
+                                                   FinalOut out, FinalOut out2)
 {
     const int64_t base = row_ptr[0];
     for (int64_t k = (int64_t)blockIdx.x * 256 + threadIdx.x; k < N; k += (int64_t)gridDim.x * 256) {
@@ -1102,16 +1117,13 @@ __global__ __launch_bounds__(256) void k_finalize2(const double *__restrict__ no
         const double len = xsq ? xsq[k] : (double)(re - rb);
         int64_t i1 = (int64_t)(b1 & kIndexMask);
         if (i1 >= M) i1 = M - 1;
-        bmu[k] = (int32_t)i1;
-        dist[k] = fma(-2.0, (double)q1, norms[i1]) + len;
+        out.put(k, (int32_t)i1, fma(-2.0, (double)q1, norms[i1]) + len);
         if (b2 == kKeyNone) {
-            bmu2[k] = -1;
-            dist2[k] = __builtin_inf();
+            out2.put(k, -1, __builtin_inf());
         } else {
             int64_t i2 = (int64_t)(b2 & kIndexMask);
             if (i2 >= M) i2 = M - 1;
-            bmu2[k] = (int32_t)i2;
-            dist2[k] = fma(-2.0, (double)q2, norms[i2]) + len;
+            out2.put(k, (int32_t)i2, fma(-2.0, (double)q2, norms[i2]) + len);
         }
     }
 }
@@ -1120,20 +1132,21 @@ __global__ __launch_bounds__(256) void k_finalize2(const double *__restrict__ no
 // got (bmu2/dist2 too when given). A sample never placed (inv[s] = -1, invalid row
 // pointers only) is left untouched. Reads gather, writes run in sample order.
 __global__ __launch_bounds__(256) void k_unpermute(const int32_t *__restrict__ inv, int64_t N,
-                                                   const int32_t *__restrict__ rbmu, const double *__restrict__ rdist,
-                                                   const int32_t *__restrict__ rbmu2,
-                                                   const double *__restrict__ rdist2, int32_t *__restrict__ bmu,
+                                                   const Staged *__restrict__ res, const Staged *__restrict__ res2,
+                                                   int32_t *__restrict__ bmu,
                                                    double *__restrict__ dist, int32_t *__restrict__ bmu2,
                                                    double *__restrict__ dist2)
 {
     for (int64_t s = (int64_t)blockIdx.x * 256 + threadIdx.x; s < N; s += (int64_t)gridDim.x * 256) {
         const int64_t k = inv[s];
         if (k < 0 || k >= N) continue;
-        bmu[s] = rbmu[k];
-        dist[s] = rdist[k];
+        const Staged r = res[k];
+        bmu[s] = r.b;
+        dist[s] = r.d;
         if (bmu2) {
-            bmu2[s] = rbmu2[k];
-            dist2[s] = rdist2[k];
+            const Staged r2 = res2[k];
+            bmu2[s] = r2.b;
+            dist2[s] = r2.d;
         }
     }
 }
@@ -1284,17 +1297,16 @@ hipError_t launch_finalize(int ta, const double *norms, int64_t M, const int32_t
     int64_t blocks = (N + 255) / 256;
     if (blocks > (1 << 22)) blocks = 1 << 22;
     // a regrouped batch is finalized by position into the workspace first
-    int32_t *fb = ob ? ob->rbmu : bmu, *fb2 = ob ? ob->rbmu2 : bmu2;
-    double *fd = ob ? ob->rdist : dist, *fd2 = ob ? ob->rdist2 : dist2;
+    const FinalOut o1{bmu, dist, ob ? ob->res : nullptr}, o2{bmu2, dist2, ob ? ob->res2 : nullptr};
     if (bmu2)
         hipLaunchKernelGGL(k_finalize2, dim3((unsigned)blocks), dim3(256), 0, st, norms, M, row_ptr, N, nnz, xsq,
-                           o.keys, o.dots, o.keys2, o.dots2, n_strips(M, ta), fb, fd, fb2, fd2);
+                           o.keys, o.dots, o.keys2, o.dots2, n_strips(M, ta), o1, o2);
     else
         hipLaunchKernelGGL(k_finalize, dim3((unsigned)blocks), dim3(256), 0, st, norms, M, row_ptr, N, nnz, xsq,
-                           o.keys, o.dots, n_strips(M, ta), fb, fd);
+                           o.keys, o.dots, n_strips(M, ta), o1);
     if (ob)
-        hipLaunchKernelGGL(k_unpermute, dim3((unsigned)blocks), dim3(256), 0, st, ob->inv, N, fb, fd,
-                           bmu2 ? fb2 : nullptr, bmu2 ? fd2 : nullptr, bmu, dist, bmu2, dist2);
+        hipLaunchKernelGGL(k_unpermute, dim3((unsigned)blocks), dim3(256), 0, st, ob->inv, N, ob->res,
+                           bmu2 ? ob->res2 : nullptr, bmu, dist, bmu2, dist2);
     return hipGetLastError();
 }
 
