@@ -114,8 +114,8 @@ typedef struct {
  * or the config is invalid. The workspace must be 256-byte aligned device
  * memory. It holds the tile plan (8 bytes per id), one 8-byte partial key
  * and one 4-byte dot product per sample and strip of 512 neurons (256 when
- * tile_samples > 8) and, unless keep_order is set, the regrouped batch (4
- * bytes per id, 16 per sample, 12 per feature).
+ * tile_samples > 8) and, unless keep_order is set, the regrouped batch and
+ * its staged results (4 bytes per id, 28 per sample, 12 per feature).
  */
 size_t som_bmu_workspace_bytes(int64_t N, int64_t M, int64_t V, int64_t nnz, const som_bmu_config *config);
 
@@ -193,7 +193,8 @@ som_status som_bmu_finalize(const double *norms, int64_t V, int64_t M, const int
  *                order and its full squared distance; -1 and +inf if M == 1.
  * The workspace must hold som_bmu2_workspace_bytes(N, M, V, nnz, config)
  * bytes: the single-best workspace plus a second key and dot product per
- * sample and strip. A two-best workspace also serves every single-best call
+ * sample and strip (and, unless keep_order is set, 16 bytes per sample for
+ * the staged second results). A two-best workspace also serves every single-best call
  * and som_bmu_input_flags with the same config.
  */
 size_t som_bmu2_workspace_bytes(int64_t N, int64_t M, int64_t V, int64_t nnz, const som_bmu_config *config);
