@@ -703,7 +703,8 @@ __global__ __launch_bounds__(256) void k_sweep(const E *__restrict__ W, const do
         // widened when it is added. Lanes whose group lies past M (last strip only)
         // re-read the row's last group; those neurons are never ranked.
         auto row_load = [&](unsigned id, Seg &seg) {
-            const E *r = W + (size_t)(id < vmax ? id : vmax) * (size_t)M;
+            // 32 x 32-bit product: ids < 2^31 and M <= 2^20
+            const E *r = W + (uint64_t)(id < vmax ? id : vmax) * (uint64_t)(unsigned)Mi;
             if constexpr (VEC) {
 #pragma unroll
                 for (int q = 0; q < NPL / G; ++q) {
@@ -718,9 +719,24 @@ __global__ __launch_bounds__(256) void k_sweep(const E *__restrict__ W, const do
                 }
             }
         };
-        // The mask is wave-uniform: each bit is a scalar branch. The empty volatile
+        // The mask is wave-uniform: each bit is a scalar branch, tested four bits at a
+        // time first (an entry usually has one or two bits set). The empty volatile
         // asm keeps the compiler from turning the branch into unconditional adds
         // and selects.
+        auto each_sample = [&](unsigned mask, auto &&body) {
+#pragma unroll
+            for (int s0 = 0; s0 < TA; s0 += 4) {
+                if (mask & (0xFu << s0)) {
+#pragma unroll
+                    for (int s = s0; s < s0 + 4; ++s) {
+                        if (mask & (1u << s)) {
+                            body(s);
+                            asm volatile("");
+                        }
+                    }
+                }
+            }
+        };
         // xv: the entry's TA sample values (REAL only; scalar registers)
         auto row_add = [&](unsigned mask, const Seg &seg, const float *xv) {
             if constexpr (sizeof(E) == 2 && VEC) {
@@ -729,9 +745,7 @@ __global__ __launch_bounds__(256) void k_sweep(const E *__restrict__ W, const do
                 // acc + h * 1.0, or acc + h * x for real values -- the same result as
                 // widening first.
                 const unsigned *dw = reinterpret_cast<const unsigned *>(&seg.v[0]);
-#pragma unroll
-                for (int s = 0; s < TA; ++s) {
-                    if (mask & (1u << s)) {
+                each_sample(mask, [&](int s) {
 #pragma unroll
                         for (int d = 0; d < NPL / 2; ++d) {
                             if constexpr (REAL) {
@@ -750,9 +764,7 @@ __global__ __launch_bounds__(256) void k_sweep(const E *__restrict__ W, const do
                                     : "v"(dw[d]));
                             }
                         }
-                        asm volatile("");
-                    }
-                }
+                });
             } else {
                 float w[NPL];
 #pragma unroll
@@ -762,19 +774,15 @@ __global__ __launch_bounds__(256) void k_sweep(const E *__restrict__ W, const do
                     else
                         w[j] = (float)seg.e[j];
                 }
+                each_sample(mask, [&](int s) {
 #pragma unroll
-                for (int s = 0; s < TA; ++s) {
-                    if (mask & (1u << s)) {
-#pragma unroll
-                        for (int j = 0; j < NPL; ++j) {
-                            if constexpr (REAL)
-                                acc[s][j] = fmaf(xv[s], w[j], acc[s][j]);
-                            else
-                                acc[s][j] += w[j];
-                        }
-                        asm volatile("");
+                    for (int j = 0; j < NPL; ++j) {
+                        if constexpr (REAL)
+                            acc[s][j] = fmaf(xv[s], w[j], acc[s][j]);
+                        else
+                            acc[s][j] += w[j];
                     }
-                }
+                });
             }
         };
         // the TA sample values of plan entry q (REAL only)
