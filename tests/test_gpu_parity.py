@@ -200,6 +200,11 @@ def test_phases_equal_search_and_flags_clean(dev):
     som.bmu_finalize(norms, rpd, V, M, nnz, b2, d2, ws)
     assert som.input_flags(ws, N, M, V, nnz) == 0
     assert torch.equal(b1, b2) and torch.equal(d1, d2)
+    # the phases only read what the previous one wrote: a second finalize gives the same results
+    b2.fill_(-7)
+    d2.fill_(-7.0)
+    som.bmu_finalize(norms, rpd, V, M, nnz, b2, d2, ws)
+    assert torch.equal(b1, b2) and torch.equal(d1, d2)
 
 
 

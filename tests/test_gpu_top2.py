@@ -132,3 +132,8 @@ def test_phases_equal_search(dev):
     assert som.input_flags(ws, N, M, V, nnz) == 0
     for a, b in zip(whole, out):
         assert torch.equal(a, b)
+    # the two-best workspace serves the single-best finalize: rank 1, the same bits
+    b1 = torch.full((N,), -7, dtype=torch.int32, device=dev)
+    d1 = torch.full((N,), -7.0, dtype=torch.float64, device=dev)
+    som.bmu_finalize(norms, rpd, V, M, nnz, b1, d1, ws)
+    assert torch.equal(b1, whole[0]) and torch.equal(d1, whole[1])
