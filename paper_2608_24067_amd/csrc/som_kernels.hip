@@ -600,8 +600,10 @@ __global__ __launch_bounds__(256) void k_plan(const int32_t *__restrict__ row_pt
 
 // Workgroup = 4 waves x one strip (blockIdx.y) of 64*NPL neurons, over groups of
 // group_tiles consecutive tiles (a multiple of 4; groups blockIdx.x, blockIdx.x +
-// gridDim.x, ...); each lane owns NPL neurons, in groups of four (see loc below). VEC: M is
-// a multiple of 4 and W 16-byte aligned, so each group is one aligned 16-byte load.
+// gridDim.x, ...); each lane owns NPL neurons, in groups of G (four fp32 values, or
+// min(8, NPL) fp16 ones; see loc below). VEC: M is a multiple of G and W aligned to a
+// group's bytes, so each group is one aligned vector load (16 bytes; 8 for fp16 at four
+// neurons per lane).
 // The plan is read defensively (offsets, counts and ids clamped to the workspace
 // and the codebook), so even a workspace the plan never wrote cannot drive an
 // access out of bounds.
@@ -1223,8 +1225,10 @@ static void sweep_ta(bool vec, dim3 grid, int64_t group_tiles, hipStream_t st, c
                      int64_t M, int64_t N, int64_t V, int64_t nnz, const uint2 *plan, const int2 *tiles, int64_t nt,
                      const SweepOut &o, const float *vals)
 {
+    // packed fp16 rows take half the registers: five rows in flight still fit 128 VGPRs
+    constexpr int UV = (sizeof(E) == 2 && NPL == 8) ? 5 : 4;
     if (vec)
-        hipLaunchKernelGGL((k_sweep<E, TA, NPL, 4, true, TOP2, REAL>), grid, dim3(256), 0, st, W, norms, M, N, V, nnz,
+        hipLaunchKernelGGL((k_sweep<E, TA, NPL, UV, true, TOP2, REAL>), grid, dim3(256), 0, st, W, norms, M, N, V, nnz,
                            plan, tiles, nt, o.keys, o.dots, o.keys2, o.dots2, vals, group_tiles);
     else
         hipLaunchKernelGGL((k_sweep<E, TA, NPL, 4, false, TOP2, REAL>), grid, dim3(256), 0, st, W, norms, M, N, V, nnz,
