@@ -1225,8 +1225,9 @@ static void sweep_ta(bool vec, dim3 grid, int64_t group_tiles, hipStream_t st, c
                      int64_t M, int64_t N, int64_t V, int64_t nnz, const uint2 *plan, const int2 *tiles, int64_t nt,
                      const SweepOut &o, const float *vals)
 {
-    // packed fp16 rows take half the registers: five rows in flight still fit 128 VGPRs
-    constexpr int UV = (sizeof(E) == 2 && NPL == 8) ? 5 : 4;
+    // Packed fp16 rows take half the registers: eight rows in flight still fit 128 VGPRs
+    // (six for real-valued rows, whose per-entry values take scalar registers).
+    constexpr int UV = (sizeof(E) == 2 && NPL == 8) ? (REAL ? 6 : 8) : 4;
     if (vec)
         hipLaunchKernelGGL((k_sweep<E, TA, NPL, UV, true, TOP2, REAL>), grid, dim3(256), 0, st, W, norms, M, N, V, nnz,
                            plan, tiles, nt, o.keys, o.dots, o.keys2, o.dots2, vals, group_tiles);
