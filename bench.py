@@ -313,7 +313,9 @@ def main():
     sweep_s = phase_ms["sweep"] / 1e3
     achieved = alg_bytes / sweep_s / 1e9
     workload = cfg.describe()
-    traffic = None if (args.top2 or args.values or args.dtype != "f32") else measured_traffic(args.config)
+    # the committed counter runs are of the default variant: fp32, binary rows, best unit, default tile
+    default_variant = not (args.top2 or args.values or args.dtype != "f32" or args.tile not in (0, som.DEFAULT_TILE_SAMPLES))
+    traffic = measured_traffic(args.config) if default_variant else None
 
     out = {
         "metric": METRIC,
