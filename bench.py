@@ -314,7 +314,8 @@ def main():
     achieved = alg_bytes / sweep_s / 1e9
     workload = cfg.describe()
     # the committed counter runs are of the default variant: fp32, binary rows, best unit, default tile
-    default_variant = not (args.top2 or args.values or args.dtype != "f32" or args.tile not in (0, som.DEFAULT_TILE_SAMPLES))
+    default_variant = not (args.top2 or args.values or args.dtype != "f32"
+                           or args.tile not in (0, som.DEFAULT_TILE_SAMPLES))
     traffic = measured_traffic(args.config) if default_variant else None
 
     out = {
