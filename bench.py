@@ -185,8 +185,8 @@ def main():
         args.top2 = True
 
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; multi-GPU sharding is designed, not built "
-                                   "(see DESIGN.md)", "n_gpus": args.gpus}))
+        print(json.dumps({"error": "this benchmark runs on one GPU only: sharding over samples or neuron ranges "
+                                   "is designed but not built", "n_gpus": args.gpus}))
         sys.exit(2)
 
     import torch
