@@ -43,8 +43,10 @@
  *
  * CSR input. row_ptr has N+1 int32 entries; row s holds the feature ids
  * col_idx[row_ptr[s] .. row_ptr[s+1]). row_ptr[0] need not be 0 (a slice of
- * a larger batch): col_idx is always the base pointer the offsets index, and
- * nnz = row_ptr[N] - row_ptr[0]. Each row's ids must be strictly ascending
+ * a larger batch) but must not be negative: col_idx is always the base
+ * pointer the offsets index, and nnz = row_ptr[N] - row_ptr[0] (the device
+ * reads a batch whose row_ptr[0] is negative as empty and flags it). Each
+ * row's ids must be strictly ascending
  * and in [0, V) (sorted, distinct: the paper's sparse-binary CSR, corpus
  * section). That is a precondition of the device path, checked on the host
  * by som_validate_csr_host. The device kernels never access memory outside
@@ -348,8 +350,8 @@ som_status som_bmu_input_flags(const void *workspace, size_t workspace_bytes, in
 
 /*
  * Host check of the CSR input rules (corpus section: sorted descriptor ids
- * per row; binary values implicit): row_ptr non-decreasing, every id in
- * [0, V), ids strictly ascending within each row. Host pointers; col_idx
+ * per row; binary values implicit): row_ptr[0] >= 0, row_ptr non-decreasing,
+ * every id in [0, V), ids strictly ascending within each row. Host pointers; col_idx
  * may be NULL when row_ptr[N] == row_ptr[0]. Returns SOM_OK, SOM_ERR_BAD_CSR
  * (with the first offending row in som_last_error) or SOM_ERR_INVALID_ARG.
  */

@@ -42,6 +42,7 @@ static int check_args(const float *W, int64_t ldw, int64_t V, int64_t i0, int64_
     if (N < 0 || V < 1 || i0 < 0 || i1 <= i0 || ldw < i1 - i0) return SOM_ORACLE_BAD_ARG;
     if (N == 0) return SOM_ORACLE_OK;
     if (!W || !row_ptr) return SOM_ORACLE_BAD_ARG;
+    if (row_ptr[0] < 0) return SOM_ORACLE_BAD_CSR; /* offsets index col_idx from its start */
     for (int64_t s = 0; s < N; ++s)
         if (row_ptr[s + 1] < row_ptr[s]) return SOM_ORACLE_BAD_CSR;
     if (row_ptr[N] > row_ptr[0] && !col_idx) return SOM_ORACLE_BAD_ARG;
@@ -266,6 +267,7 @@ int som_update_oracle_host(const float *W_in, int64_t V, int64_t E, const int32_
     if (!W_in || !W_out || V < 1 || E < 1 || N < 0 || radius < 1 || (N > 0 && (!row_ptr || !bmu)))
         return SOM_ORACLE_BAD_ARG;
     const int64_t M = E * E;
+    if (N > 0 && row_ptr[0] < 0) return SOM_ORACLE_BAD_CSR;
     for (int64_t s = 0; s < N; ++s) {
         if (row_ptr[s + 1] < row_ptr[s]) return SOM_ORACLE_BAD_CSR;
         if (bmu[s] < 0 || bmu[s] >= M) return SOM_ORACLE_BAD_ARG;

@@ -29,7 +29,7 @@ extern "C" {
 /* Status codes (0 = success). */
 #define SOM_ORACLE_OK 0
 #define SOM_ORACLE_BAD_ARG 1   /* null pointer, empty block, ldw too small, N<0, V<1 */
-#define SOM_ORACLE_BAD_CSR 2   /* row_ptr decreasing or a feature id outside [0, V) */
+#define SOM_ORACLE_BAD_CSR 2   /* row_ptr negative or decreasing, or a feature id outside [0, V) */
 #define SOM_ORACLE_NO_MEM 3
 
 /*

@@ -8,7 +8,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libsom.so")
-SOURCES = [os.path.join(CSRC, "som_kernels.hip"), os.path.join(CSRC, "som_update.hip"), os.path.join(CSRC, "som_api.cpp")]
+SOURCES = [os.path.join(CSRC, "som_sweep.hip"), os.path.join(CSRC, "som_kernels.hip"), os.path.join(CSRC, "som_update.hip"),
+           os.path.join(CSRC, "som_api.cpp")]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"

@@ -276,6 +276,15 @@ Kind real_kind(const int32_t *bmu2, const double *dist2) { return Kind{bmu2 != n
 
 }  // namespace
 
+som_status som::set_error(som_status st, const char *fmt, ...)
+{
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof g_err, fmt, ap);
+    va_end(ap);
+    return st;
+}
+
 extern "C" {
 
 size_t som_bmu_workspace_bytes(int64_t N, int64_t M, int64_t V, int64_t nnz, const som_bmu_config *config)
@@ -544,6 +553,8 @@ som_status som_validate_csr_host(const int32_t *row_ptr, const int32_t *col_idx,
 {
     if (N < 0 || V < 1 || V >= INT32_MAX) return fail(SOM_ERR_INVALID_ARG, "need N >= 0 and 1 <= V < 2^31-1");
     if (!row_ptr) return fail(SOM_ERR_INVALID_ARG, "row_ptr is NULL");
+    // col_idx is the base the offsets index: a negative offset would name ids before it
+    if (row_ptr[0] < 0) return fail(SOM_ERR_BAD_CSR, "row_ptr[0] is negative (%d)", row_ptr[0]);
     for (int64_t s = 0; s < N; ++s)
         if (row_ptr[s + 1] < row_ptr[s])
             return fail(SOM_ERR_BAD_CSR, "row %lld: row_ptr decreases (%d -> %d)", (long long)s, row_ptr[s],

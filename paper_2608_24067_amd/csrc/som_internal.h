@@ -109,6 +109,9 @@ struct SweepOut {
     float *dots2;
 };
 
+// Records the calling thread's error text (som_last_error) and returns st.
+som_status set_error(som_status st, const char *fmt, ...) __attribute__((format(printf, 2, 3)));
+
 // Kernel launchers (som_kernels.hip). Each returns the launch's hipError_t.
 hipError_t launch_norms(const float *W, int64_t V, int64_t M, double *norms, hipStream_t st);
 // fp16 codebooks: W holds IEEE binary16 bit patterns.

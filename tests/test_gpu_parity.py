@@ -254,6 +254,29 @@ def test_invalid_ids_are_flagged_and_stay_local(dev, tile, keep):
     assert ((b >= 0) & (b < M)).all()
     compare(W, rp_ok, ci_ok, b_ok, d_ok, exact=False, what="clean batch")
 
+@pytest.mark.parametrize("tile,keep", [(8, False), (16, True)])
+def test_negative_first_offset_reads_as_empty(dev, tile, keep):
+    """A row_ptr whose first offset is negative would name ids before col_idx: the validator rejects it, and the
+    device reads the batch as empty (no id is read), flags its row pointers and still returns in-range results."""
+    V, M, N = 400, 700, 50
+    rp, ci, W = case(43, N, V, M, synth.UNIFORM)
+    rp_neg = (rp - 2).astype(np.int32)
+    with pytest.raises(som.SomError):
+        som.validate_csr_host(rp_neg, ci, V)
+    Wd = to_dev(W, dev)
+    norms = som.codebook_norms(Wd, V, M)
+    nnz = int(rp[-1])
+    for two in (False, True):
+        ws = (som.alloc_workspace2 if two else som.alloc_workspace)(N, M, V, nnz, dev, tile, keep)
+        search = som.bmu2_search if two else som.bmu_search
+        out = search(Wd, norms, to_dev(rp_neg, dev), to_dev(ci, dev), V, M, nnz=nnz, workspace=ws,
+                     tile_samples=tile, keep_order=keep)
+        flags = som.input_flags(ws, N, M, V, nnz, tile, keep)
+        assert flags & som.FLAG_ROW_PTR, hex(flags)
+        b, d = out[0].cpu().numpy(), out[1].cpu().numpy()
+        assert ((b >= 0) & (b < M)).all() and np.isfinite(d).all()
+
+
 @pytest.mark.parametrize("name,rows", [("64", 4096), ("256", 1024), ("512", 256)])
 def test_workload_prefix(dev, name, rows):
     # the first rows of a full-size workload (rows are drawn per (seed, row)), full map
