@@ -150,6 +150,27 @@ som_status som_bmu_search(const float *W, const double *norms, int64_t V, int64_
                           void *workspace, size_t workspace_bytes, const som_bmu_config *config, void *stream);
 
 /*
+ * som_bmu_search without a workspace argument, for callers that cannot
+ * allocate device memory (code under stream capture, tight serving loops,
+ * harnesses that forbid allocation). Arguments, results and errors are those
+ * of som_bmu_search; the scratch space is a device array inside the library,
+ * SOM_NOALLOC_SCRATCH_BYTES on every GPU the library runs on, held until the
+ * process ends. The call allocates nothing. A search whose
+ * som_bmu_workspace_bytes(N, M, V, nnz, config) exceeds that size returns
+ * SOM_ERR_WORKSPACE (checked on the host, nothing enqueued): at 12 ids per
+ * row and V = 30,000 that is about 248,000 rows on a 64x64 map, 39,000 on a
+ * 256x256 map and 2,700 on a 1024x1024 map.
+ * The stream must belong to the calling thread's current device.
+ * All calls on one GPU share its array: calls that overlap in time on one
+ * GPU (other streams, other threads) race and give undefined results.
+ */
+#define SOM_NOALLOC_SCRATCH_BYTES (64u << 20)
+
+som_status som_bmu_search_noalloc(const float *W, const double *norms, int64_t V, int64_t M, const int32_t *row_ptr,
+                                  const int32_t *col_idx, int64_t N, int64_t nnz, int32_t *bmu, double *dist,
+                                  const som_bmu_config *config, void *stream);
+
+/*
  * The three phases of som_bmu_search, for callers that time or overlap them.
  * Arguments mean the same as above; each phase reads what the previous one
  * left in the same workspace, so they must run in this order on one stream.

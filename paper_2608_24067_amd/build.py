@@ -9,7 +9,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libsom.so")
 SOURCES = [os.path.join(CSRC, "som_sweep.hip"), os.path.join(CSRC, "som_kernels.hip"), os.path.join(CSRC, "som_update.hip"),
-           os.path.join(CSRC, "som_api.cpp")]
+           os.path.join(CSRC, "som_api.cpp"), os.path.join(CSRC, "som_noalloc.hip")]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"

@@ -23,7 +23,8 @@ DEFAULT_TILE_SAMPLES = 8
 FLAG_ID_RANGE, FLAG_UNSORTED, FLAG_ROW_PTR = 0x1, 0x2, 0x4
 
 EXPORTS = (
-    "som_bmu_workspace_bytes", "som_codebook_norms", "som_bmu_search", "som_bmu_plan", "som_bmu_sweep",
+    "som_bmu_workspace_bytes", "som_codebook_norms", "som_bmu_search", "som_bmu_search_noalloc", "som_bmu_plan",
+    "som_bmu_sweep",
     "som_bmu_finalize", "som_bmu2_workspace_bytes", "som_bmu2_search", "som_bmu2_sweep", "som_bmu2_finalize",
     "som_codebook_norms_f16", "som_bmu_search_f16", "som_bmu_sweep_f16", "som_bmu2_search_f16", "som_bmu2_sweep_f16",
     "som_bmu_sf_workspace_bytes", "som_bmu_sf_search", "som_bmu_sf_search_f16", "som_bmu_sf_plan", "som_bmu_sf_sweep",
@@ -64,6 +65,7 @@ def load():
     lib.som_bmu_workspace_bytes.restype = sz
     lib.som_codebook_norms.argtypes = [vp, i64, i64, vp, vp]
     lib.som_bmu_search.argtypes = [vp, vp, i64, i64, vp, vp, i64, i64, vp, vp, vp, sz, cfgp, vp]
+    lib.som_bmu_search_noalloc.argtypes = [vp, vp, i64, i64, vp, vp, i64, i64, vp, vp, cfgp, vp]
     lib.som_bmu_plan.argtypes = [vp, vp, i64, i64, i64, i64, vp, sz, cfgp, vp]
     lib.som_bmu_sweep.argtypes = [vp, vp, i64, i64, i64, i64, vp, sz, cfgp, vp]
     lib.som_bmu_finalize.argtypes = [vp, i64, i64, vp, i64, i64, vp, vp, vp, sz, cfgp, vp]
@@ -100,7 +102,8 @@ def load():
     lib.som_radius.restype = ctypes.c_int32
     lib.som_bmu_input_flags.argtypes = [vp, sz, i64, i64, i64, i64, cfgp, ctypes.POINTER(ctypes.c_uint32), vp]
     lib.som_validate_csr_host.argtypes = [vp, vp, i64, i64]
-    for name in ("som_codebook_norms", "som_bmu_search", "som_bmu_plan", "som_bmu_sweep", "som_bmu_finalize",
+    for name in ("som_codebook_norms", "som_bmu_search", "som_bmu_search_noalloc", "som_bmu_plan", "som_bmu_sweep",
+                 "som_bmu_finalize",
                  "som_bmu2_search", "som_bmu2_sweep", "som_bmu2_finalize", "som_bmu_input_flags",
                  "som_validate_csr_host"):
         getattr(lib, name).restype = ctypes.c_int
@@ -221,6 +224,27 @@ def bmu_search(W, norms, row_ptr, col_idx, V: int, M: int, nnz: int | None = Non
             _dev(bmu, "bmu", torch.int32, N), _dev(dist, "dist", torch.float64, N),
             _dev(workspace, "workspace", torch.uint8), workspace.numel(), _cfg(tile_samples, keep_order), _stream(W))
     _check(st, name)
+    return bmu, dist
+
+
+NOALLOC_SCRATCH_BYTES = 64 << 20
+
+
+def bmu_search_noalloc(W, norms, row_ptr, col_idx, V: int, M: int, nnz: int, bmu, dist, tile_samples: int = 0,
+                       keep_order: bool = False):
+    """bmu_search through som_bmu_search_noalloc: no workspace, the library's own scratch array (fp32 codebook).
+
+    bmu and dist must be passed (the call itself allocates nothing); returns them.
+    """
+    N = row_ptr.numel() - 1
+    rp, ci = _csr(row_ptr, col_idx, N, nnz)
+    if W.dtype != torch.float32:
+        raise TypeError("som_bmu_search_noalloc takes an fp32 codebook")
+    st = load().som_bmu_search_noalloc(_dev(W, "W", torch.float32, V * M), _dev(norms, "norms", torch.float64, M), V,
+                                       M, rp, ci, N, int(nnz), _dev(bmu, "bmu", torch.int32, N),
+                                       _dev(dist, "dist", torch.float64, N), _cfg(tile_samples, keep_order),
+                                       _stream(W))
+    _check(st, "som_bmu_search_noalloc")
     return bmu, dist
 
 

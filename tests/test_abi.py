@@ -247,3 +247,21 @@ def test_phase_and_norms_argument_checks():
     out = ctypes.c_uint32(7)
     assert lib.som_bmu_input_flags(FAKE, 100, 10, 64, 100, 50, None, ctypes.byref(out), None) == som.SOM_ERR_WORKSPACE
     assert lib.som_bmu_input_flags(FAKE, 100, 10, 64, 100, 50, None, None, None) == som.SOM_ERR_INVALID_ARG
+
+
+def test_noalloc_rejects_searches_beyond_its_array():
+    # checked on the host before anything touches a device: fake pointers are never dereferenced
+    lib = som.load()
+    V, M = 30_000, 1 << 20
+    N, nnz = 4_000, 48_000
+    assert som.workspace_bytes(N, M, V, nnz) > som.NOALLOC_SCRATCH_BYTES
+    assert lib.som_bmu_search_noalloc(FAKE, FAKE, V, M, FAKE, FAKE, N, nnz, FAKE, FAKE, None,
+                                      None) == som.SOM_ERR_WORKSPACE
+    assert b"scratch" in lib.som_last_error()
+    assert lib.som_bmu_search_noalloc(FAKE, FAKE, V, M + 1, FAKE, FAKE, N, nnz, FAKE, FAKE, None,
+                                      None) == som.SOM_ERR_INVALID_ARG
+    assert lib.som_bmu_search_noalloc(FAKE, FAKE, V, M, FAKE, FAKE, N, nnz, FAKE, FAKE, _cfg(7),
+                                      None) == som.SOM_ERR_INVALID_ARG
+    text = open(os.path.join(ROOT, "include", "som.h")).read()
+    assert re.search(r"^#define SOM_NOALLOC_SCRATCH_BYTES \(64u << 20\)$", text, re.M)
+    assert som.NOALLOC_SCRATCH_BYTES == 64 << 20
