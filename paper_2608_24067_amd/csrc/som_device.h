@@ -62,6 +62,34 @@ __device__ __forceinline__ void load_group(const E *p, float *w)
 constexpr u64 kKeyNone = ~0ull;
 constexpr u64 kIndexMask = (1ull << 20) - 1;
 
+// The second word of a plan entry: the TA-bit mask of the tile's samples that hold
+// the entry's feature. For tiles of up to 16 samples it also carries the slot of the
+// lowest set bit (bits 24-28) and, in bit 31, whether more than one bit is set, so the
+// sweep can send an entry held by one sample (most of them) straight to that
+// sample's accumulators.
+constexpr int kPlanSlotShift = 24;
+constexpr unsigned kPlanMulti = 1u << 31;
+
+template <int TA>
+__device__ __forceinline__ unsigned plan_word(unsigned mask)
+{
+    if constexpr (TA <= 16)
+        return mask | ((unsigned)__builtin_ctz(mask | (1u << 30)) << kPlanSlotShift) |
+               ((mask & (mask - 1)) ? kPlanMulti : 0u);
+    else
+        return mask;
+}
+
+// The sample mask of a plan word.
+template <int TA>
+__device__ __forceinline__ unsigned plan_mask(unsigned y)
+{
+    if constexpr (TA < 32)
+        return y & ((1u << TA) - 1u);
+    else
+        return y;
+}
+
 __device__ __forceinline__ u64 rank_key(double d, unsigned i)
 {
     u64 b = (u64)__double_as_longlong(d);

@@ -352,7 +352,7 @@ __global__ __launch_bounds__(256) void k_plan(const int32_t *__restrict__ row_pt
                     (unsigned)((bal >> (grp * TA)) & (TA == 32 ? 0xFFFFFFFFull : ((1ull << TA) - 1)));
                 if (m != INT_MAX) {
                     if (k < cap) {
-                        if (sl == 0) plan[plo + k] = make_uint2((unsigned)m, mask);
+                        if (sl == 0) plan[plo + k] = make_uint2((unsigned)m, plan_word<TA>(mask));
                         if (REAL && cur == m) vals[(int64_t)(plo + k) * TA + sl] = curv;
                     }
                     ++k;

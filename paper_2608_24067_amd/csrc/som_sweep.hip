@@ -21,6 +21,7 @@
 // frequently used rows stay in L2.
 
 #include "som_device.h"
+#include "som_tree16.h"
 
 namespace som {
 namespace {
@@ -86,6 +87,19 @@ __global__ __launch_bounds__(256) void k_sweep(const E *__restrict__ W, const do
     }
     const float nmax = wave_max_f32(nmax_l);
     const unsigned vmax = (unsigned)(V - 1);
+    // Tiles of 16 with four fp32 neurons per lane: the row dispatch is one assembly
+    // block per row (som_tree16.h), and a row's address is one vector multiply-add
+    // from the lane's own start of the strip (the row pitch is kept in a vector
+    // register for that), which leaves the scalar unit to the dispatch.
+    constexpr bool T16 = sizeof(E) == 4 && TA == 16 && NPL == 4 && VEC && !REAL;
+    const char *lrow = nullptr;
+    unsigned pitch = 0;
+    if constexpr (T16) {
+        const int g = base + lg;
+        lrow = reinterpret_cast<const char *>(W + (g < Mi ? g : Mi - G));
+        pitch = (unsigned)Mi * (unsigned)sizeof(E);
+        asm volatile("" : "+v"(pitch));
+    }
 
     // Tiles wv, wv + 4, ... of the workgroup's groups. The next tile's header (its plan
     // offset and union size, and the next tile's offset that bounds it) and its first
@@ -134,6 +148,11 @@ __global__ __launch_bounds__(256) void k_sweep(const E *__restrict__ W, const do
         // widened when it is added. Lanes whose group lies past M (last strip only)
         // re-read the row's last group; those neurons are never ranked.
         auto row_load = [&](unsigned id, Seg &seg) {
+            if constexpr (T16) {
+                const unsigned idc = id < vmax ? id : vmax;
+                seg.v[0] = *reinterpret_cast<const typename Seg::vec *>(lrow + (uint64_t)idc * pitch);
+                return;
+            }
             // 32 x 32-bit product: ids < 2^31 and M <= 2^20
             const E *r = W + (uint64_t)(id < vmax ? id : vmax) * (uint64_t)(unsigned)Mi;
             if constexpr (VEC) {
@@ -170,7 +189,10 @@ __global__ __launch_bounds__(256) void k_sweep(const E *__restrict__ W, const do
         };
         // xv: the entry's TA sample values (REAL only; scalar registers)
         auto row_add = [&](unsigned mask, const Seg &seg, const float *xv) {
-            if constexpr (sizeof(E) == 2 && VEC) {
+            if constexpr (T16) {
+                const float w[4] = {seg.v[0][0], seg.v[0][1], seg.v[0][2], seg.v[0][3]};
+                SOM_T16_DISPATCH(acc, w, mask);
+            } else if constexpr (sizeof(E) == 2 && VEC) {
                 // Packed fp16: each update is one mixed-precision FMA with h read as a
                 // half straight from the loaded dword (exact widening, one rounding):
                 // acc + h * 1.0, or acc + h * x for real values -- the same result as
@@ -458,7 +480,8 @@ static void sweep_ta(bool vec, dim3 grid, int64_t group_tiles, hipStream_t st, c
 {
     // Packed fp16 rows take half the registers: eight rows in flight still fit 128 VGPRs
     // (six for real-valued rows, whose per-entry values take scalar registers).
-    constexpr int UV = (sizeof(E) == 2 && NPL == 8) ? (REAL ? 6 : 8) : 4;
+    // fp32 rows of four neurons per lane take four registers: eight in flight.
+    constexpr int UV = (sizeof(E) == 2 && NPL == 8) ? (REAL ? 6 : 8) : (sizeof(E) == 4 && NPL == 4 ? 8 : 4);
     if (vec)
         hipLaunchKernelGGL((k_sweep<E, TA, NPL, UV, true, TOP2, REAL>), grid, dim3(256), 0, st, W, norms, M, N, V, nnz,
                            plan, tiles, nt, o.keys, o.dots, o.keys2, o.dots2, vals, group_tiles);
@@ -472,9 +495,13 @@ static void sweep_ta(bool vec, dim3 grid, int64_t group_tiles, hipStream_t st, c
 // (regrouped) batch, but a strip must still span many rounds of resident
 // workgroups, or the chip works on two strips at once and their rows compete for
 // L2: up to 32 tiles, and at least 16,384 groups per strip where there are enough.
+// Between 62,000 and 131,000 tiles (the 1024 x 1024 map's 500,000 rows) two tiles per
+// wave still leave 7,500 groups (about seven rounds) per strip: 784 -> 769 ms there,
+// while 12 or 16 tiles (5,200 or 3,900 groups) cost 4-7%.
 static int64_t sweep_group_tiles(int64_t nt)
 {
     int64_t g = nt / 16384 / 4 * 4;
+    if (g < 8 && nt >= 8 * 7500) g = 8;
     return g < 4 ? 4 : (g > 32 ? 32 : g);
 }
 
