@@ -330,7 +330,7 @@ som_status som_bmu_sf_finalize(const double *norms, int64_t V, int64_t M, const 
  *   chunk_features  features blurred per pass (0 = all V); the workspace holds
  *                   three chunk x M fields, so smaller chunks need less memory.
  * som_update_workspace_bytes(V, E, N, chunk_features) sizes the workspace for a
- * batch of N samples (three chunk x M fields, seven M-sized buffers and N int32
+ * batch of N samples (three chunk x M fields, nine M-sized buffers and N int32
  * positions for sorting the samples of crowded units); 0 for invalid sizes.
  * Per unit, den = samples assigned to it and num[v] = those holding feature v
  * (exact integer counts), both converted to fp32 and blurred by three
@@ -338,8 +338,13 @@ som_status som_bmu_sf_finalize(const double *norms, int64_t V, int64_t M, const 
  * column, each over the clamped window [k-r, k+r] and unnormalised (the paper's
  * four rules: unnormalised sums, clamped boundary, a unit whose blurred den is
  * zero keeps its prototype, fp32 accumulation with the binary16 conversion only
- * at the final write). W = num / den. The passes run in a fixed order, so the
- * result is the same bits on every run. Norms must be recomputed afterwards.
+ * at the final write). W = num / den, clamped to [0, 1] (the range of a mean of
+ * 0/1 inputs). The blurred den is zero, in exact arithmetic, exactly where no
+ * unit within 3r cells along both axes holds a sample; fp32 sums past 2^24 can
+ * leave a residual there, so the keep-the-prototype rule is applied on that
+ * support, counted exactly (and wherever the fp32 den is not positive). The
+ * passes run in a fixed order, so the result is the same bits on every run.
+ * Norms must be recomputed afterwards.
  */
 size_t som_update_workspace_bytes(int64_t V, int64_t E, int64_t N, int64_t chunk_features);
 

@@ -20,7 +20,9 @@
  *     count of assigned samples and, per feature, of those holding it), blurs
  *     both fields with three running-sum box passes along the rows and three
  *     along the columns (clamped window, unnormalised, fp32 as the paper
- *     fixes), and divides, leaving units with a zero denominator unchanged.
+ *     fixes), and divides, leaving units with no sample in their neighbourhood
+ *     unchanged (a zero denominator, read on the exact support: see below) and
+ *     keeping every quotient in [0, 1], the range of a mean of 0/1 inputs.
  *   - Discussion, sparse real-valued inputs: som_bmu_sf_oracle_host takes a
  *     value with every feature id (x_v real instead of 1) and ranks the same
  *     squared distance.
@@ -253,6 +255,33 @@ static void box_pass(float *line, int64_t n, int64_t stride, int64_t r, float *t
 }
 
 /* Three passes along every lattice row, then three along every lattice column. */
+/* sup[i] = occupied units (cnt > 0) within R cells of unit i along both lattice
+ * axes (windows clamped to the lattice): window counts along every row, then
+ * along every column, each from a prefix sum of whole numbers. */
+static int occupied_support(const int64_t *cnt, int64_t E, int64_t R, int64_t *sup)
+{
+    int64_t *pre = (int64_t *)malloc((size_t)(E + 1) * sizeof(int64_t));
+    if (!pre) return SOM_ORACLE_NO_MEM;
+    for (int64_t row = 0; row < E; ++row) {
+        pre[0] = 0;
+        for (int64_t c = 0; c < E; ++c) pre[c + 1] = pre[c] + (cnt[row * E + c] > 0 ? 1 : 0);
+        for (int64_t c = 0; c < E; ++c) {
+            const int64_t lo = c - R < 0 ? 0 : c - R, hi = c + R + 1 > E ? E : c + R + 1;
+            sup[row * E + c] = pre[hi] - pre[lo];
+        }
+    }
+    for (int64_t c = 0; c < E; ++c) {
+        pre[0] = 0;
+        for (int64_t row = 0; row < E; ++row) pre[row + 1] = pre[row] + sup[row * E + c];
+        for (int64_t row = 0; row < E; ++row) {
+            const int64_t lo = row - R < 0 ? 0 : row - R, hi = row + R + 1 > E ? E : row + R + 1;
+            sup[row * E + c] = pre[hi] - pre[lo];
+        }
+    }
+    free(pre);
+    return SOM_ORACLE_OK;
+}
+
 static void blur_field(float *f, int64_t E, int64_t r, float *tmp)
 {
     for (int64_t row = 0; row < E; ++row)
@@ -275,11 +304,12 @@ int som_update_oracle_host(const float *W_in, int64_t V, int64_t E, const int32_
     if (N > 0 && row_ptr[N] > row_ptr[0] && !col_idx) return SOM_ORACLE_BAD_ARG;
 
     int64_t *cnt = (int64_t *)calloc((size_t)M, sizeof(int64_t));
+    int64_t *sup = (int64_t *)calloc((size_t)M, sizeof(int64_t));
     float *den = (float *)malloc((size_t)M * sizeof(float));
     float *num = (float *)malloc((size_t)M * sizeof(float));
     float *tmp = (float *)malloc((size_t)E * sizeof(float));
     int rc = SOM_ORACLE_OK;
-    if (!cnt || !den || !num || !tmp) {
+    if (!cnt || !sup || !den || !num || !tmp) {
         rc = SOM_ORACLE_NO_MEM;
         goto done;
     }
@@ -288,6 +318,12 @@ int som_update_oracle_host(const float *W_in, int64_t V, int64_t E, const int32_
     for (int64_t s = 0; s < N; ++s) cnt[bmu[s]] += 1;
     for (int64_t i = 0; i < M; ++i) den[i] = (float)cnt[i];
     blur_field(den, E, radius, tmp);
+    /* Where the blurred denominator is zero in exact arithmetic: no occupied unit
+     * within 3*radius cells along both axes (three windows of half-width radius,
+     * clamped to the lattice, reach exactly that far). fp32 running sums that pass
+     * 2^24 can leave a residual there, so the keep-the-prototype rule is taken on
+     * this support, counted in whole numbers. */
+    if ((rc = occupied_support(cnt, E, 3 * radius, sup)) != SOM_ORACLE_OK) goto done;
 
     /* num, one feature at a time: samples per unit holding feature v (x binary) */
     for (int64_t v = 0; v < V; ++v) {
@@ -302,11 +338,21 @@ int som_update_oracle_host(const float *W_in, int64_t V, int64_t E, const int32_
             }
         for (int64_t i = 0; i < M; ++i) num[i] = (float)cnt[i];
         blur_field(num, E, radius, tmp);
-        /* the prototype becomes the neighbourhood mean; a unit whose blurred
-         * denominator is zero keeps its prototype */
-        for (int64_t i = 0; i < M; ++i) W_out[v * M + i] = den[i] > 0.0f ? num[i] / den[i] : W_in[v * M + i];
+        /* the prototype becomes the neighbourhood mean, a mean of 0/1 inputs and so in
+         * [0, 1] (the quotient of rounded sums is clamped there); a unit with no sample
+         * in its neighbourhood, or whose rounded denominator is not positive, keeps its
+         * prototype */
+        for (int64_t i = 0; i < M; ++i) {
+            if (sup[i] > 0 && den[i] > 0.0f) {
+                const float q = num[i] / den[i];
+                W_out[v * M + i] = fminf(fmaxf(q, 0.0f), 1.0f);
+            } else {
+                W_out[v * M + i] = W_in[v * M + i];
+            }
+        }
     }
 done:
+    free(sup);
     free(cnt);
     free(den);
     free(num);

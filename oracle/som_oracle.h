@@ -81,13 +81,20 @@ int som_bmu_sf_oracle_host(const float *W, int64_t ldw, int64_t V, int64_t i0, i
  *   bmu     host int32[N], the best unit of every sample (from a search).
  *   radius  box half-width r >= 1 (the schedule's sigma rounded to whole cells,
  *           at least one).
- *   W_out   host float[V*M]: num/den where the blurred den > 0, else W_in.
+ *   W_out   host float[V*M]: num/den clamped to [0, 1] where the unit has a
+ *           sample within 3r cells along both axes and the blurred den > 0,
+ *           else W_in.
  * num[v][i] = number of samples at unit i holding feature v, den[i] = number of
  * samples at unit i, both converted to fp32, then blurred: three box passes
  * along every lattice row, then three along every lattice column, each pass a
  * running window sum over the clamped window (first window summed in ascending
  * order, then add the element entering, subtract the one leaving), unnormalised,
- * in fp32; the quotient is an fp32 division. Plain loops, one thread.
+ * in fp32; the quotient is an fp32 division. In exact arithmetic the blurred den
+ * is zero exactly where no unit within 3r cells along both axes holds a sample
+ * (three clamped windows of half-width r reach that far); fp32 running sums past
+ * 2^24 can leave a residual there (or a wrong quotient near its edge), so units
+ * outside that support -- counted exactly, in whole numbers -- keep W_in, and
+ * quotients are clamped to [0, 1]. Plain loops, one thread.
  */
 int som_update_oracle_host(const float *W_in, int64_t V, int64_t E, const int32_t *row_ptr, const int32_t *col_idx,
                            int64_t N, const int32_t *bmu, int64_t radius, float *W_out);

@@ -504,6 +504,8 @@ static som_status update_impl(const Book &b, void *W, int64_t V, int64_t E, cons
     char *w = static_cast<char *>(workspace);
     som::UpdateBuffers ub;
     ub.den_cnt = reinterpret_cast<int32_t *>(w + L.den_cnt);
+    ub.sup_row = reinterpret_cast<int32_t *>(w + L.sup_row);
+    ub.sup = reinterpret_cast<int32_t *>(w + L.sup);
     ub.den_a = reinterpret_cast<float *>(w + L.den_a);
     ub.den_b = reinterpret_cast<float *>(w + L.den_b);
     ub.start = reinterpret_cast<int32_t *>(w + L.start);

@@ -142,6 +142,7 @@ hipError_t launch_order(const int32_t *row_ptr, const int32_t *col_idx, const fl
 // and two float buffers of chunk * M.
 struct UpdateBuffers {
     int32_t *den_cnt;
+    int32_t *sup_row, *sup;  // the exact support of the blurred den (row windows, then both axes)
     float *den_a, *den_b;
     int32_t *start, *cursor, *slot, *hunit, *order;
     int32_t *cnt;
@@ -149,7 +150,7 @@ struct UpdateBuffers {
 };
 
 struct UpdateLayout {
-    size_t den_cnt, den_a, den_b, start, cursor, slot, hunit, order, cnt, a, b, total;
+    size_t den_cnt, sup_row, sup, den_a, den_b, start, cursor, slot, hunit, order, cnt, a, b, total;
 };
 
 inline UpdateLayout update_layout(int64_t M, int64_t N, int64_t chunk)
@@ -162,6 +163,8 @@ inline UpdateLayout update_layout(int64_t M, int64_t N, int64_t chunk)
         return at;
     };
     L.den_cnt = take((size_t)M * 4);
+    L.sup_row = take((size_t)M * 4);
+    L.sup = take((size_t)M * 4);
     L.den_a = take((size_t)M * 4);
     L.den_b = take((size_t)M * 4);
     L.start = take((size_t)(M + 2) * 4);

@@ -16,9 +16,13 @@
 //      sum over the clamped window (the first window summed in ascending order,
 //      then per step the element entering added and the one leaving subtracted),
 //      unnormalised -- the constant cancels in the quotient;
-//   3. replaces every prototype by num / den (fp32 division), leaving a unit whose
-//      blurred den is zero unchanged; an fp16 codebook receives the quotient
-//      rounded once to binary16 at this final write.
+//   3. replaces every prototype by num / den (fp32 division), clamped to [0, 1] (a
+//      mean of 0/1 inputs), leaving a unit unchanged where no sample lies in its
+//      neighbourhood; an fp16 codebook receives the quotient rounded once to
+//      binary16 at this final write. In exact arithmetic the blurred den is zero
+//      exactly where no unit within 3r cells along both axes holds a sample, but
+//      fp32 running sums past 2^24 can leave a residual there, so that support is
+//      counted separately in whole numbers (k_support) and decides the rule.
 // A lane owns one lattice line (row or column) of one field and runs its three
 // passes sequentially, exactly in the order above, so the result is the same
 // bits on every run. The quotient is fused with the one transpose, from the
@@ -337,12 +341,34 @@ __global__ __launch_bounds__(256) void k_blur3(const In *src, float *x, float *y
     }
 }
 
-// W[v0 + v][i] = num[i][v] / den[i] where den[i] > 0 (fp32; rounded once to binary16
-// for an fp16 codebook), unchanged elsewhere: the quotient fused with the transpose
-// from unit-major to feature-major, in 64 (units) x 64 (features) tiles through LDS.
+// Occupied units counted over windows of half-width R along lattice lines, one lane per
+// line: rows (in = the den counts, counted where > 0; out[r][c] = occupied units in row r
+// within R of column c), then columns (in = the row counts, summed). Whole numbers, exact.
+__global__ __launch_bounds__(256) void k_support(const int32_t *__restrict__ in, int32_t *__restrict__ out,
+                                                 int64_t E, int64_t R, int rows)
+{
+    const int64_t l = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (l >= E) return;
+    const int64_t first = rows ? l * E : l, step = rows ? 1 : E;
+    auto val = [&](int64_t j) { return rows ? (in[first + j * step] > 0 ? 1 : 0) : in[first + j * step]; };
+    int32_t s = 0;
+    for (int64_t j = 0; j <= R && j < E; ++j) s += val(j);
+    out[first] = s;
+    for (int64_t i = 1; i < E; ++i) {
+        if (i + R < E) s += val(i + R);
+        if (i - R - 1 >= 0) s -= val(i - R - 1);
+        out[first + i * step] = s;
+    }
+}
+
+// W[v0 + v][i] = num[i][v] / den[i], clamped to [0, 1], where unit i has a sample in its
+// neighbourhood (sup[i] > 0) and den[i] > 0 (fp32; rounded once to binary16 for an fp16
+// codebook), unchanged elsewhere: the quotient fused with the transpose from unit-major
+// to feature-major, in 64 (units) x 64 (features) tiles through LDS.
 template <typename E>
 __global__ __launch_bounds__(256) void k_quotient_t(E *__restrict__ W, const float *__restrict__ num,
-                                                    const float *__restrict__ den, int64_t f, int64_t M, int64_t v0)
+                                                    const float *__restrict__ den, const int32_t *__restrict__ sup,
+                                                    int64_t f, int64_t M, int64_t v0)
 {
     __shared__ float tile[64][65];
     const int64_t it = (M + 63) / 64, vt = (f + 63) / 64;
@@ -354,9 +380,9 @@ __global__ __launch_bounds__(256) void k_quotient_t(E *__restrict__ W, const flo
         __syncthreads();
         if (i0 + tx < M) {
             const float d = den[i0 + tx];
-            if (d > 0.0f)
+            if (sup[i0 + tx] > 0 && d > 0.0f)
                 for (int y = ty; y < 64; y += 4)
-                    if (w0 + y < f) W[(v0 + w0 + y) * M + i0 + tx] = (E)(tile[tx][y] / d);
+                    if (w0 + y < f) W[(v0 + w0 + y) * M + i0 + tx] = (E)fminf(fmaxf(tile[tx][y] / d, 0.0f), 1.0f);
         }
         __syncthreads();
     }
@@ -404,6 +430,9 @@ hipError_t launch_update(bool f16, void *W, int64_t V, int64_t E, const int32_t 
     hipLaunchKernelGGL(k_heavy_scatter, dim3(lg), dim3(1024), 0, st, bmu, N, M, ub.start, ub.slot, ub.hunit, ub.cursor,
                        ub.order);
     blur(ub.den_cnt, ub.den_a, ub.den_b, 1, E, radius, st);
+    const unsigned lines = (unsigned)((E + 255) / 256);
+    hipLaunchKernelGGL(k_support, dim3(lines), dim3(256), 0, st, ub.den_cnt, ub.sup_row, E, 3 * radius, 1);
+    hipLaunchKernelGGL(k_support, dim3(lines), dim3(256), 0, st, ub.sup_row, ub.sup, E, 3 * radius, 0);
     const int64_t runs = (N + kRunSamples - 1) / kRunSamples;
     for (int64_t v0 = 0; v0 < V; v0 += chunk) {
         const int64_t f = V - v0 < chunk ? V - v0 : chunk;
@@ -418,10 +447,10 @@ hipError_t launch_update(bool f16, void *W, int64_t V, int64_t E, const int32_t 
         const unsigned qg = (unsigned)(qt < (1 << 20) ? qt : (1 << 20));
         if (f16)
             hipLaunchKernelGGL(k_quotient_t<_Float16>, dim3(qg), dim3(256), 0, st, static_cast<_Float16 *>(W), ub.b,
-                               ub.den_b, f, M, v0);
+                               ub.den_b, ub.sup, f, M, v0);
         else
             hipLaunchKernelGGL(k_quotient_t<float>, dim3(qg), dim3(256), 0, st, static_cast<float *>(W), ub.b,
-                               ub.den_b, f, M, v0);
+                               ub.den_b, ub.sup, f, M, v0);
     }
     return hipGetLastError();
 }

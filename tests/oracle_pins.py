@@ -446,6 +446,38 @@ def check_update_impulse_and_pair(lib):
     assert np.allclose(got2[0][k1 == 1.0] + got2[5][k1 == 1.0], 1.0, rtol=0, atol=1e-6)
 
 
+def residual_case():
+    """A batch whose blurred den, summed in fp32 with running windows, keeps a residual outside the exact support:
+    352,197 samples at unit (2, 5) of a 10 x 10 lattice (all holding feature 0) and 17,570 at unit (0, 7) (feature
+    1), radius 1. The window sums pass 2^24, and the running sums leave den = 2 at four units of column 5 that no
+    sample reaches (rows 6-9: more than 3 cells from row 2)."""
+    E, r = 10, 1
+    n_a, n_b = 352_197, 17_570
+    bmu = np.concatenate([np.full(n_a, 2 * E + 5), np.full(n_b, 7)]).astype(np.int32)
+    rp = np.arange(n_a + n_b + 1, dtype=np.int32)
+    ci = np.concatenate([np.zeros(n_a), np.ones(n_b)]).astype(np.int32)
+    W = (0.125 + np.arange(2 * E * E, dtype=np.float32) / 1024).astype(np.float32).reshape(2, E * E)
+    return E, r, W, rp, ci, bmu
+
+
+def check_update_residual_support(lib):
+    """Units that no sample reaches (beyond 3r cells along either axis; exact integer arithmetic gives den = 0 there)
+    keep their prototype bit for bit even where the fp32 running sums leave a residual, and every prototype stays
+    in [0, 1], the range of a mean of 0/1 inputs."""
+    E, r, W, rp, ci, bmu = residual_case()
+    got = oracle.update(W, E, rp, ci, bmu, r, lib=lib)
+    occ = np.zeros((E, E), dtype=bool)
+    occ.flat[np.unique(bmu)] = True
+    near = np.zeros((E, E), dtype=bool)
+    for i, j in np.argwhere(occ):
+        near[max(0, i - 3 * r):i + 3 * r + 1, max(0, j - 3 * r):j + 3 * r + 1] = True
+    assert not near[6:, 5].any(), "the case's residual units must lie outside the support"
+    assert np.array_equal(got[:, ~near.ravel()], W[:, ~near.ravel()]), "units out of reach must keep their prototype"
+    assert ((got >= 0) & (got <= 1)).all()
+    # every unit in reach changed: the batch moves them all away from these prototypes
+    assert (got[:, near.ravel()] != W[:, near.ravel()]).all()
+
+
 GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
 
 
@@ -507,4 +539,5 @@ ALL_CHECKS = [
     check_update_direct_windows,
     check_update_impulse_and_pair,
     check_update_kernel_width,
+    check_update_residual_support,
 ]

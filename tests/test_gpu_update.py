@@ -154,3 +154,21 @@ def test_one_epoch_on_the_tiny_workload(dev):
         return oracle.distance_at(W1[:, i], ci[rp[k]:rp[k + 1]])
 
     check_margin_rule(b2.cpu().numpy(), d2.cpu().numpy(), b2_ref, d2_ref, dd2_ref, dist_at, what="epoch 2")
+
+
+@pytest.mark.parametrize("f16", [False, True])
+def test_update_residual_den_keeps_unreached_units(dev, f16):
+    """fp32 running sums past 2^24 leave den = 2 at four units no sample reaches (the oracle pins' residual case,
+    369,767 samples on a 10 x 10 lattice): the kernels take the keep-the-prototype rule on the exact support, as the
+    oracle does, so the codebook matches it bit for bit and those units keep their prototype."""
+    import oracle_pins
+
+    E, r, W, rp, ci, bmu = oracle_pins.residual_case()
+    if f16:
+        W = W.astype(np.float16)
+    got = gpu_update(W, rp, ci, bmu, E, r, dev)
+    ref = oracle.update(W.astype(np.float32), E, rp, ci, bmu, r).astype(W.dtype)
+    assert np.array_equal(got, ref)
+    unreached = np.zeros((E, E), dtype=bool)
+    unreached[6:, 5] = True
+    assert np.array_equal(got[:, unreached.ravel()], W[:, unreached.ravel()])

@@ -6,7 +6,7 @@ and by a mutation check: each plausible slip planted in a copy of oracle.c
 (wrong sign, dropped square, dropped term, transposed stride, wrong
 tie-break, lost block offset, wrong second best, dropped feature, the
 rank-2/rank-3 slips of the two-best oracle, the value slips of the
-real-valued oracle, and the window, pass and quotient slips of the update)
+real-valued oracle, and the window, pass, quotient and support slips of the update)
 must make at least one pin fail.
 """
 import os
@@ -51,7 +51,9 @@ MUTANTS = [
     ("sf_value_squared", "x[v] = (double)values[p];", "x[v] = (double)values[p] * (double)values[p];"),
     ("box_window_off_by_one", "if (i - r - 1 >= 0) s -= line[(i - r - 1) * stride];",
      "if (i - r >= 0) s -= line[(i - r) * stride];"),
-    ("zero_den_filled", "? num[i] / den[i] : W_in[v * M + i];", "? num[i] / den[i] : 0.0f;"),
+    ("zero_den_filled", "W_out[v * M + i] = W_in[v * M + i];", "W_out[v * M + i] = 0.0f;"),
+    ("support_ignored", "if (sup[i] > 0 && den[i] > 0.0f) {", "if (den[i] > 0.0f) {"),
+    ("support_radius_r", "occupied_support(cnt, E, 3 * radius, sup)", "occupied_support(cnt, E, radius, sup)"),
     ("two_row_passes", "for (int pass = 0; pass < 3; ++pass) box_pass(f + row * E, E, 1, r, tmp);",
      "for (int pass = 0; pass < 2; ++pass) box_pass(f + row * E, E, 1, r, tmp);"),
     ("columns_skipped", "for (int pass = 0; pass < 3; ++pass) box_pass(f + col, E, E, r, tmp);",
