@@ -177,7 +177,8 @@ som_status som_bmu_search_noalloc(const float *W, const double *norms, int64_t V
  *
  * som_bmu_plan -- tile plan (Algorithm 2, step 5; SpMM-tile kernel section):
  *   unless keep_order is set, the batch is first regrouped by each sample's
- *   least frequent feature (a permuted copy in the workspace); then, for each
+ *   least frequent feature (a permutation and its row offsets in the workspace;
+ *   the rows are read from row_ptr / col_idx through it); then, for each
  *   tile of tile_samples consecutive rows, the ascending list of the distinct
  *   feature ids its rows hold, each with a bit mask of the rows holding it.
  *   Also clears and sets the input flags.

@@ -113,12 +113,12 @@ som_status carve(void *ws, size_t bytes, int64_t N, int64_t M, int64_t V, int64_
     c->ob.freq = reinterpret_cast<uint32_t *>(b + L.freq);
     c->ob.bucket = reinterpret_cast<unsigned long long *>(b + L.bucket);
     c->ob.skey = reinterpret_cast<int32_t *>(b + L.skey);
+    c->ob.rank = reinterpret_cast<unsigned long long *>(b + L.rank);
     c->ob.inv = reinterpret_cast<int32_t *>(b + L.inv);
     c->ob.res = reinterpret_cast<som::Staged *>(b + L.res);
     c->ob.res2 = k.layout_top2() ? reinterpret_cast<som::Staged *>(b + L.res2) : nullptr;
     c->ob.prp = reinterpret_cast<int32_t *>(b + L.prp);
-    c->ob.pci = reinterpret_cast<int32_t *>(b + L.pci);
-    c->ob.pvals = k.real ? reinterpret_cast<float *>(b + L.pvals) : nullptr;
+    c->ob.psrc = reinterpret_cast<int32_t *>(b + L.psrc);
     c->vals = k.real ? reinterpret_cast<float *>(b + L.vals) : nullptr;
     c->xsq = k.real ? reinterpret_cast<double *>(b + L.xsq) : nullptr;
     return SOM_OK;
@@ -189,16 +189,12 @@ som_status plan_impl(const int32_t *row_ptr, const int32_t *col_idx, const float
     hipStream_t s = static_cast<hipStream_t>(stream);
     hipError_t e = som::launch_clear_flags(c.flags, s);
     if (e != hipSuccess) return hip_fail(e, who);
-    const int32_t *rp = row_ptr, *ci = col_idx;
-    const float *vs = k.real ? values : nullptr;
     if (o.order) {
-        e = som::launch_order(row_ptr, col_idx, vs, N, nnz, V, c.ob, c.flags, s);
+        e = som::launch_order(row_ptr, col_idx, N, nnz, V, c.ob, c.flags, s);
         if (e != hipSuccess) return hip_fail(e, who);
-        rp = c.ob.prp;
-        ci = c.ob.pci;
-        if (vs) vs = c.ob.pvals;
     }
-    e = som::launch_plan(o.ta, rp, ci, vs, N, nnz, V, c.plan, c.tiles, c.vals, c.xsq, c.flags, s);
+    e = som::launch_plan(o.ta, row_ptr, col_idx, k.real ? values : nullptr, N, nnz, V, o.order ? &c.ob : nullptr,
+                         c.plan, c.tiles, c.vals, c.xsq, c.flags, s);
     if (e != hipSuccess) return hip_fail(e, who);
     return ok();
 }

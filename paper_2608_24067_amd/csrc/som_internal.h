@@ -41,16 +41,16 @@ struct Layout {
     size_t freq;    // uint32 [V+1]: feature counts of the batch
     size_t bucket;  // uint64 [V+1]: per-bucket (samples << 32 | ids) counts, then offsets
     size_t skey;    // int32 [N]: each sample's bucket
+    size_t rank;    // uint64 [N]: each sample's rank in its bucket (samples << 32 | ids before it)
     size_t inv;     // int32 [N]: each sample's position in the ordered batch (-1: never placed)
     size_t prp;     // int32 [N+1]: row pointers of the ordered batch
-    size_t pci;     // int32 [nnz]: feature ids of the ordered batch
+    size_t psrc;    // int32 [N]: where each position's row starts in the caller's col_idx
     size_t res;     // Staged [N]: best unit and distance by position, before they go back to input order
     size_t keys2;   // uint64 [n_strips * N]: per-strip second-smallest keys (two-best search only)
     size_t dots2;   // float [n_strips * N]: their dot products (two-best search only)
     size_t res2;    // Staged [N]: second unit and distance by position (two-best search, ordered batch only)
     size_t vals;    // float [nnz * TA]: sample values of every plan entry (real-valued rows only)
     size_t xsq;     // double [N]: ||x||^2 by batch position (real-valued rows only)
-    size_t pvals;   // float [nnz]: values of the ordered batch (real-valued rows, regrouped only)
     size_t total;
 };
 
@@ -77,9 +77,10 @@ inline Layout layout_for(int64_t N, int64_t M, int64_t V, int64_t nnz, int ta, b
     L.freq = take(o * (size_t)(V + 1) * 4);
     L.bucket = take(o * (size_t)(V + 1) * 8);
     L.skey = take(o * (size_t)N * 4);
+    L.rank = take(o * (size_t)N * 8);
     L.inv = take(o * (size_t)N * 4);
     L.prp = take(o * (size_t)(N + 1) * 4);
-    L.pci = take(o * (size_t)nnz * 4);
+    L.psrc = take(o * (size_t)N * 4);
     L.res = take(o * (size_t)N * sizeof(Staged));
     const size_t t2 = top2 ? 1 : 0;
     L.keys2 = take(t2 * (size_t)n_strips(M, ta) * (size_t)N * 8);
@@ -88,17 +89,15 @@ inline Layout layout_for(int64_t N, int64_t M, int64_t V, int64_t nnz, int ta, b
     const size_t r = real ? 1 : 0;
     L.vals = take(r * (size_t)nnz * (size_t)ta * 4);
     L.xsq = take(r * (size_t)N * 8);
-    L.pvals = take(r * o * (size_t)nnz * 4);
     L.total = off;
     return L;
 }
 
 struct OrderBuffers {
     uint32_t *freq;
-    unsigned long long *bucket;
-    int32_t *skey, *inv, *prp, *pci;
+    unsigned long long *bucket, *rank;
+    int32_t *skey, *inv, *prp, *psrc;
     Staged *res, *res2;  // results by position (res2: two-best only)
-    float *pvals;  // real-valued rows only
 };
 
 // Where the sweep leaves its per-(sample, strip) results.
@@ -117,10 +116,12 @@ hipError_t launch_norms(const float *W, int64_t V, int64_t M, double *norms, hip
 // fp16 codebooks: W holds IEEE binary16 bit patterns.
 hipError_t launch_norms_f16(const uint16_t *W, int64_t V, int64_t M, double *norms, hipStream_t st);
 hipError_t launch_clear_flags(uint32_t *flags, hipStream_t st);
-// values, vals, xsq: real-valued rows only (else null).
+// values, vals, xsq: real-valued rows only (else null). row_ptr, col_idx, values: the caller's batch.
+// ob non-null: the batch was regrouped: position p's row has plan offsets ob->prp[p] ... and its
+// ids start at ob->psrc[p] in the caller's col_idx.
 hipError_t launch_plan(int ta, const int32_t *row_ptr, const int32_t *col_idx, const float *values, int64_t N,
-                       int64_t nnz, int64_t V, uint2 *plan, int2 *tiles, float *vals, double *xsq, uint32_t *flags,
-                       hipStream_t st);
+                       int64_t nnz, int64_t V, const OrderBuffers *ob, uint2 *plan, int2 *tiles, float *vals,
+                       double *xsq, uint32_t *flags, hipStream_t st);
 // f16: W holds binary16 values; top2: fill keys2/dots2 too; vals: real-valued rows (tile 8 only).
 hipError_t launch_sweep(int ta, bool f16, bool top2, const void *W, const double *norms, int64_t M, int64_t N,
                         int64_t V, int64_t nnz, const uint2 *plan, const int2 *tiles, const float *vals,
@@ -131,8 +132,8 @@ hipError_t launch_sweep(int ta, bool f16, bool top2, const void *W, const double
 hipError_t launch_finalize(int ta, const double *norms, int64_t M, const int32_t *row_ptr, int64_t N, int64_t nnz,
                            const OrderBuffers *ob, const double *xsq, const SweepOut &o, int32_t *bmu, double *dist,
                            int32_t *bmu2, double *dist2, hipStream_t st);
-hipError_t launch_order(const int32_t *row_ptr, const int32_t *col_idx, const float *values, int64_t N, int64_t nnz,
-                        int64_t V, const OrderBuffers &ob, uint32_t *flags, hipStream_t st);
+hipError_t launch_order(const int32_t *row_ptr, const int32_t *col_idx, int64_t N, int64_t nnz, int64_t V,
+                        const OrderBuffers &ob, uint32_t *flags, hipStream_t st);
 
 // ----------------------------------------------------------------- update
 

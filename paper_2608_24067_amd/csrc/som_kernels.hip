@@ -61,8 +61,10 @@ __global__ void k_clear_flags(uint32_t *flags) { flags[threadIdx.x] = 0u; }
 // the same or neighbouring tiles, which run close together in time, so a rare
 // codebook row is re-read while still in L2. A sample's result does not depend on where it
 // sits (its sum order is fixed by its own features), so the permutation never
-// shows in the output. The permuted batch is written to the workspace as a CSR
-// of its own (prp, pci); k_unpermute moves the results back to their samples.
+// shows in the output. The permuted batch is written to the workspace as row offsets
+// of its own (prp) and, per position, where that row's ids start in the caller's
+// batch (psrc), from which the plan reads them; k_unpermute moves the results back
+// to their samples.
 
 constexpr int kLdsHistMax = 32768;          // features whose counts fit the LDS histogram
 constexpr int64_t kFreqSample = 1ll << 25;  // ids counted: the ordering needs only a rough rarity rank
@@ -117,10 +119,13 @@ __device__ __forceinline__ void row_range(const int32_t *row_ptr, int64_t base, 
 
 // skey[s] = the sample's least frequent valid feature (ties: the larger id), V if it
 // has none; bucket[key] += (1 << 32) | row length: samples counted in the high
-// half, ids in the low half of one 64-bit word.
+// half, ids in the low half of one 64-bit word. The word the atomic returns is the
+// sample's rank in its bucket (samples and ids before it), kept in rank[s]: once the
+// buckets' starts are known it gives the sample's place without a second atomic.
 __global__ __launch_bounds__(256) void k_rarest(const int32_t *__restrict__ row_ptr, const int32_t *__restrict__ col_idx,
                                                 int64_t N, int64_t nnz, int32_t V, const uint32_t *__restrict__ freq,
                                                 int32_t *__restrict__ skey, u64 *__restrict__ bucket,
+                                                u64 *__restrict__ rank,
                                                 uint32_t *__restrict__ flags)
 {
     // the four lanes of a quad share a row (lane q of the quad takes ids q, q + 4, ...)
@@ -150,7 +155,7 @@ __global__ __launch_bounds__(256) void k_rarest(const int32_t *__restrict__ row_
         if (sub == 0) {
             const int key = best == kKeyNone ? V : (int)(V - 1 - (int)(unsigned)(best & 0xFFFFFFFFull));
             skey[s] = key;
-            atomicAdd(&bucket[key], (1ull << 32) | (u64)(re - rb));
+            rank[s] = atomicAdd(&bucket[key], (1ull << 32) | (u64)(re - rb));
         }
     }
     if (bad) atomicOr(flags, bad);
@@ -191,47 +196,26 @@ __global__ __launch_bounds__(1024) void k_bucket_scan(u64 *__restrict__ bucket, 
     if (t == 1023) *prp_end = (int32_t)(si[1023] < nnz ? si[1023] : nnz);
 }
 
-// Each sample takes the next (position, id offset) of its bucket with one atomic and
-// copies its ids (and values, for real-valued rows) there: sample s sits at position
-// inv[s] of the permuted batch, its ids from pci[prp[inv[s]]] on. A quad of
-// lanes shares a row: its first lane takes the atomic, the quad copies every
-// fourth id, so the reads of row_ptr and col_idx run in batch order and only the
-// writes scatter, as whole rows. Positions past N and id offsets past nnz (only
-// reachable with invalid row pointers) are dropped or clamped.
-constexpr int kPlaceLanes = 4;
-
-__global__ __launch_bounds__(256) void k_place(const int32_t *__restrict__ row_ptr, const int32_t *__restrict__ col_idx,
-                                               int64_t N, int64_t nnz, const int32_t *__restrict__ skey,
-                                               u64 *__restrict__ bucket, int32_t *__restrict__ inv,
-                                               int32_t *__restrict__ prp, int32_t *__restrict__ pci,
-                                               const float *__restrict__ values, float *__restrict__ pvals)
+// Sample s goes to its bucket's start plus its rank in the bucket (both packed as
+// samples << 32 | ids; the id halves never carry): it sits at position inv[s] of the
+// permuted batch, its ids at plan offsets prp[inv[s]] ..., and psrc[inv[s]] is where
+// its row starts in the caller's col_idx (past row_ptr[0]). The rows themselves are
+// not copied: the plan reads each position's ids from there. Positions past N and
+// offsets past nnz (only reachable with invalid row pointers or a workspace the
+// regrouping did not write) are dropped or clamped.
+__global__ __launch_bounds__(256) void k_place(const int32_t *__restrict__ row_ptr, int64_t N, int64_t nnz,
+                                               const int32_t *__restrict__ skey, const u64 *__restrict__ bucket,
+                                               const u64 *__restrict__ rank, int64_t nb, int32_t *__restrict__ inv,
+                                               int32_t *__restrict__ prp, int32_t *__restrict__ psrc)
 {
     const int64_t base = csr_base(row_ptr, nnz);
-    const int sub = threadIdx.x % kPlaceLanes;
-    constexpr int64_t per_block = 256 / kPlaceLanes;
-    uint32_t bad = 0;
-    for (int64_t s = (int64_t)blockIdx.x * per_block + threadIdx.x / kPlaceLanes; s < N;
-         s += (int64_t)gridDim.x * per_block) {
-        int64_t rb, re;
-        row_range(row_ptr, base, nnz, s, rb, re, bad);
-        u64 old = 0;
-        if (sub == 0) old = atomicAdd(&bucket[skey[s]], (1ull << 32) | (u64)(re - rb));
-        // the quad is active or idle as a whole (one row): its lanes read lane 0's word
-        old = dpp64<0x00>(old);
-        const int64_t ps = (int64_t)(old >> 32), pi = (int64_t)(old & 0xFFFFFFFFull);
-        if (sub == 0) inv[s] = ps < N ? (int32_t)ps : -1;
+    for (int64_t s = (int64_t)blockIdx.x * 256 + threadIdx.x; s < N; s += (int64_t)gridDim.x * 256) {
+        const u64 at = bucket[clamp64(skey[s], 0, nb - 1)] + rank[s];
+        const int64_t ps = (int64_t)(at >> 32), pi = (int64_t)(at & 0xFFFFFFFFull);
+        inv[s] = ps < N ? (int32_t)ps : -1;
         if (ps >= N) continue;
-        const int64_t dst = pi < nnz ? pi : nnz;
-        if (sub == 0) prp[ps] = (int32_t)dst;
-        const int64_t n = re - rb < nnz - dst ? re - rb : nnz - dst;
-        const int32_t *src = col_idx + base + rb;
-        int32_t *out = pci + dst;
-        for (int64_t q = sub; q < n; q += kPlaceLanes) out[q] = src[q];
-        if (values) {
-            const float *vs = values + base + rb;
-            float *vo = pvals + dst;
-            for (int64_t q = sub; q < n; q += kPlaceLanes) vo[q] = vs[q];
-        }
+        prp[ps] = (int32_t)(pi < nnz ? pi : nnz);
+        psrc[ps] = (int32_t)clamp64((int64_t)row_ptr[s] - base, 0, nnz);
     }
 }
 
@@ -249,12 +233,18 @@ constexpr int kPlanStage = 2048;  // ids staged in LDS per wave
 // writes more entries than its own CSR span, so no input can drive an access out
 // of bounds.
 //
+// Regrouped batch (psrc non-null): off (the regrouped row offsets, prp) places every
+// tile's entries and gives each position's row length; the row's ids start at
+// psrc[p] in the caller's col_idx (past src_ptr[0]), clamped to the batch. Otherwise
+// off is the caller's row_ptr and positions are samples.
+//
 // Real-valued rows (REAL, values given): every union entry also gets the TA values of
 // its samples (vals[entry*TA + s], written for the samples whose mask bit is set;
 // the other slots are never read), and every row the fp64 sum of its squared
 // values in its own order (xsq, by batch position), which is ||x||^2.
 template <int TA, bool REAL>
-__global__ __launch_bounds__(256) void k_plan(const int32_t *__restrict__ row_ptr, const int32_t *__restrict__ col_idx,
+__global__ __launch_bounds__(256) void k_plan(const int32_t *__restrict__ off, const int32_t *__restrict__ src_ptr,
+                                              const int32_t *__restrict__ psrc, const int32_t *__restrict__ col_idx,
                                               int64_t N, int64_t nnz, int32_t V, int64_t n_tiles,
                                               uint2 *__restrict__ plan, int2 *__restrict__ tiles,
                                               uint32_t *__restrict__ flags, const float *__restrict__ values,
@@ -266,7 +256,8 @@ __global__ __launch_bounds__(256) void k_plan(const int32_t *__restrict__ row_pt
     const int wv = wave_id();
     const int grp = lane / TA;
     const int sl = lane % TA;
-    const int64_t base = csr_base(row_ptr, nnz);
+    const int64_t base = csr_base(off, nnz);
+    const int64_t sbase = psrc ? csr_base(src_ptr, nnz) : base;
     uint32_t bad = 0;
 
     for (int64_t tb = (int64_t)blockIdx.x * kPlanWaves * G; tb < n_tiles; tb += (int64_t)gridDim.x * kPlanWaves * G) {
@@ -277,31 +268,43 @@ __global__ __launch_bounds__(256) void k_plan(const int32_t *__restrict__ row_pt
         int64_t wlo = 0, whi = 0;
         if (tw < n_tiles) {
             const int64_t te = tw + G < n_tiles ? tw + G : n_tiles;
-            wlo = clamp64((int64_t)row_ptr[tw * TA] - base, 0, nnz);
-            whi = clamp64((int64_t)row_ptr[te * TA < N ? te * TA : N] - base, wlo, nnz);
+            wlo = clamp64((int64_t)off[tw * TA] - base, 0, nnz);
+            whi = clamp64((int64_t)off[te * TA < N ? te * TA : N] - base, wlo, nnz);
         }
         int64_t lo = 0, hi = 0, b = 0, e = 0;
+        int64_t src = 0;  // where the lane's ids start in col_idx (past its base)
         if (live) {
             const int64_t s0 = t * TA;
             const int64_t s1 = s0 + TA < N ? s0 + TA : N;
-            lo = clamp64((int64_t)row_ptr[s0] - base, wlo, whi);
-            hi = clamp64((int64_t)row_ptr[s1] - base, lo, whi);
+            lo = clamp64((int64_t)off[s0] - base, wlo, whi);
+            hi = clamp64((int64_t)off[s1] - base, lo, whi);
             if (s0 + sl < N) {
-                const int64_t rb = (int64_t)row_ptr[s0 + sl] - base;
-                const int64_t re = (int64_t)row_ptr[s0 + sl + 1] - base;
+                const int64_t rb = (int64_t)off[s0 + sl] - base;
+                const int64_t re = (int64_t)off[s0 + sl + 1] - base;
                 if (re < rb || rb < lo || re > hi) bad |= SOM_FLAG_ROW_PTR;
                 b = clamp64(rb, lo, hi);
                 e = clamp64(re, b, hi);
+                src = b;
+                if (psrc) {
+                    // the caller's row at this position (its flags were set by the regrouping),
+                    // never reaching past the batch
+                    src = clamp64(psrc[s0 + sl], 0, nnz);
+                    if (nnz - src < e - b) e = b + (nnz - src);
+                }
             }
         }
         const bool staged = (whi - wlo) <= kPlanStage;  // wave-uniform
-        if (staged)
-            for (int64_t q = lane; q < whi - wlo; q += 64) stage[wv][q] = col_idx[base + wlo + q];
+        if (staged) {
+            if (psrc) {
+                for (int64_t q = 0; q < e - b; ++q) stage[wv][b - wlo + q] = col_idx[sbase + src + q];
+            } else {
+                for (int64_t q = lane; q < whi - wlo; q += 64) stage[wv][q] = col_idx[base + wlo + q];
+            }
+        }
         __syncthreads();
 
         // positions in 32 bits: every offset lies in [0, nnz] and nnz < 2^31
-        const int32_t *ids = col_idx + base;
-        const float *vsrc = REAL ? values + base : nullptr;
+        const int64_t shift = sbase + src - b;  // the lane's id q (b <= q < e) is col_idx[shift + q]
         int p = (int)b;
         const int pe = (int)e, plo = (int)lo, pwlo = (int)wlo;
         int cur = INT_MAX;
@@ -317,7 +320,7 @@ __global__ __launch_bounds__(256) void k_plan(const int32_t *__restrict__ row_pt
                 if constexpr (STAGED)
                     return stage[wv][q - pwlo];
                 else
-                    return ids[q];
+                    return col_idx[shift + q];
             };
             // next valid id of this lane's row (INT_MAX once the row is done), with its value;
             // ids outside [0, V) (invalid input) are skipped on a path of their own
@@ -335,7 +338,7 @@ __global__ __launch_bounds__(256) void k_plan(const int32_t *__restrict__ row_pt
                 }
                 cur = id;
                 if constexpr (REAL) {
-                    curv = vsrc[p];
+                    curv = values[shift + p];
                     sq = fma((double)curv, (double)curv, sq);
                 }
             };
@@ -544,8 +547,8 @@ hipError_t launch_clear_flags(uint32_t *flags, hipStream_t st)
 }
 
 hipError_t launch_plan(int ta, const int32_t *row_ptr, const int32_t *col_idx, const float *values, int64_t N,
-                       int64_t nnz, int64_t V, uint2 *plan, int2 *tiles, float *vals, double *xsq, uint32_t *flags,
-                       hipStream_t st)
+                       int64_t nnz, int64_t V, const OrderBuffers *ob, uint2 *plan, int2 *tiles, float *vals,
+                       double *xsq, uint32_t *flags, hipStream_t st)
 {
     const int64_t nt = n_tiles(N, ta);
     const int64_t per_block = (int64_t)kPlanWaves * (64 / ta);
@@ -553,24 +556,26 @@ hipError_t launch_plan(int ta, const int32_t *row_ptr, const int32_t *col_idx, c
     if (blocks > (1 << 22)) blocks = 1 << 22;
     const dim3 grid((unsigned)blocks), block(256);
     const int32_t v = (int32_t)V;
+    const int32_t *off = ob ? ob->prp : row_ptr;
+    const int32_t *psrc = ob ? ob->psrc : nullptr;
     if (values) {  // real-valued rows: tiles of 8 only
         if (ta != 8) return hipErrorInvalidValue;
-        hipLaunchKernelGGL((k_plan<8, true>), grid, block, 0, st, row_ptr, col_idx, N, nnz, v, nt, plan, tiles, flags,
-                           values, vals, xsq);
+        hipLaunchKernelGGL((k_plan<8, true>), grid, block, 0, st, off, row_ptr, psrc, col_idx, N, nnz, v, nt, plan,
+                           tiles, flags, values, vals, xsq);
         return hipGetLastError();
     }
     switch (ta) {
     case 8:
-        hipLaunchKernelGGL((k_plan<8, false>), grid, block, 0, st, row_ptr, col_idx, N, nnz, v, nt, plan, tiles, flags,
-                           nullptr, nullptr, nullptr);
+        hipLaunchKernelGGL((k_plan<8, false>), grid, block, 0, st, off, row_ptr, psrc, col_idx, N, nnz, v, nt, plan,
+                           tiles, flags, nullptr, nullptr, nullptr);
         break;
     case 16:
-        hipLaunchKernelGGL((k_plan<16, false>), grid, block, 0, st, row_ptr, col_idx, N, nnz, v, nt, plan, tiles,
-                           flags, nullptr, nullptr, nullptr);
+        hipLaunchKernelGGL((k_plan<16, false>), grid, block, 0, st, off, row_ptr, psrc, col_idx, N, nnz, v, nt, plan,
+                           tiles, flags, nullptr, nullptr, nullptr);
         break;
     case 32:
-        hipLaunchKernelGGL((k_plan<32, false>), grid, block, 0, st, row_ptr, col_idx, N, nnz, v, nt, plan, tiles,
-                           flags, nullptr, nullptr, nullptr);
+        hipLaunchKernelGGL((k_plan<32, false>), grid, block, 0, st, off, row_ptr, psrc, col_idx, N, nnz, v, nt, plan,
+                           tiles, flags, nullptr, nullptr, nullptr);
         break;
     default: return hipErrorInvalidValue;
     }
@@ -597,8 +602,8 @@ hipError_t launch_finalize(int ta, const double *norms, int64_t M, const int32_t
     return hipGetLastError();
 }
 
-hipError_t launch_order(const int32_t *row_ptr, const int32_t *col_idx, const float *values, int64_t N, int64_t nnz,
-                        int64_t V, const OrderBuffers &ob, uint32_t *flags, hipStream_t st)
+hipError_t launch_order(const int32_t *row_ptr, const int32_t *col_idx, int64_t N, int64_t nnz, int64_t V,
+                        const OrderBuffers &ob, uint32_t *flags, hipStream_t st)
 {
     const int64_t nb = V + 1;  // one bucket per feature, one for rows without a valid feature
     int64_t fb = (nb + 255) / 256;
@@ -614,12 +619,13 @@ hipError_t launch_order(const int32_t *row_ptr, const int32_t *col_idx, const fl
     int64_t qb = (N + 63) / 64;  // a row per quad of lanes
     if (qb > (1 << 22)) qb = 1 << 22;
     hipLaunchKernelGGL(k_rarest, dim3((unsigned)qb), dim3(256), 0, st, row_ptr, col_idx, N, nnz, (int32_t)V, ob.freq,
-                       ob.skey, ob.bucket, flags);
+                       ob.skey, ob.bucket, ob.rank, flags);
     hipLaunchKernelGGL(k_bucket_scan, dim3(1), dim3(1024), 0, st, ob.bucket, nb, nnz, ob.prp + N);
-    int64_t pb = (N + 256 / kPlaceLanes - 1) / (256 / kPlaceLanes);
+    int64_t pb = (N + 255) / 256;
     if (pb > (1 << 22)) pb = 1 << 22;
-    hipLaunchKernelGGL(k_place, dim3((unsigned)pb), dim3(256), 0, st, row_ptr, col_idx, N, nnz, ob.skey, ob.bucket,
-                       ob.inv, ob.prp, ob.pci, values, values ? ob.pvals : nullptr);
+    hipLaunchKernelGGL(k_place, dim3((unsigned)pb), dim3(256), 0, st, row_ptr, N, nnz, ob.skey, ob.bucket, ob.rank, nb,
+                       ob.inv,
+                       ob.prp, ob.psrc);
     return hipGetLastError();
 }
 

@@ -19,8 +19,8 @@ namespace som {
 hipError_t launch_norms(const float *, int64_t, int64_t, double *, hipStream_t) { reached("launch_norms"); }
 hipError_t launch_norms_f16(const uint16_t *, int64_t, int64_t, double *, hipStream_t) { reached("launch_norms_f16"); }
 hipError_t launch_clear_flags(uint32_t *, hipStream_t) { reached("launch_clear_flags"); }
-hipError_t launch_plan(int, const int32_t *, const int32_t *, const float *, int64_t, int64_t, int64_t, uint2 *, int2 *,
-                       float *, double *, uint32_t *, hipStream_t)
+hipError_t launch_plan(int, const int32_t *, const int32_t *, const float *, int64_t, int64_t, int64_t,
+                       const OrderBuffers *, uint2 *, int2 *, float *, double *, uint32_t *, hipStream_t)
 {
     reached("launch_plan");
 }
@@ -34,8 +34,8 @@ hipError_t launch_finalize(int, const double *, int64_t, const int32_t *, int64_
 {
     reached("launch_finalize");
 }
-hipError_t launch_order(const int32_t *, const int32_t *, const float *, int64_t, int64_t, int64_t,
-                        const OrderBuffers &, uint32_t *, hipStream_t)
+hipError_t launch_order(const int32_t *, const int32_t *, int64_t, int64_t, int64_t, const OrderBuffers &, uint32_t *,
+                        hipStream_t)
 {
     reached("launch_order");
 }

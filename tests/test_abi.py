@@ -90,8 +90,8 @@ def test_real_valued_workspace_and_checks():
     lib = som.load()
     n2 = som.workspace2_bytes(10_000, 4096, 2000, 120_000)
     nsf = som.workspace_sf_bytes(10_000, 4096, 2000, 120_000)
-    # per-entry values (8 per id), ||x||^2 per sample and the regrouped values on top of the two-best layout
-    assert nsf >= n2 + 32 * 120_000 + 8 * 10_000 + 4 * 120_000
+    # per-entry values (8 per id) and ||x||^2 per sample on top of the two-best layout
+    assert nsf >= n2 + 32 * 120_000 + 8 * 10_000
     assert lib.som_bmu_sf_workspace_bytes(10, 64, 100, 50, _cfg(16)) == 0  # tiles of 8 only
     assert lib.som_bmu_sf_search(FAKE, FAKE, 100, 64, FAKE, FAKE, None, 10, 50, FAKE, FAKE, None, None, FAKE,
                                  1 << 30, None, None) == som.SOM_ERR_INVALID_ARG  # no values
