@@ -480,8 +480,9 @@ static void sweep_ta(bool vec, dim3 grid, int64_t group_tiles, hipStream_t st, c
 {
     // Packed fp16 rows take half the registers: eight rows in flight still fit 128 VGPRs
     // (six for real-valued rows, whose per-entry values take scalar registers).
-    // fp32 rows of four neurons per lane take four registers: eight in flight.
-    constexpr int UV = (sizeof(E) == 2 && NPL == 8) ? (REAL ? 6 : 8) : (sizeof(E) == 4 && NPL == 4 ? 8 : 4);
+    // Tiles of 16 with fp32 rows of four neurons per lane: four registers a row, eight in
+    // flight (tiles of 32 keep four: their 128 accumulators leave no room).
+    constexpr int UV = (sizeof(E) == 2 && NPL == 8) ? (REAL ? 6 : 8) : (sizeof(E) == 4 && TA == 16 ? 8 : 4);
     if (vec)
         hipLaunchKernelGGL((k_sweep<E, TA, NPL, UV, true, TOP2, REAL>), grid, dim3(256), 0, st, W, norms, M, N, V, nnz,
                            plan, tiles, nt, o.keys, o.dots, o.keys2, o.dots2, vals, group_tiles);
@@ -495,9 +496,10 @@ static void sweep_ta(bool vec, dim3 grid, int64_t group_tiles, hipStream_t st, c
 // (regrouped) batch, but a strip must still span many rounds of resident
 // workgroups, or the chip works on two strips at once and their rows compete for
 // L2: up to 32 tiles, and at least 16,384 groups per strip where there are enough.
-// Between 62,000 and 131,000 tiles (the 1024 x 1024 map's 500,000 rows) two tiles per
-// wave still leave 7,500 groups (about seven rounds) per strip: 784 -> 769 ms there,
-// while 12 or 16 tiles (5,200 or 3,900 groups) cost 4-7%.
+// From 60,000 tiles on, groups hold at least 8 tiles (two per wave): the 1024 x 1024
+// map's 500,000 rows (62,500 tiles) then still span 7,800 groups, about seven rounds,
+// per strip, and the sweep takes 769 ms instead of 784; 12 or 16 tiles (5,200 or
+// 3,900 groups) cost 4-7%.
 static int64_t sweep_group_tiles(int64_t nt)
 {
     int64_t g = nt / 16384 / 4 * 4;
