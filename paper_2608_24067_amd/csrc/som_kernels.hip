@@ -222,7 +222,7 @@ __global__ __launch_bounds__(256) void k_place(const int32_t *__restrict__ row_p
 // ------------------------------------------------------------------ plan
 
 constexpr int kPlanWaves = 4;
-constexpr int kPlanStage = 2048;  // ids staged in LDS per wave
+constexpr int kPlanStage = 1024;  // ids staged in LDS per wave (16 KiB a workgroup: 2048 halves the workgroups a CU holds and costs 5% at 64x64)
 
 // A wave plans 64/TA consecutive tiles at once (TA = 2 ... 32): lane l works on row s = l % TA of
 // tile l / TA. Each step takes, per tile, the smallest current id over its TA
