@@ -79,9 +79,13 @@ typedef enum {
  * preconditions; its results are defined only as far as stated here: an id
  * outside [0, V) is left out of the row's dot products (the binary row's
  * ||x||^2, its length, still counts it), and rows with valid ids get the
- * results they get in a valid batch. Rows with unsorted or repeated ids, and
- * every row of a batch with bad row pointers, get in-range but unspecified
- * results; no input drives an access out of bounds. */
+ * results they get in a valid batch. Rows with unsorted or repeated ids get
+ * in-range but unspecified results. Row pointers are checked before any row
+ * is read: a batch whose row_ptr decreases or leaves [row_ptr[0],
+ * row_ptr[0] + nnz] is searched as if every row were empty (each sample gets
+ * the unit of smallest norm, lowest index first; its distance is unspecified
+ * when the batch is not regrouped), so overlapping rows cannot multiply the
+ * work. No input drives an access out of bounds. */
 #define SOM_FLAG_ID_RANGE 0x1u   /* a feature id outside [0, V) was skipped      */
 #define SOM_FLAG_UNSORTED 0x2u   /* a row's ids were not strictly ascending       */
 #define SOM_FLAG_ROW_PTR 0x4u    /* row_ptr decreased or left [row_ptr[0], +nnz]  */
@@ -345,7 +349,11 @@ som_status som_bmu_sf_finalize(const double *norms, int64_t V, int64_t M, const 
  * leave a residual there, so the keep-the-prototype rule is applied on that
  * support, counted exactly (and wherever the fp32 den is not positive). The
  * passes run in a fixed order, so the result is the same bits on every run.
- * Norms must be recomputed afterwards.
+ * Norms must be recomputed afterwards. N == 0 is a no-op. The row pointers
+ * are checked on the device before any row is read: if row_ptr[0] is
+ * negative, or row_ptr decreases or leaves [row_ptr[0], row_ptr[0] + nnz],
+ * the codebook is left unchanged (som_validate_csr_host checks the rest of
+ * the CSR rules; ids outside [0, V) are skipped).
  */
 size_t som_update_workspace_bytes(int64_t V, int64_t E, int64_t N, int64_t chunk_features);
 

@@ -189,6 +189,8 @@ som_status plan_impl(const int32_t *row_ptr, const int32_t *col_idx, const float
     hipStream_t s = static_cast<hipStream_t>(stream);
     hipError_t e = som::launch_clear_flags(c.flags, s);
     if (e != hipSuccess) return hip_fail(e, who);
+    e = som::launch_check_rows(row_ptr, N, nnz, c.flags, s);
+    if (e != hipSuccess) return hip_fail(e, who);
     if (o.order) {
         e = som::launch_order(row_ptr, col_idx, N, nnz, V, c.ob, c.flags, s);
         if (e != hipSuccess) return hip_fail(e, who);
@@ -497,8 +499,10 @@ static som_status update_impl(const Book &b, void *W, int64_t V, int64_t E, cons
     if (workspace_bytes < L.total)
         return fail(SOM_ERR_WORKSPACE, "%s: workspace holds %zu bytes, the update needs %zu", who, workspace_bytes,
                     L.total);
+    if (N == 0) return ok();  // no sample: every unit keeps its prototype
     char *w = static_cast<char *>(workspace);
     som::UpdateBuffers ub;
+    ub.flags = reinterpret_cast<uint32_t *>(w + L.flags);
     ub.den_cnt = reinterpret_cast<int32_t *>(w + L.den_cnt);
     ub.sup_row = reinterpret_cast<int32_t *>(w + L.sup_row);
     ub.sup = reinterpret_cast<int32_t *>(w + L.sup);

@@ -116,6 +116,9 @@ hipError_t launch_norms(const float *W, int64_t V, int64_t M, double *norms, hip
 // fp16 codebooks: W holds IEEE binary16 bit patterns.
 hipError_t launch_norms_f16(const uint16_t *W, int64_t V, int64_t M, double *norms, hipStream_t st);
 hipError_t launch_clear_flags(uint32_t *flags, hipStream_t st);
+// Flags SOM_FLAG_ROW_PTR when row_ptr decreases or leaves [row_ptr[0], row_ptr[0] + nnz];
+// the plan then reads the batch as empty.
+hipError_t launch_check_rows(const int32_t *row_ptr, int64_t N, int64_t nnz, uint32_t *flags, hipStream_t st);
 // values, vals, xsq: real-valued rows only (else null). row_ptr, col_idx, values: the caller's batch.
 // ob non-null: the batch was regrouped: position p's row has plan offsets ob->prp[p] ... and its
 // ids start at ob->psrc[p] in the caller's col_idx.
@@ -142,6 +145,7 @@ hipError_t launch_order(const int32_t *row_ptr, const int32_t *col_idx, int64_t 
 // cursor[M], slot[M], hunit[M], order[N]) and, for one chunk of features, counts
 // and two float buffers of chunk * M.
 struct UpdateBuffers {
+    uint32_t *flags;  // SOM_FLAG_ROW_PTR: the batch's row pointers are invalid, nothing is updated
     int32_t *den_cnt;
     int32_t *sup_row, *sup;  // the exact support of the blurred den (row windows, then both axes)
     float *den_a, *den_b;
@@ -151,7 +155,7 @@ struct UpdateBuffers {
 };
 
 struct UpdateLayout {
-    size_t den_cnt, sup_row, sup, den_a, den_b, start, cursor, slot, hunit, order, cnt, a, b, total;
+    size_t flags, den_cnt, sup_row, sup, den_a, den_b, start, cursor, slot, hunit, order, cnt, a, b, total;
 };
 
 inline UpdateLayout update_layout(int64_t M, int64_t N, int64_t chunk)
@@ -163,6 +167,7 @@ inline UpdateLayout update_layout(int64_t M, int64_t N, int64_t chunk)
         off += align256(bytes);
         return at;
     };
+    L.flags = take(256);
     L.den_cnt = take((size_t)M * 4);
     L.sup_row = take((size_t)M * 4);
     L.sup = take((size_t)M * 4);

@@ -53,6 +53,28 @@ __global__ __launch_bounds__(64) void k_norms(const E *__restrict__ W, int64_t V
 
 __global__ void k_clear_flags(uint32_t *flags) { flags[threadIdx.x] = 0u; }
 
+// Row pointers checked before any kernel walks a row: non-decreasing and inside
+// [row_ptr[0], row_ptr[0] + nnz], with row_ptr[0] >= 0. A batch that fails is flagged
+// (SOM_FLAG_ROW_PTR) and every later kernel of the plan reads it as empty (rows_nnz),
+// so row pointers that decrease cannot make rows overlap and multiply the work.
+__global__ __launch_bounds__(256) void k_check_rows(const int32_t *__restrict__ row_ptr, int64_t N, int64_t nnz,
+                                                    uint32_t *__restrict__ flags)
+{
+    const int64_t base = row_ptr[0];
+    bool bad = base < 0;
+    for (int64_t s = (int64_t)blockIdx.x * 256 + threadIdx.x; s < N; s += (int64_t)gridDim.x * 256) {
+        const int64_t a = (int64_t)row_ptr[s] - base, b = (int64_t)row_ptr[s + 1] - base;
+        if (b < a || a < 0 || b > nnz) bad = true;
+    }
+    if (__ballot(bad) != 0 && (threadIdx.x & 63) == 0) atomicOr(flags, SOM_FLAG_ROW_PTR);
+}
+
+// The ids a plan kernel may read: nnz, or none once the row pointers are flagged.
+__device__ __forceinline__ int64_t rows_nnz(const uint32_t *flags, int64_t nnz)
+{
+    return (flags[0] & SOM_FLAG_ROW_PTR) ? 0 : nnz;
+}
+
 // ----------------------------------------------------------------- order
 
 // Sample order. The post-submission section's tuning groups samples so that a
@@ -129,6 +151,7 @@ __global__ __launch_bounds__(256) void k_rarest(const int32_t *__restrict__ row_
                                                 uint32_t *__restrict__ flags)
 {
     // the four lanes of a quad share a row (lane q of the quad takes ids q, q + 4, ...)
+    nnz = rows_nnz(flags, nnz);
     const int64_t base = csr_base(row_ptr, nnz);
     const int sub = threadIdx.x & 3;
     uint32_t bad = 0;
@@ -206,8 +229,10 @@ __global__ __launch_bounds__(1024) void k_bucket_scan(u64 *__restrict__ bucket, 
 __global__ __launch_bounds__(256) void k_place(const int32_t *__restrict__ row_ptr, int64_t N, int64_t nnz,
                                                const int32_t *__restrict__ skey, const u64 *__restrict__ bucket,
                                                const u64 *__restrict__ rank, int64_t nb, int32_t *__restrict__ inv,
-                                               int32_t *__restrict__ prp, int32_t *__restrict__ psrc)
+                                               int32_t *__restrict__ prp, int32_t *__restrict__ psrc,
+                                               const uint32_t *__restrict__ flags)
 {
+    nnz = rows_nnz(flags, nnz);
     const int64_t base = csr_base(row_ptr, nnz);
     for (int64_t s = (int64_t)blockIdx.x * 256 + threadIdx.x; s < N; s += (int64_t)gridDim.x * 256) {
         const u64 at = bucket[clamp64(skey[s], 0, nb - 1)] + rank[s];
@@ -256,6 +281,7 @@ __global__ __launch_bounds__(256) void k_plan(const int32_t *__restrict__ off, c
     const int wv = wave_id();
     const int grp = lane / TA;
     const int sl = lane % TA;
+    nnz = rows_nnz(flags, nnz);
     const int64_t base = csr_base(off, nnz);
     const int64_t sbase = psrc ? csr_base(src_ptr, nnz) : base;
     uint32_t bad = 0;
@@ -546,6 +572,15 @@ hipError_t launch_clear_flags(uint32_t *flags, hipStream_t st)
     return hipGetLastError();
 }
 
+hipError_t launch_check_rows(const int32_t *row_ptr, int64_t N, int64_t nnz, uint32_t *flags, hipStream_t st)
+{
+    int64_t blocks = (N + 255) / 256;
+    if (blocks < 1) blocks = 1;
+    if (blocks > 4096) blocks = 4096;
+    hipLaunchKernelGGL(k_check_rows, dim3((unsigned)blocks), dim3(256), 0, st, row_ptr, N, nnz, flags);
+    return hipGetLastError();
+}
+
 hipError_t launch_plan(int ta, const int32_t *row_ptr, const int32_t *col_idx, const float *values, int64_t N,
                        int64_t nnz, int64_t V, const OrderBuffers *ob, uint2 *plan, int2 *tiles, float *vals,
                        double *xsq, uint32_t *flags, hipStream_t st)
@@ -624,8 +659,7 @@ hipError_t launch_order(const int32_t *row_ptr, const int32_t *col_idx, int64_t 
     int64_t pb = (N + 255) / 256;
     if (pb > (1 << 22)) pb = 1 << 22;
     hipLaunchKernelGGL(k_place, dim3((unsigned)pb), dim3(256), 0, st, row_ptr, N, nnz, ob.skey, ob.bucket, ob.rank, nb,
-                       ob.inv,
-                       ob.prp, ob.psrc);
+                       ob.inv, ob.prp, ob.psrc, flags);
     return hipGetLastError();
 }
 

@@ -240,9 +240,10 @@ __global__ __launch_bounds__(256) void k_count_light(const int32_t *__restrict__
                                                      const int32_t *__restrict__ col_idx, int64_t N, int64_t nnz,
                                                      const int32_t *__restrict__ bmu, int64_t M,
                                                      const int32_t *__restrict__ units, int32_t v0, int32_t v1,
-                                                     int32_t *__restrict__ cnt)
+                                                     int32_t *__restrict__ cnt, const uint32_t *__restrict__ flags)
 {
-    const int64_t base = row_ptr[0];
+    if (flags[0] & SOM_FLAG_ROW_PTR) return;  // invalid row pointers: no row is read
+    const int64_t base = row_ptr[0];           // >= 0 once the row pointers passed the check
     const int64_t f = (int64_t)v1 - v0;
     for (int64_t s = (int64_t)blockIdx.x * 256 + threadIdx.x; s < N; s += (int64_t)gridDim.x * 256) {
         const int32_t u = bmu[s];
@@ -265,10 +266,11 @@ __global__ __launch_bounds__(256) void k_count_heavy(const int32_t *__restrict__
                                                      const int32_t *__restrict__ units,
                                                      const int32_t *__restrict__ start,
                                                      const int32_t *__restrict__ order, int32_t v0, int32_t v1,
-                                                     int32_t *__restrict__ cnt)
+                                                     int32_t *__restrict__ cnt, const uint32_t *__restrict__ flags)
 {
     __shared__ uint32_t hist[kLdsBins];
-    const int64_t base = row_ptr[0];
+    if (flags[0] & SOM_FLAG_ROW_PTR) return;  // uniform: invalid row pointers, no row is read
+    const int64_t base = row_ptr[0];           // >= 0 once the row pointers passed the check
     const int64_t f = (int64_t)v1 - v0;
     const int64_t total = start[M];
     const int64_t p0 = (int64_t)blockIdx.x * kRunSamples;
@@ -368,9 +370,10 @@ __global__ __launch_bounds__(256) void k_support(const int32_t *__restrict__ in,
 template <typename E>
 __global__ __launch_bounds__(256) void k_quotient_t(E *__restrict__ W, const float *__restrict__ num,
                                                     const float *__restrict__ den, const int32_t *__restrict__ sup,
-                                                    int64_t f, int64_t M, int64_t v0)
+                                                    int64_t f, int64_t M, int64_t v0, const uint32_t *__restrict__ flags)
 {
     __shared__ float tile[64][65];
+    if (flags[0] & SOM_FLAG_ROW_PTR) return;  // uniform: invalid row pointers leave the codebook as it is
     const int64_t it = (M + 63) / 64, vt = (f + 63) / 64;
     const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;  // 64 x 4 threads
     for (int64_t t = blockIdx.x; t < it * vt; t += gridDim.x) {
@@ -417,6 +420,10 @@ hipError_t launch_update(bool f16, void *W, int64_t V, int64_t E, const int32_t 
                          const UpdateBuffers &ub, hipStream_t st)
 {
     const int64_t M = E * E;
+    // row pointers checked before any row is read: a batch that fails updates nothing
+    hipError_t e = launch_clear_flags(ub.flags, st);
+    if (e == hipSuccess) e = launch_check_rows(row_ptr, N, nnz, ub.flags, st);
+    if (e != hipSuccess) return e;
     // den: counts, blur, kept in ub.den_b; the samples of heavy units sorted by unit
     const unsigned sg = (unsigned)((N + 255) / 256 < kScanBlocks ? (N + 255) / 256 + 1 : kScanBlocks);
     const unsigned lg = (unsigned)((N + 1023) / 1024 < 512 ? (N + 1023) / 1024 + 1 : 512);
@@ -438,19 +445,19 @@ hipError_t launch_update(bool f16, void *W, int64_t V, int64_t E, const int32_t 
         const int64_t f = V - v0 < chunk ? V - v0 : chunk;
         hipLaunchKernelGGL(k_zero_i32, dim3(grid_for(f * M)), dim3(256), 0, st, ub.cnt, f * M);
         hipLaunchKernelGGL(k_count_light, dim3(grid_for(N)), dim3(256), 0, st, row_ptr, col_idx, N, nnz, bmu, M,
-                           ub.den_cnt, (int32_t)v0, (int32_t)(v0 + f), ub.cnt);
+                           ub.den_cnt, (int32_t)v0, (int32_t)(v0 + f), ub.cnt, ub.flags);
         if (runs > 0)
             hipLaunchKernelGGL(k_count_heavy, dim3((unsigned)runs), dim3(256), 0, st, row_ptr, col_idx, nnz, bmu, M,
-                               ub.den_cnt, ub.start, ub.order, (int32_t)v0, (int32_t)(v0 + f), ub.cnt);
+                               ub.den_cnt, ub.start, ub.order, (int32_t)v0, (int32_t)(v0 + f), ub.cnt, ub.flags);
         blur(ub.cnt, ub.a, ub.b, f, E, radius, st);
         const int64_t qt = ((M + 63) / 64) * ((f + 63) / 64);
         const unsigned qg = (unsigned)(qt < (1 << 20) ? qt : (1 << 20));
         if (f16)
             hipLaunchKernelGGL(k_quotient_t<_Float16>, dim3(qg), dim3(256), 0, st, static_cast<_Float16 *>(W), ub.b,
-                               ub.den_b, ub.sup, f, M, v0);
+                               ub.den_b, ub.sup, f, M, v0, ub.flags);
         else
             hipLaunchKernelGGL(k_quotient_t<float>, dim3(qg), dim3(256), 0, st, static_cast<float *>(W), ub.b,
-                               ub.den_b, ub.sup, f, M, v0);
+                               ub.den_b, ub.sup, f, M, v0, ub.flags);
     }
     return hipGetLastError();
 }

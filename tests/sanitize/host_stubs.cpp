@@ -19,6 +19,7 @@ namespace som {
 hipError_t launch_norms(const float *, int64_t, int64_t, double *, hipStream_t) { reached("launch_norms"); }
 hipError_t launch_norms_f16(const uint16_t *, int64_t, int64_t, double *, hipStream_t) { reached("launch_norms_f16"); }
 hipError_t launch_clear_flags(uint32_t *, hipStream_t) { reached("launch_clear_flags"); }
+hipError_t launch_check_rows(const int32_t *, int64_t, int64_t, uint32_t *, hipStream_t) { reached("launch_check_rows"); }
 hipError_t launch_plan(int, const int32_t *, const int32_t *, const float *, int64_t, int64_t, int64_t,
                        const OrderBuffers *, uint2 *, int2 *, float *, double *, uint32_t *, hipStream_t)
 {

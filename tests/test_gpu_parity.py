@@ -277,6 +277,40 @@ def test_negative_first_offset_reads_as_empty(dev, tile, keep):
         assert ((b >= 0) & (b < M)).all() and np.isfinite(d).all()
 
 
+@pytest.mark.parametrize("tile,keep", [(8, False), (8, True), (16, False)])
+def test_decreasing_row_ptr_reads_as_empty(dev, tile, keep):
+    """Row pointers that decrease would let rows overlap ([0, nnz, 0, nnz, ...]: every even row spans the whole
+    batch) and multiply the work. They are checked before any row is read: the batch is flagged and searched as if
+    every row were empty, so every sample gets the unit of smallest norm, lowest index first (its distance too, when
+    the batch is regrouped: the regrouped rows are all empty). The sizes keep even the overlapping walk short."""
+    V, M, N = 300, 500, 2000
+    rp, ci, W = case(44, N, V, M, synth.UNIFORM)
+    nnz = int(rp[-1])
+    bad = np.zeros(N + 1, np.int32)
+    bad[1::2] = nnz
+    with pytest.raises(som.SomError):
+        som.validate_csr_host(bad, ci, V)
+    Wd = to_dev(W, dev)
+    norms = som.codebook_norms(Wd, V, M)
+    nrm = norms.cpu().numpy()
+    order = np.argsort(nrm, kind="stable")  # ascending norm, lower index first among equal norms
+    for two in (False, True):
+        ws = (som.alloc_workspace2 if two else som.alloc_workspace)(N, M, V, nnz, dev, tile, keep)
+        search = som.bmu2_search if two else som.bmu_search
+        out = search(Wd, norms, to_dev(bad, dev), to_dev(ci, dev), V, M, nnz=nnz, workspace=ws,
+                     tile_samples=tile, keep_order=keep)
+        flags = som.input_flags(ws, N, M, V, nnz, tile, keep)
+        assert flags & som.FLAG_ROW_PTR, hex(flags)
+        res = [t.cpu().numpy() for t in out]
+        assert (res[0] == order[0]).all()
+        if two:
+            assert (res[2] == order[1]).all()
+        if not keep:
+            assert (res[1] == nrm[order[0]]).all()
+            if two:
+                assert (res[3] == nrm[order[1]]).all()
+
+
 @pytest.mark.parametrize("name,rows", [("64", 4096), ("256", 1024), ("512", 256)])
 def test_workload_prefix(dev, name, rows):
     # the first rows of a full-size workload (rows are drawn per (seed, row)), full map

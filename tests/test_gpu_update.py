@@ -114,6 +114,25 @@ def test_update_empty_batch_keeps_codebook(dev):
     assert np.array_equal(got, W)
 
 
+@pytest.mark.parametrize("how", ["decreasing", "negative_first"])
+def test_update_invalid_row_ptr_keeps_codebook(dev, how):
+    """Row pointers that decrease (overlapping rows), or a negative first offset (which would name ids before
+    col_idx), are caught on the device before any row is read, and the update then leaves the codebook as it is."""
+    rp, ci, W, bmu = update_case(108, 600, 80, 10)
+    nnz = int(rp[-1])
+    if how == "decreasing":
+        bad = rp.copy()
+        bad[1::2] = nnz
+    else:
+        bad = (rp - 3).astype(np.int32)
+    with pytest.raises(som.SomError):
+        som.validate_csr_host(bad, ci, 80)
+    Wd = to_dev(W, dev)
+    som.update(Wd, to_dev(bad, dev), to_dev(ci, dev), to_dev(bmu, dev), 80, 10, 2, nnz=nnz)
+    torch.cuda.synchronize()
+    assert np.array_equal(Wd.cpu().numpy(), W)
+
+
 def test_update_f16(dev):
     rp, ci, W, bmu = update_case(99, 3000, 400, 24, spread=0.5)
     W16 = W.astype(np.float16)
