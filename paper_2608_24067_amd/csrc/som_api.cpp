@@ -508,6 +508,7 @@ static som_status update_impl(const Book &b, void *W, int64_t V, int64_t E, cons
     ub.sup = reinterpret_cast<int32_t *>(w + L.sup);
     ub.den_a = reinterpret_cast<float *>(w + L.den_a);
     ub.den_b = reinterpret_cast<float *>(w + L.den_b);
+    ub.den_blur = reinterpret_cast<float *>(w + L.den_blur);
     ub.start = reinterpret_cast<int32_t *>(w + L.start);
     ub.cursor = reinterpret_cast<int32_t *>(w + L.cursor);
     ub.slot = reinterpret_cast<int32_t *>(w + L.slot);

@@ -148,14 +148,15 @@ struct UpdateBuffers {
     uint32_t *flags;  // SOM_FLAG_ROW_PTR: the batch's row pointers are invalid, nothing is updated
     int32_t *den_cnt;
     int32_t *sup_row, *sup;  // the exact support of the blurred den (row windows, then both axes)
-    float *den_a, *den_b;
+    float *den_a, *den_b;  // scratch of the den blur
+    float *den_blur;       // the blurred den
     int32_t *start, *cursor, *slot, *hunit, *order;
     int32_t *cnt;
     float *a, *b;
 };
 
 struct UpdateLayout {
-    size_t flags, den_cnt, sup_row, sup, den_a, den_b, start, cursor, slot, hunit, order, cnt, a, b, total;
+    size_t flags, den_cnt, sup_row, sup, den_a, den_b, den_blur, start, cursor, slot, hunit, order, cnt, a, b, total;
 };
 
 inline UpdateLayout update_layout(int64_t M, int64_t N, int64_t chunk)
@@ -173,6 +174,7 @@ inline UpdateLayout update_layout(int64_t M, int64_t N, int64_t chunk)
     L.sup = take((size_t)M * 4);
     L.den_a = take((size_t)M * 4);
     L.den_b = take((size_t)M * 4);
+    L.den_blur = take((size_t)M * 4);
     L.start = take((size_t)(M + 2) * 4);
     L.cursor = take((size_t)M * 4);
     L.slot = take((size_t)M * 4);

@@ -24,8 +24,8 @@
 //      fp32 running sums past 2^24 can leave a residual there, so that support is
 //      counted separately in whole numbers (k_support) and decides the rule.
 // A lane owns one lattice line (row or column) of one field and runs its three
-// passes sequentially, exactly in the order above, so the result is the same
-// bits on every run. The quotient is fused with the one transpose, from the
+// passes in one sweep of the line, each pass exactly in the order above, so the
+// result is the same bits on every run; the blurred field replaces the counts. The quotient is fused with the one transpose, from the
 // unit-major fields to the feature-major codebook. Features are processed in
 // chunks, so the workspace holds three fields of chunk * M values rather than V * M.
 
@@ -309,37 +309,81 @@ __global__ __launch_bounds__(256) void k_count_heavy(const int32_t *__restrict__
     }
 }
 
-// One running-sum box pass over a line of n values (stride apart), half-width r.
-template <typename In>
-__device__ __forceinline__ void box_pass(const In *in, float *out, int64_t n, int64_t stride, int64_t r)
-{
-    float s = 0.0f;
-    for (int64_t j = 0; j <= r && j < n; ++j) s += (float)in[j * stride];
-    out[0] = s;
-    for (int64_t i = 1; i < n; ++i) {
-        if (i + r < n) s += (float)in[(i + r) * stride];
-        if (i - r - 1 >= 0) s -= (float)in[(i - r - 1) * stride];
-        out[i * stride] = s;
-    }
-}
-
-// Three box passes along lines of n values, `stride` apart: src -> x -> y -> x (src
-// is the integer counts for the row passes). Fields are unit-major: element (r, c) of feature v
-// is at (r * E + c) * f + v. Line l is feature v = l % f of the line k = l / f, and
-// starts at k * outer + v; neighbouring lanes take neighbouring features, so every
-// step of every pass is one coalesced read. Row passes (along c): outer = E * f,
-// stride = f; column passes (along r): outer = f, stride = E * f.
-// Result in x. src may be y (its line is read in full before y is written); the
-// lines of different lanes are disjoint.
-template <typename In>
-__global__ __launch_bounds__(256) void k_blur3(const In *src, float *x, float *y, int64_t lines, int64_t f,
-                                               int64_t outer, int64_t n, int64_t stride, int64_t r)
+// Three running-sum box passes of half-width r along lines of n values, `stride`
+// apart, in one sweep of each line. Pass k+1 takes every value of pass k as pass k
+// produces it -- that is the value entering pass k+1's window -- and reads the value
+// leaving its window back from where pass k stored it (x holds pass 1's output, y
+// pass 2's). Each pass is still exactly the oracle's sequence of fp32 operations: its
+// first window summed in ascending order, then per step the entering value added and
+// the leaving one subtracted. Per element that is four reads and three writes, where
+// three separate passes take six reads and three writes.
+// in holds the first pass's input as 32-bit words: integer counts (INT) or float
+// bits. out receives the third pass as float bits and may be in itself: out[i] is
+// written once pass 1 has gone past i + 2m (m = min(r, n - 1)), after its last read
+// of in[i] at i + r + 1. The words are read and written through one type, so no
+// access to in and out can be reordered across another.
+// Fields are unit-major: element (r, c) of feature v is at (r * E + c) * f + v. Line
+// l is feature v = l % f of the line k = l / f and starts at k * outer + v;
+// neighbouring lanes take neighbouring features, so every step is one coalesced
+// access per lane group. Row passes (along c): outer = E * f, stride = f; column
+// passes (along r): outer = f, stride = E * f. The lines of different lanes are
+// disjoint.
+template <bool INT>
+__global__ __launch_bounds__(256) void k_blur3(const uint32_t *in, float *x, float *y, uint32_t *out, int64_t lines,
+                                               int64_t f, int64_t outer, int64_t n, int64_t stride, int64_t r)
 {
     for (int64_t l = (int64_t)blockIdx.x * 256 + threadIdx.x; l < lines; l += (int64_t)gridDim.x * 256) {
         const int64_t off = (l / f) * outer + l % f;
-        box_pass(src + off, x + off, n, stride, r);
-        box_pass(x + off, y + off, n, stride, r);
-        box_pass(y + off, x + off, n, stride, r);
+        const uint32_t *src = in + off;
+        float *px = x + off, *py = y + off;
+        uint32_t *dst = out + off;
+        auto input = [&](int64_t k) {
+            const uint32_t u = src[k * stride];
+            return INT ? (float)(int32_t)u : __uint_as_float(u);
+        };
+        const int64_t m = r < n - 1 ? r : n - 1;  // the first window is [0, m]
+        float s1 = 0.0f, s2 = 0.0f;
+        int64_t next1 = 0, next2 = 0;  // the next output index of passes 2 and 3
+        // pass 3 receives pass 2's output j
+        auto feed2 = [&](int64_t j, float v) {
+            py[j * stride] = v;
+            s2 += v;
+            if (j >= m) {  // output i = j - m: its first window is complete, or v entered at i + r
+                const int64_t i = j - m;
+                if (i - r - 1 >= 0) s2 -= py[(i - r - 1) * stride];
+                dst[i * stride] = __float_as_uint(s2);
+                next2 = i + 1;
+            }
+        };
+        // pass 2 receives pass 1's output j
+        auto feed1 = [&](int64_t j, float v) {
+            px[j * stride] = v;
+            s1 += v;
+            if (j >= m) {
+                const int64_t i = j - m;
+                if (i - r - 1 >= 0) s1 -= px[(i - r - 1) * stride];
+                feed2(i, s1);
+                next1 = i + 1;
+            }
+        };
+        // pass 1
+        float s0 = 0.0f;
+        for (int64_t k = 0; k <= m; ++k) s0 += input(k);
+        feed1(0, s0);
+        for (int64_t i = 1; i < n; ++i) {
+            if (i + r < n) s0 += input(i + r);
+            if (i - r - 1 >= 0) s0 -= input(i - r - 1);
+            feed1(i, s0);
+        }
+        // passes 2 and 3 past the last entering value: only leaving values remain
+        for (int64_t i = next1; i < n; ++i) {
+            if (i - r - 1 >= 0) s1 -= px[(i - r - 1) * stride];
+            feed2(i, s1);
+        }
+        for (int64_t i = next2; i < n; ++i) {
+            if (i - r - 1 >= 0) s2 -= py[(i - r - 1) * stride];
+            dst[i * stride] = __float_as_uint(s2);
+        }
     }
 }
 
@@ -405,12 +449,15 @@ unsigned grid_for(int64_t n)
 }
 
 // The blur of f unit-major lattices (E x E) of counts: three row passes, then three
-// column passes. Result in b.
-void blur(const int32_t *cnt, float *a, float *b, int64_t f, int64_t E, int64_t r, hipStream_t st)
+// column passes, with a and b as the passes' scratch. Result in out (fp32), which
+// may be the counts themselves.
+void blur(const int32_t *cnt, float *a, float *b, float *out, int64_t f, int64_t E, int64_t r, hipStream_t st)
 {
     const unsigned g = grid_for(f * E);
-    hipLaunchKernelGGL(k_blur3<int32_t>, dim3(g), dim3(256), 0, st, cnt, a, b, f * E, f, E * f, E, f, r);  // -> a
-    hipLaunchKernelGGL(k_blur3<float>, dim3(g), dim3(256), 0, st, a, b, a, f * E, f, f, E, E * f, r);      // -> b
+    const uint32_t *in = reinterpret_cast<const uint32_t *>(cnt);
+    uint32_t *o = reinterpret_cast<uint32_t *>(out);
+    hipLaunchKernelGGL(k_blur3<true>, dim3(g), dim3(256), 0, st, in, a, b, o, f * E, f, E * f, E, f, r);
+    hipLaunchKernelGGL(k_blur3<false>, dim3(g), dim3(256), 0, st, o, a, b, o, f * E, f, f, E, E * f, r);
 }
 
 }  // namespace
@@ -424,7 +471,7 @@ hipError_t launch_update(bool f16, void *W, int64_t V, int64_t E, const int32_t 
     hipError_t e = launch_clear_flags(ub.flags, st);
     if (e == hipSuccess) e = launch_check_rows(row_ptr, N, nnz, ub.flags, st);
     if (e != hipSuccess) return e;
-    // den: counts, blur, kept in ub.den_b; the samples of heavy units sorted by unit
+    // den: counts, blur, kept in ub.den_blur; the samples of heavy units sorted by unit
     const unsigned sg = (unsigned)((N + 255) / 256 < kScanBlocks ? (N + 255) / 256 + 1 : kScanBlocks);
     const unsigned lg = (unsigned)((N + 1023) / 1024 < 512 ? (N + 1023) / 1024 + 1 : 512);
     hipLaunchKernelGGL(k_zero_i32, dim3(grid_for(M)), dim3(256), 0, st, ub.den_cnt, M);
@@ -436,7 +483,7 @@ hipError_t launch_update(bool f16, void *W, int64_t V, int64_t E, const int32_t 
                        ub.hunit);
     hipLaunchKernelGGL(k_heavy_scatter, dim3(lg), dim3(1024), 0, st, bmu, N, M, ub.start, ub.slot, ub.hunit, ub.cursor,
                        ub.order);
-    blur(ub.den_cnt, ub.den_a, ub.den_b, 1, E, radius, st);
+    blur(ub.den_cnt, ub.den_a, ub.den_b, ub.den_blur, 1, E, radius, st);
     const unsigned lines = (unsigned)((E + 255) / 256);
     hipLaunchKernelGGL(k_support, dim3(lines), dim3(256), 0, st, ub.den_cnt, ub.sup_row, E, 3 * radius, 1);
     hipLaunchKernelGGL(k_support, dim3(lines), dim3(256), 0, st, ub.sup_row, ub.sup, E, 3 * radius, 0);
@@ -449,15 +496,16 @@ hipError_t launch_update(bool f16, void *W, int64_t V, int64_t E, const int32_t 
         if (runs > 0)
             hipLaunchKernelGGL(k_count_heavy, dim3((unsigned)runs), dim3(256), 0, st, row_ptr, col_idx, nnz, bmu, M,
                                ub.den_cnt, ub.start, ub.order, (int32_t)v0, (int32_t)(v0 + f), ub.cnt, ub.flags);
-        blur(ub.cnt, ub.a, ub.b, f, E, radius, st);
+        float *num = reinterpret_cast<float *>(ub.cnt);  // the blur's result replaces the counts
+        blur(ub.cnt, ub.a, ub.b, num, f, E, radius, st);
         const int64_t qt = ((M + 63) / 64) * ((f + 63) / 64);
         const unsigned qg = (unsigned)(qt < (1 << 20) ? qt : (1 << 20));
         if (f16)
-            hipLaunchKernelGGL(k_quotient_t<_Float16>, dim3(qg), dim3(256), 0, st, static_cast<_Float16 *>(W), ub.b,
-                               ub.den_b, ub.sup, f, M, v0, ub.flags);
+            hipLaunchKernelGGL(k_quotient_t<_Float16>, dim3(qg), dim3(256), 0, st, static_cast<_Float16 *>(W), num,
+                               ub.den_blur, ub.sup, f, M, v0, ub.flags);
         else
-            hipLaunchKernelGGL(k_quotient_t<float>, dim3(qg), dim3(256), 0, st, static_cast<float *>(W), ub.b,
-                               ub.den_b, ub.sup, f, M, v0, ub.flags);
+            hipLaunchKernelGGL(k_quotient_t<float>, dim3(qg), dim3(256), 0, st, static_cast<float *>(W), num,
+                               ub.den_blur, ub.sup, f, M, v0, ub.flags);
     }
     return hipGetLastError();
 }
