@@ -335,7 +335,7 @@ som_status som_bmu_sf_finalize(const double *norms, int64_t V, int64_t M, const 
  *   chunk_features  features blurred per pass (0 = all V); the workspace holds
  *                   three chunk x M fields, so smaller chunks need less memory.
  * som_update_workspace_bytes(V, E, N, chunk_features) sizes the workspace for a
- * batch of N samples (three chunk x M fields, nine M-sized buffers and N int32
+ * batch of N samples (three chunk x M fields, ten M-sized buffers and N int32
  * positions for sorting the samples of crowded units); 0 for invalid sizes.
  * Per unit, den = samples assigned to it and num[v] = those holding feature v
  * (exact integer counts), both converted to fp32 and blurred by three
