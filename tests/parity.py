@@ -10,6 +10,8 @@ The bar (stated with the numbers in each helper):
 """
 from __future__ import annotations
 
+import os
+
 import numpy as np
 import torch
 
@@ -18,6 +20,16 @@ import paper_2608_24067_amd.som as som
 
 DIST_RTOL = 1e-5
 MARGIN = 1e-4
+# Oracle runs above this many element-updates (rows x V x M) take the streamed, merged
+# oracle over the host's threads (pinned against one whole call in the oracle's tests).
+THREADED_WORK = 2e9
+HOST_THREADS = max(1, min(16, os.cpu_count() or 1))
+
+
+def _threads(nthreads: int, rows, W) -> int:
+    if nthreads == 1 and len(rows) * W.shape[0] * W.shape[1] > THREADED_WORK:
+        return HOST_THREADS
+    return nthreads
 
 
 def to_dev(a: np.ndarray, dev):
@@ -76,6 +88,7 @@ def compare(W: np.ndarray, row_ptr, col_idx, b_gpu, d_gpu, exact: bool, what="",
     sub_ci = (np.concatenate([col_idx[row_ptr[r]:row_ptr[r + 1]] for r in rows]) if len(rows)
               else np.zeros(0, np.int32))
     M = W.shape[1]
+    nthreads = _threads(nthreads, rows, W)
     if nthreads > 1:
         b_ref, d_ref, d2_ref = oracle.bmu_streamed(lambda i0, i1: np.ascontiguousarray(W[:, i0:i1]), M, sub_rp,
                                                    sub_ci, block=max(256, -(-M // nthreads)), nthreads=nthreads)
@@ -154,6 +167,7 @@ def compare2(W, row_ptr, col_idx, g, exact: bool, what="", rows=None, nthreads=1
     sub_rp[1:] = np.cumsum(row_ptr[rows + 1] - row_ptr[rows])
     sub_ci = (np.concatenate([col_idx[row_ptr[r]:row_ptr[r + 1]] for r in rows]) if len(rows)
               else np.zeros(0, np.int32))
+    nthreads = _threads(nthreads, rows, W)
     if nthreads > 1:
         M = W.shape[1]
         ref = oracle.bmu2_streamed(lambda i0, i1: np.ascontiguousarray(W[:, i0:i1]), M, sub_rp, sub_ci,
@@ -198,6 +212,7 @@ def compare_sf(W, row_ptr, col_idx, values, g, exact: bool, what="", rows=None, 
     idx = np.concatenate(pick) if len(rows) else np.zeros(0, np.int64)
     sub_ci, sub_v = col_idx[idx], values[idx]
     M = W.shape[1]
+    nthreads = _threads(nthreads, rows, W)
     if nthreads > 1:
         ref = oracle.bmu_sf_streamed(lambda i0, i1: np.ascontiguousarray(W[:, i0:i1]), M, sub_rp, sub_ci, sub_v,
                                      block=max(256, -(-M // nthreads)), nthreads=nthreads)
