@@ -117,8 +117,7 @@ som_status carve(void *ws, size_t bytes, int64_t N, int64_t M, int64_t V, int64_
     c->ob.inv = reinterpret_cast<int32_t *>(b + L.inv);
     c->ob.res = reinterpret_cast<som::Staged *>(b + L.res);
     c->ob.res2 = k.layout_top2() ? reinterpret_cast<som::Staged *>(b + L.res2) : nullptr;
-    c->ob.prp = reinterpret_cast<int32_t *>(b + L.prp);
-    c->ob.psrc = reinterpret_cast<int32_t *>(b + L.psrc);
+    c->ob.pos = reinterpret_cast<int32_t *>(b + L.pos);
     c->vals = k.real ? reinterpret_cast<float *>(b + L.vals) : nullptr;
     c->xsq = k.real ? reinterpret_cast<double *>(b + L.xsq) : nullptr;
     return SOM_OK;
@@ -235,8 +234,7 @@ som_status finalize_impl(const Kind &k, const double *norms, int64_t V, int64_t 
         return fail(SOM_ERR_INVALID_ARG, "%s: null pointer", who);
     if ((st = setup(N, M, V, nnz, config, workspace, workspace_bytes, k, &o, &c, &noop)) != SOM_OK) return st;
     if (noop) return ok();
-    const int32_t *rp = o.order ? c.ob.prp : row_ptr;
-    hipError_t e = som::launch_finalize(o.ta, norms, M, rp, N, nnz, o.order ? &c.ob : nullptr, c.xsq, c.out, bmu, dist,
+    hipError_t e = som::launch_finalize(o.ta, norms, M, row_ptr, N, nnz, o.order ? &c.ob : nullptr, c.xsq, c.out, bmu, dist,
                                         k.top2 ? bmu2 : nullptr, k.top2 ? dist2 : nullptr,
                                         static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, who);

@@ -43,8 +43,8 @@ struct Layout {
     size_t skey;    // int32 [N]: each sample's bucket
     size_t rank;    // uint64 [N]: each sample's rank in its bucket (samples << 32 | ids before it)
     size_t inv;     // int32 [N]: each sample's position in the ordered batch (-1: never placed)
-    size_t prp;     // int32 [N+1]: row pointers of the ordered batch
-    size_t psrc;    // int32 [N]: where each position's row starts in the caller's col_idx
+    size_t pos;     // int32 [2N+2]: per position p of the ordered batch, pos[2p] = its row offset and
+                    // pos[2p+1] = where its ids start in the caller's col_idx; pos[2N] = all ids
     size_t res;     // Staged [N]: best unit and distance by position, before they go back to input order
     size_t keys2;   // uint64 [n_strips * N]: per-strip second-smallest keys (two-best search only)
     size_t dots2;   // float [n_strips * N]: their dot products (two-best search only)
@@ -79,8 +79,7 @@ inline Layout layout_for(int64_t N, int64_t M, int64_t V, int64_t nnz, int ta, b
     L.skey = take(o * (size_t)N * 4);
     L.rank = take(o * (size_t)N * 8);
     L.inv = take(o * (size_t)N * 4);
-    L.prp = take(o * (size_t)(N + 1) * 4);
-    L.psrc = take(o * (size_t)N * 4);
+    L.pos = take(o * (size_t)(N + 1) * 8);
     L.res = take(o * (size_t)N * sizeof(Staged));
     const size_t t2 = top2 ? 1 : 0;
     L.keys2 = take(t2 * (size_t)n_strips(M, ta) * (size_t)N * 8);
@@ -96,7 +95,7 @@ inline Layout layout_for(int64_t N, int64_t M, int64_t V, int64_t nnz, int ta, b
 struct OrderBuffers {
     uint32_t *freq;
     unsigned long long *bucket, *rank;
-    int32_t *skey, *inv, *prp, *psrc;
+    int32_t *skey, *inv, *pos;
     Staged *res, *res2;  // results by position (res2: two-best only)
 };
 
@@ -120,8 +119,8 @@ hipError_t launch_clear_flags(uint32_t *flags, hipStream_t st);
 // the plan then reads the batch as empty.
 hipError_t launch_check_rows(const int32_t *row_ptr, int64_t N, int64_t nnz, uint32_t *flags, hipStream_t st);
 // values, vals, xsq: real-valued rows only (else null). row_ptr, col_idx, values: the caller's batch.
-// ob non-null: the batch was regrouped: position p's row has plan offsets ob->prp[p] ... and its
-// ids start at ob->psrc[p] in the caller's col_idx.
+// ob non-null: the batch was regrouped: position p's row has plan offsets ob->pos[2p] ... and its
+// ids start at ob->pos[2p + 1] in the caller's col_idx.
 hipError_t launch_plan(int ta, const int32_t *row_ptr, const int32_t *col_idx, const float *values, int64_t N,
                        int64_t nnz, int64_t V, const OrderBuffers *ob, uint2 *plan, int2 *tiles, float *vals,
                        double *xsq, uint32_t *flags, hipStream_t st);
@@ -130,8 +129,8 @@ hipError_t launch_sweep(int ta, bool f16, bool top2, const void *W, const double
                         int64_t V, int64_t nnz, const uint2 *plan, const int2 *tiles, const float *vals,
                         const SweepOut &o, hipStream_t st);
 // bmu2/dist2 non-null: the two best units. xsq: real-valued rows (else ||x||^2 = nnz of the row).
-// ob non-null: the batch was regrouped (row_ptr is the ordered batch's); results are staged by
-// position and then moved to their samples.
+// ob non-null: the batch was regrouped (the row lengths come from ob->pos, not row_ptr); results
+// are staged by position and then moved to their samples.
 hipError_t launch_finalize(int ta, const double *norms, int64_t M, const int32_t *row_ptr, int64_t N, int64_t nnz,
                            const OrderBuffers *ob, const double *xsq, const SweepOut &o, int32_t *bmu, double *dist,
                            int32_t *bmu2, double *dist2, hipStream_t st);

@@ -87,8 +87,8 @@ __device__ __forceinline__ int64_t rows_nnz(const uint32_t *flags, int64_t nnz)
 // codebook row is re-read while still in L2. A sample's result does not depend on where it
 // sits (its sum order is fixed by its own features), so the permutation never
 // shows in the output. The permuted batch is written to the workspace as row offsets
-// of its own (prp) and, per position, where that row's ids start in the caller's
-// batch (psrc), from which the plan reads them; k_unpermute moves the results back
+// of its own and, per position, where that row's ids start in the caller's batch
+// (both in pos, interleaved), from which the plan reads them; k_unpermute moves the results back
 // to their samples.
 
 constexpr int kLdsHistMax = 32768;          // features whose counts fit the LDS histogram
@@ -188,7 +188,7 @@ __global__ __launch_bounds__(256) void k_rarest(const int32_t *__restrict__ row_
 }
 
 // One workgroup: exclusive scan of the nb packed bucket counts into packed starting
-// offsets (sample offset << 32 | id offset). prp[N] = total ids (capped at nnz).
+// offsets (sample offset << 32 | id offset). *prp_end = total ids (capped at nnz).
 __global__ __launch_bounds__(1024) void k_bucket_scan(u64 *__restrict__ bucket, int64_t nb, int64_t nnz,
                                                       int32_t *__restrict__ prp_end)
 {
@@ -224,7 +224,7 @@ __global__ __launch_bounds__(1024) void k_bucket_scan(u64 *__restrict__ bucket, 
 
 // Sample s goes to its bucket's start plus its rank in the bucket (both packed as
 // samples << 32 | ids; the id halves never carry): it sits at position inv[s] of the
-// permuted batch, its ids at plan offsets prp[inv[s]] ..., and psrc[inv[s]] is where
+// permuted batch, its ids at plan offsets pos[2 inv[s]] ..., and pos[2 inv[s] + 1] is where
 // its row starts in the caller's col_idx (past row_ptr[0]). The rows themselves are
 // not copied: the plan reads each position's ids from there. Positions past N and
 // offsets past nnz (only reachable with invalid row pointers or a workspace the
@@ -232,8 +232,7 @@ __global__ __launch_bounds__(1024) void k_bucket_scan(u64 *__restrict__ bucket, 
 __global__ __launch_bounds__(256) void k_place(const int32_t *__restrict__ row_ptr, int64_t N, int64_t nnz,
                                                const int32_t *__restrict__ skey, const u64 *__restrict__ bucket,
                                                const u64 *__restrict__ rank, int64_t nb, int32_t *__restrict__ inv,
-                                               int32_t *__restrict__ prp, int32_t *__restrict__ psrc,
-                                               const uint32_t *__restrict__ flags)
+                                               int32_t *__restrict__ pos, const uint32_t *__restrict__ flags)
 {
     nnz = rows_nnz(flags, nnz);
     const int64_t base = csr_base(row_ptr, nnz);
@@ -242,15 +241,18 @@ __global__ __launch_bounds__(256) void k_place(const int32_t *__restrict__ row_p
         const int64_t ps = (int64_t)(at >> 32), pi = (int64_t)(at & 0xFFFFFFFFull);
         inv[s] = ps < N ? (int32_t)ps : -1;
         if (ps >= N) continue;
-        prp[ps] = (int32_t)(pi < nnz ? pi : nnz);
-        psrc[ps] = (int32_t)clamp64((int64_t)row_ptr[s] - base, 0, nnz);
+        // one 8-byte word per sample: a scattered write costs a whole memory burst either way
+        reinterpret_cast<int2 *>(pos)[ps] =
+            make_int2((int32_t)(pi < nnz ? pi : nnz), (int32_t)clamp64((int64_t)row_ptr[s] - base, 0, nnz));
     }
 }
 
 // ------------------------------------------------------------------ plan
 
 constexpr int kPlanWaves = 4;
-constexpr int kPlanStage = 1024;  // ids staged in LDS per wave (16 KiB a workgroup: 2048 halves the workgroups a CU holds and costs 5% at 64x64)
+// ids staged in LDS per wave: 16 KiB a workgroup (2048 would halve the workgroups a CU
+// holds, 5% slower on the 64x64 workload)
+constexpr int kPlanStage = 1024;
 
 // A wave plans 64/TA consecutive tiles at once (TA = 2 ... 32): lane l works on row s = l % TA of
 // tile l / TA. Each step takes, per tile, the smallest current id over its TA
@@ -261,18 +263,20 @@ constexpr int kPlanStage = 1024;  // ids staged in LDS per wave (16 KiB a workgr
 // writes more entries than its own CSR span, so no input can drive an access out
 // of bounds.
 //
-// Regrouped batch (psrc non-null): off (the regrouped row offsets, prp) places every
-// tile's entries and gives each position's row length; the row's ids start at
-// psrc[p] in the caller's col_idx (past src_ptr[0]), clamped to the batch. Otherwise
-// off is the caller's row_ptr and positions are samples.
+// Offsets are read os words apart: off[p * os]. Regrouped batch (psrc non-null, os = 2):
+// off (the regrouped row offsets) places every tile's entries and gives each position's
+// row length; the row's ids start at psrc[p * os] in the caller's col_idx (past
+// src_ptr[0]), clamped to the batch. Otherwise off is the caller's row_ptr (os = 1) and
+// positions are samples.
 //
 // Real-valued rows (REAL, values given): every union entry also gets the TA values of
 // its samples (vals[entry*TA + s], written for the samples whose mask bit is set;
 // the other slots are never read), and every row the fp64 sum of its squared
 // values in its own order (xsq, by batch position), which is ||x||^2.
 template <int TA, bool REAL>
-__global__ __launch_bounds__(256) void k_plan(const int32_t *__restrict__ off, const int32_t *__restrict__ src_ptr,
-                                              const int32_t *__restrict__ psrc, const int32_t *__restrict__ col_idx,
+__global__ __launch_bounds__(256) void k_plan(const int32_t *__restrict__ off, int os,
+                                              const int32_t *__restrict__ src_ptr, const int32_t *__restrict__ psrc,
+                                              const int32_t *__restrict__ col_idx,
                                               int64_t N, int64_t nnz, int32_t V, int64_t n_tiles,
                                               uint2 *__restrict__ plan, int2 *__restrict__ tiles,
                                               uint32_t *__restrict__ flags, const float *__restrict__ values,
@@ -297,19 +301,19 @@ __global__ __launch_bounds__(256) void k_plan(const int32_t *__restrict__ off, c
         int64_t wlo = 0, whi = 0;
         if (tw < n_tiles) {
             const int64_t te = tw + G < n_tiles ? tw + G : n_tiles;
-            wlo = clamp64((int64_t)off[tw * TA] - base, 0, nnz);
-            whi = clamp64((int64_t)off[te * TA < N ? te * TA : N] - base, wlo, nnz);
+            wlo = clamp64((int64_t)off[tw * TA * os] - base, 0, nnz);
+            whi = clamp64((int64_t)off[(te * TA < N ? te * TA : N) * os] - base, wlo, nnz);
         }
         int64_t lo = 0, hi = 0, b = 0, e = 0;
         int64_t src = 0;  // where the lane's ids start in col_idx (past its base)
         if (live) {
             const int64_t s0 = t * TA;
             const int64_t s1 = s0 + TA < N ? s0 + TA : N;
-            lo = clamp64((int64_t)off[s0] - base, wlo, whi);
-            hi = clamp64((int64_t)off[s1] - base, lo, whi);
+            lo = clamp64((int64_t)off[s0 * os] - base, wlo, whi);
+            hi = clamp64((int64_t)off[s1 * os] - base, lo, whi);
             if (s0 + sl < N) {
-                const int64_t rb = (int64_t)off[s0 + sl] - base;
-                const int64_t re = (int64_t)off[s0 + sl + 1] - base;
+                const int64_t rb = (int64_t)off[(s0 + sl) * os] - base;
+                const int64_t re = (int64_t)off[(s0 + sl + 1) * os] - base;
                 if (re < rb || rb < lo || re > hi) bad |= SOM_FLAG_ROW_PTR;
                 b = clamp64(rb, lo, hi);
                 e = clamp64(re, b, hi);
@@ -317,7 +321,7 @@ __global__ __launch_bounds__(256) void k_plan(const int32_t *__restrict__ off, c
                 if (psrc) {
                     // the caller's row at this position (its flags were set by the regrouping),
                     // never reaching past the batch
-                    src = clamp64(psrc[s0 + sl], 0, nnz);
+                    src = clamp64(psrc[(s0 + sl) * os], 0, nnz);
                     if (nnz - src < e - b) e = b + (nnz - src);
                 }
             }
@@ -436,7 +440,7 @@ constexpr int kFinalizeBatch = 8;   // strips whose keys one lane loads at once
 constexpr int kFinalize2Batch = 4;  // the same for the two-best search (four words per strip)
 
 __global__ __launch_bounds__(256) void k_finalize(const double *__restrict__ norms, int64_t M,
-                                                  const int32_t *__restrict__ row_ptr, int64_t N, int64_t nnz,
+                                                  const int32_t *__restrict__ row_ptr, int rs, int64_t N, int64_t nnz,
                                                   const double *__restrict__ xsq,
                                                   const u64 *__restrict__ keys,
                                                   const float *__restrict__ dots, int64_t n_strips,
@@ -460,8 +464,8 @@ __global__ __launch_bounds__(256) void k_finalize(const double *__restrict__ nor
         }
         int64_t b = (int64_t)(best & kIndexMask);
         if (b >= M) b = M - 1;
-        const int64_t rb = clamp64((int64_t)row_ptr[k] - base, 0, nnz);
-        const int64_t re = clamp64((int64_t)row_ptr[k + 1] - base, rb, nnz);
+        const int64_t rb = clamp64((int64_t)row_ptr[k * rs] - base, 0, nnz);
+        const int64_t re = clamp64((int64_t)row_ptr[(k + 1) * rs] - base, rb, nnz);
         out.put(k, (int32_t)b, fma(-2.0, (double)dots[gb * N + k], norms[b]) + (xsq ? xsq[k] : (double)(re - rb)));
     }
 }
@@ -470,7 +474,7 @@ __global__ __launch_bounds__(256) void k_finalize(const double *__restrict__ nor
 // strip's two smallest), with their dot products from the sweep. Without a second
 // unit (M == 1) bmu2 = -1 and dist2 = +inf.
 __global__ __launch_bounds__(256) void k_finalize2(const double *__restrict__ norms, int64_t M,
-                                                   const int32_t *__restrict__ row_ptr, int64_t N, int64_t nnz,
+                                                   const int32_t *__restrict__ row_ptr, int rs, int64_t N, int64_t nnz,
                                                    const double *__restrict__ xsq,
                                                    const u64 *__restrict__ keys,
                                                    const float *__restrict__ dots, const u64 *__restrict__ keys2,
@@ -511,8 +515,8 @@ __global__ __launch_bounds__(256) void k_finalize2(const double *__restrict__ no
                 offer(k2[j], d2[j]);
             }
         }
-        const int64_t rb = clamp64((int64_t)row_ptr[k] - base, 0, nnz);
-        const int64_t re = clamp64((int64_t)row_ptr[k + 1] - base, rb, nnz);
+        const int64_t rb = clamp64((int64_t)row_ptr[k * rs] - base, 0, nnz);
+        const int64_t re = clamp64((int64_t)row_ptr[(k + 1) * rs] - base, rb, nnz);
         const double len = xsq ? xsq[k] : (double)(re - rb);
         int64_t i1 = (int64_t)(b1 & kIndexMask);
         if (i1 >= M) i1 = M - 1;
@@ -600,26 +604,28 @@ hipError_t launch_plan(int ta, const int32_t *row_ptr, const int32_t *col_idx, c
     if (blocks > (1 << 22)) blocks = 1 << 22;
     const dim3 grid((unsigned)blocks), block(256);
     const int32_t v = (int32_t)V;
-    const int32_t *off = ob ? ob->prp : row_ptr;
-    const int32_t *psrc = ob ? ob->psrc : nullptr;
+    // a regrouped batch's offsets and sources are interleaved in ob->pos
+    const int32_t *off = ob ? ob->pos : row_ptr;
+    const int32_t *psrc = ob ? ob->pos + 1 : nullptr;
+    const int os = ob ? 2 : 1;
     if (values) {  // real-valued rows: tiles of 8 only
         if (ta != 8) return hipErrorInvalidValue;
-        hipLaunchKernelGGL((k_plan<8, true>), grid, block, 0, st, off, row_ptr, psrc, col_idx, N, nnz, v, nt, plan,
-                           tiles, flags, values, vals, xsq);
+        hipLaunchKernelGGL((k_plan<8, true>), grid, block, 0, st, off, os, row_ptr, psrc, col_idx, N, nnz, v, nt,
+                           plan, tiles, flags, values, vals, xsq);
         return hipGetLastError();
     }
     switch (ta) {
     case 8:
-        hipLaunchKernelGGL((k_plan<8, false>), grid, block, 0, st, off, row_ptr, psrc, col_idx, N, nnz, v, nt, plan,
-                           tiles, flags, nullptr, nullptr, nullptr);
+        hipLaunchKernelGGL((k_plan<8, false>), grid, block, 0, st, off, os, row_ptr, psrc, col_idx, N, nnz, v, nt,
+                           plan, tiles, flags, nullptr, nullptr, nullptr);
         break;
     case 16:
-        hipLaunchKernelGGL((k_plan<16, false>), grid, block, 0, st, off, row_ptr, psrc, col_idx, N, nnz, v, nt, plan,
-                           tiles, flags, nullptr, nullptr, nullptr);
+        hipLaunchKernelGGL((k_plan<16, false>), grid, block, 0, st, off, os, row_ptr, psrc, col_idx, N, nnz, v, nt,
+                           plan, tiles, flags, nullptr, nullptr, nullptr);
         break;
     case 32:
-        hipLaunchKernelGGL((k_plan<32, false>), grid, block, 0, st, off, row_ptr, psrc, col_idx, N, nnz, v, nt, plan,
-                           tiles, flags, nullptr, nullptr, nullptr);
+        hipLaunchKernelGGL((k_plan<32, false>), grid, block, 0, st, off, os, row_ptr, psrc, col_idx, N, nnz, v, nt,
+                           plan, tiles, flags, nullptr, nullptr, nullptr);
         break;
     default: return hipErrorInvalidValue;
     }
@@ -632,13 +638,16 @@ hipError_t launch_finalize(int ta, const double *norms, int64_t M, const int32_t
 {
     int64_t blocks = (N + 255) / 256;
     if (blocks > (1 << 22)) blocks = 1 << 22;
-    // a regrouped batch is finalized by position into the workspace first
+    // a regrouped batch is finalized by position into the workspace first, with its row
+    // lengths from the interleaved offsets of its positions
     const FinalOut o1{bmu, dist, ob ? ob->res : nullptr}, o2{bmu2, dist2, ob ? ob->res2 : nullptr};
+    const int32_t *rp = ob ? ob->pos : row_ptr;
+    const int rs = ob ? 2 : 1;
     if (bmu2)
-        hipLaunchKernelGGL(k_finalize2, dim3((unsigned)blocks), dim3(256), 0, st, norms, M, row_ptr, N, nnz, xsq,
+        hipLaunchKernelGGL(k_finalize2, dim3((unsigned)blocks), dim3(256), 0, st, norms, M, rp, rs, N, nnz, xsq,
                            o.keys, o.dots, o.keys2, o.dots2, n_strips(M, ta), o1, o2);
     else
-        hipLaunchKernelGGL(k_finalize, dim3((unsigned)blocks), dim3(256), 0, st, norms, M, row_ptr, N, nnz, xsq,
+        hipLaunchKernelGGL(k_finalize, dim3((unsigned)blocks), dim3(256), 0, st, norms, M, rp, rs, N, nnz, xsq,
                            o.keys, o.dots, n_strips(M, ta), o1);
     if (ob)
         hipLaunchKernelGGL(k_unpermute, dim3((unsigned)blocks), dim3(256), 0, st, ob->inv, N, ob->res,
@@ -664,11 +673,11 @@ hipError_t launch_order(const int32_t *row_ptr, const int32_t *col_idx, int64_t 
     if (qb > (1 << 22)) qb = 1 << 22;
     hipLaunchKernelGGL(k_rarest, dim3((unsigned)qb), dim3(256), 0, st, row_ptr, col_idx, N, nnz, (int32_t)V, ob.freq,
                        ob.skey, ob.bucket, ob.rank, flags);
-    hipLaunchKernelGGL(k_bucket_scan, dim3(1), dim3(1024), 0, st, ob.bucket, nb, nnz, ob.prp + N);
+    hipLaunchKernelGGL(k_bucket_scan, dim3(1), dim3(1024), 0, st, ob.bucket, nb, nnz, ob.pos + 2 * N);
     int64_t pb = (N + 255) / 256;
     if (pb > (1 << 22)) pb = 1 << 22;
     hipLaunchKernelGGL(k_place, dim3((unsigned)pb), dim3(256), 0, st, row_ptr, N, nnz, ob.skey, ob.bucket, ob.rank, nb,
-                       ob.inv, ob.prp, ob.psrc, flags);
+                       ob.inv, ob.pos, flags);
     return hipGetLastError();
 }
 

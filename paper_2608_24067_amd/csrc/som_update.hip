@@ -25,8 +25,9 @@
 //      counted separately in whole numbers (k_support) and decides the rule.
 // A lane owns one lattice line (row or column) of one field and runs its three
 // passes in one sweep of the line, each pass exactly in the order above, so the
-// result is the same bits on every run; the blurred field replaces the counts. The quotient is fused with the one transpose, from the
-// unit-major fields to the feature-major codebook. Features are processed in
+// result is the same bits on every run; the blurred field replaces the counts.
+// The quotient is fused with the one transpose, from the unit-major fields to the
+// feature-major codebook. Features are processed in
 // chunks, so the workspace holds three fields of chunk * M values rather than V * M.
 
 #include <climits>
