@@ -44,6 +44,9 @@ def gpu_update(W, rp, ci, bmu, E, r, dev, chunk=0):
     (96, 5000, 2000, 32, 16, 0, 1.0),
     (97, 1, 30, 5, 3, 0, 1.0),         # one sample
     (98, 400, 64, 1, 1, 0, 1.0),       # a one-unit map
+    (109, 800, 50, 6, 9, 0, 1.0),      # radius beyond the lattice: every window is the whole line
+    (110, 600, 40, 8, 7, 3, 1.0),      # radius E - 1
+    (111, 3000, 60, 7, 2, 0, 1.0),     # odd lattice, short lines
 ])
 def test_update_bit_exact(dev, seed, N, V, E, r, chunk, spread):
     rp, ci, W, bmu = update_case(seed, N, V, E, spread=spread)
