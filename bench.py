@@ -47,7 +47,7 @@ ALG_TILE = 16  # tile size that defines the algorithmic bytes
 METRIC = "BMU-search samples/sec + effective codebook HBM GB/s (% of peak) per map size"
 # the sources the sweep kernel is compiled from: a counter record is used only while they are unchanged
 SWEEP_SRC = [os.path.join(ROOT, "paper_2608_24067_amd", "csrc", f)
-             for f in ("som_sweep.hip", "som_device.h", "som_tree16.h")]
+             for f in ("som_sweep.hip", "som_device.h", "som_tree16.h", "som_tree8.h")]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 
 

@@ -22,11 +22,20 @@
 
 #include "som_device.h"
 #include "som_tree16.h"
+#include "som_tree8.h"
 
 namespace som {
 namespace {
 
 // ----------------------------------------------------------------- sweep
+
+// fp16 tiles of 8 keep four waves per SIMD (128 registers): the assembly dispatch of
+// their rows would otherwise take 131 and lose a wave.
+template <typename E, int TA, int NPL, bool VEC, bool REAL>
+constexpr int sweep_min_waves()
+{
+    return (sizeof(E) == 2 && TA == 8 && NPL == 8 && VEC && !REAL) ? 4 : 1;
+}
 
 // Workgroup = 4 waves x one strip (blockIdx.y) of 64*NPL neurons, over groups of
 // group_tiles consecutive tiles (a multiple of 4; groups blockIdx.x, blockIdx.x +
@@ -46,12 +55,11 @@ namespace {
 // (one fused multiply-add, fp32) instead of the weight, still in ascending feature
 // order per sample.
 template <typename E, int TA, int NPL, int U, bool VEC, bool TOP2, bool REAL>
-__global__ __launch_bounds__(256) void k_sweep(const E *__restrict__ W, const double *__restrict__ norms,
-                                               int64_t M, int64_t N, int64_t V, int64_t nnz,
-                                               const uint2 *__restrict__ plan, const int2 *__restrict__ tiles,
-                                               int64_t n_tiles, u64 *__restrict__ keys, float *__restrict__ dots,
-                                               u64 *__restrict__ keys2, float *__restrict__ dots2,
-                                               const float *__restrict__ vals, int64_t group_tiles)
+__global__ __launch_bounds__(256, (sweep_min_waves<E, TA, NPL, VEC, REAL>())) void k_sweep(
+    const E *__restrict__ W, const double *__restrict__ norms, int64_t M, int64_t N, int64_t V, int64_t nnz,
+    const uint2 *__restrict__ plan, const int2 *__restrict__ tiles, int64_t n_tiles, u64 *__restrict__ keys,
+    float *__restrict__ dots, u64 *__restrict__ keys2, float *__restrict__ dots2, const float *__restrict__ vals,
+    int64_t group_tiles)
 {
     const int lane = threadIdx.x & 63;
     const int wv = wave_id();
@@ -92,6 +100,11 @@ __global__ __launch_bounds__(256) void k_sweep(const E *__restrict__ W, const do
     // from the lane's own start of the strip (the row pitch is kept in a vector
     // register for that), which leaves the scalar unit to the dispatch.
     constexpr bool T16 = sizeof(E) == 4 && TA == 16 && NPL == 4 && VEC && !REAL;
+    // fp16 tiles of 8 (eight neurons per lane, one packed 16-byte load per row): the same
+    // kind of assembly dispatch (som_tree8.h). Their sweep is bound by instruction issue
+    // (64x64: 112.5 -> 107.2 ms, 1024x1024: 544 -> 525 ms); the fp32 sweep, bound by its
+    // vector-memory path, keeps the C++ dispatch (the block made it 1-4% slower).
+    constexpr bool T8 = sizeof(E) == 2 && TA == 8 && NPL == 8 && VEC && !REAL;
     const char *lrow = nullptr;
     unsigned pitch = 0;
     if constexpr (T16) {
@@ -192,6 +205,10 @@ __global__ __launch_bounds__(256) void k_sweep(const E *__restrict__ W, const do
             if constexpr (T16) {
                 const float w[4] = {seg.v[0][0], seg.v[0][1], seg.v[0][2], seg.v[0][3]};
                 SOM_T16_DISPATCH(acc, w, mask);
+            } else if constexpr (T8) {
+                const unsigned *dw = reinterpret_cast<const unsigned *>(&seg.v[0]);
+                const unsigned d[4] = {dw[0], dw[1], dw[2], dw[3]};
+                SOM_T8_DISPATCH16(acc, d, mask);
             } else if constexpr (sizeof(E) == 2 && VEC) {
                 // Packed fp16: each update is one mixed-precision FMA with h read as a
                 // half straight from the loaded dword (exact widening, one rounding):
