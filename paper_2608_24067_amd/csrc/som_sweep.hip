@@ -29,12 +29,13 @@ namespace {
 
 // ----------------------------------------------------------------- sweep
 
-// fp16 tiles of 8 keep four waves per SIMD (128 registers): the assembly dispatch of
-// their rows would otherwise take 131 and lose a wave.
+// Tiles of 8 with eight neurons per lane keep four waves per SIMD (128 registers): the
+// assembly dispatch of fp16 and real-valued rows would otherwise take up to 133 and
+// lose a wave.
 template <typename E, int TA, int NPL, bool VEC, bool REAL>
 constexpr int sweep_min_waves()
 {
-    return (sizeof(E) == 2 && TA == 8 && NPL == 8 && VEC && !REAL) ? 4 : 1;
+    return (TA == 8 && NPL == 8 && VEC) ? 4 : 1;
 }
 
 // Workgroup = 4 waves x one strip (blockIdx.y) of 64*NPL neurons, over groups of
@@ -100,11 +101,14 @@ __global__ __launch_bounds__(256, (sweep_min_waves<E, TA, NPL, VEC, REAL>())) vo
     // from the lane's own start of the strip (the row pitch is kept in a vector
     // register for that), which leaves the scalar unit to the dispatch.
     constexpr bool T16 = sizeof(E) == 4 && TA == 16 && NPL == 4 && VEC && !REAL;
-    // fp16 tiles of 8 (eight neurons per lane, one packed 16-byte load per row): the same
-    // kind of assembly dispatch (som_tree8.h). Their sweep is bound by instruction issue
-    // (64x64: 112.5 -> 107.2 ms, 1024x1024: 544 -> 525 ms); the fp32 sweep, bound by its
-    // vector-memory path, keeps the C++ dispatch (the block made it 1-4% slower).
+    // fp16 tiles of 8 (eight neurons per lane, one packed 16-byte load per row) and
+    // real-valued tiles of 8: the same kind of assembly dispatch (som_tree8.h). These
+    // sweeps are bound by instruction issue (fp16 64x64: 112.5 -> 107.2 ms, 1024x1024:
+    // 544 -> 525 ms; real-valued rows over fp16 -4 to -5%, over fp32 -1 to -2%); the fp32
+    // sweep of binary rows, bound by its vector-memory path, keeps the C++ dispatch (the
+    // block made it 1-4% slower).
     constexpr bool T8 = sizeof(E) == 2 && TA == 8 && NPL == 8 && VEC && !REAL;
+    constexpr bool T8R = TA == 8 && NPL == 8 && VEC && REAL;
     const char *lrow = nullptr;
     unsigned pitch = 0;
     if constexpr (T16) {
@@ -205,6 +209,14 @@ __global__ __launch_bounds__(256, (sweep_min_waves<E, TA, NPL, VEC, REAL>())) vo
             if constexpr (T16) {
                 const float w[4] = {seg.v[0][0], seg.v[0][1], seg.v[0][2], seg.v[0][3]};
                 SOM_T16_DISPATCH(acc, w, mask);
+            } else if constexpr (T8R && sizeof(E) == 4) {
+                const float w[8] = {seg.v[0][0], seg.v[0][1], seg.v[0][2], seg.v[0][3],
+                                    seg.v[1][0], seg.v[1][1], seg.v[1][2], seg.v[1][3]};
+                SOM_T8_DISPATCH32R(acc, w, xv, mask);
+            } else if constexpr (T8R) {
+                const unsigned *dw = reinterpret_cast<const unsigned *>(&seg.v[0]);
+                const unsigned d[4] = {dw[0], dw[1], dw[2], dw[3]};
+                SOM_T8_DISPATCH16R(acc, d, xv, mask);
             } else if constexpr (T8) {
                 const unsigned *dw = reinterpret_cast<const unsigned *>(&seg.v[0]);
                 const unsigned d[4] = {dw[0], dw[1], dw[2], dw[3]};
