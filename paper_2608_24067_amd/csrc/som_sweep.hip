@@ -109,9 +109,12 @@ __global__ __launch_bounds__(256, (sweep_min_waves<E, TA, NPL, VEC, REAL>())) vo
     // block made it 1-4% slower).
     constexpr bool T8 = sizeof(E) == 2 && TA == 8 && NPL == 8 && VEC && !REAL;
     constexpr bool T8R = TA == 8 && NPL == 8 && VEC && REAL;
+    // One vector load per row and lane (tiles of 16, and fp16 tiles of 8): the row address
+    // is one vector multiply-add from the lane's own strip start (fp16: -1% sweep time).
+    constexpr bool LROW = T16 || (sizeof(E) == 2 && TA == 8 && NPL == 8 && VEC);
     const char *lrow = nullptr;
     unsigned pitch = 0;
-    if constexpr (T16) {
+    if constexpr (LROW) {
         const int g = base + lg;
         lrow = reinterpret_cast<const char *>(W + (g < Mi ? g : Mi - G));
         pitch = (unsigned)Mi * (unsigned)sizeof(E);
@@ -165,7 +168,7 @@ __global__ __launch_bounds__(256, (sweep_min_waves<E, TA, NPL, VEC, REAL>())) vo
         // widened when it is added. Lanes whose group lies past M (last strip only)
         // re-read the row's last group; those neurons are never ranked.
         auto row_load = [&](unsigned id, Seg &seg) {
-            if constexpr (T16) {
+            if constexpr (LROW) {
                 const unsigned idc = id < vmax ? id : vmax;
                 seg.v[0] = *reinterpret_cast<const typename Seg::vec *>(lrow + (uint64_t)idc * pitch);
                 return;
